@@ -1,0 +1,204 @@
+"""CPU oracle for the TASQ masked quantized linear layer.
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and the
+CPU-baseline leg of the benchmark, never by the product path.  It shares no
+code with the HIP library (``paper_2608_03057_amd``) and imports nothing from
+it; the two meet only in the seeded inputs the tests hand to both.
+
+The arithmetic lives in ``tasq_oracle.c`` (plain C, int64 accumulation, fp64
+dequantisation).  This module loads it with ctypes and adds the schedule
+(Sec. 3.2 contiguous stages, Sec. 4.1 step/stage counts), which only loops
+over the C definition.  ``brute.py`` is a second, pure-Python route for tiny
+shapes.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tasq_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+OK, EBITS, EOVERFLOW, EDIM = 0, 1, 2, 3
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP over output rows)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared",
+                               "-Wall", "-Werror", _SRC, "-o", tmp])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        p = ctypes.c_void_p
+        i64 = ctypes.c_int64
+        L.oracle_num_threads.restype = ctypes.c_int
+        L.oracle_mask.argtypes = [p, i64, ctypes.c_int, p]
+        L.oracle_stage_of_step.argtypes = [ctypes.c_int] * 3
+        L.oracle_masked_linear.argtypes = [p, p, ctypes.c_double, p, p, i64, i64, i64,
+                                           ctypes.c_int, p, p]
+        L.oracle_masked_linear_entries.argtypes = [p, p, ctypes.c_double, p, p, i64,
+                                                   ctypes.c_int, p, p, i64, p, p]
+        L.oracle_conv3x3.argtypes = [p, p, ctypes.c_double, p, p, i64, i64, i64, i64,
+                                     ctypes.c_int, p, p]
+        L.oracle_pack_planes.argtypes = [p, i64, i64, p]
+        _lib = L
+    return _lib
+
+
+def _np(a, dtype):
+    """Contiguous numpy view of a numpy array or CPU torch tensor."""
+    if hasattr(a, "detach"):
+        a = a.detach().cpu().numpy()
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def num_threads() -> int:
+    return lib().oracle_num_threads()
+
+
+def mask(W, b: int) -> np.ndarray:
+    """2^k * floor(W / 2^k), k = 8 - b (App. G.2 Eq. hw_rightshift, masked form)."""
+    W = _np(W, np.int8)
+    out = np.empty_like(W)
+    rc = lib().oracle_mask(_ptr(W), W.size, b, _ptr(out))
+    if rc != OK:
+        raise ValueError(f"oracle_mask: b={b} outside [1, 8]")
+    return out
+
+
+def stage_of_step(t: int, S: int, T: int) -> int:
+    """Stage of denoising step t: floor(t*S/T), step 0 the noisiest."""
+    s = lib().oracle_stage_of_step(t, S, T)
+    if s < 0:
+        raise ValueError(f"bad (t, S, T) = {(t, S, T)}")
+    return s
+
+
+def masked_linear(X, W, sx: float, sw, b: int, bias=None):
+    """(acc int32 [M x N], y fp64 [M x N]) of the masked quantized linear."""
+    X = _np(X, np.int8)
+    W = _np(W, np.int8)
+    sw = _np(sw, np.float32)
+    bias = None if bias is None else _np(bias, np.float32)
+    M, K = X.shape
+    N, K2 = W.shape
+    assert K == K2 and sw.shape == (N,)
+    acc = np.empty((M, N), np.int32)
+    y = np.empty((M, N), np.float64)
+    rc = lib().oracle_masked_linear(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias),
+                                    M, N, K, b, _ptr(acc), _ptr(y))
+    if rc == EOVERFLOW:
+        raise OverflowError("accumulator outside int32")
+    if rc != OK:
+        raise ValueError(f"oracle_masked_linear rc={rc}")
+    return acc, y
+
+
+def masked_linear_entries(X, W, sx, sw, b, rows, cols, bias=None):
+    """The (rows[i], cols[i]) outputs only, each computed as one dot product.
+
+    ``X`` is addressed by ``rows`` and ``W`` by ``cols`` (row n of W is output
+    channel n), so callers may pass just the rows of X and W they sample,
+    with ``rows``/``cols`` indexing those arrays, and ``sw``/``bias`` indexed
+    likewise."""
+    X = _np(X, np.int8)
+    W = _np(W, np.int8)
+    sw = _np(sw, np.float32)
+    bias = None if bias is None else _np(bias, np.float32)
+    rows = _np(rows, np.int64)
+    cols = _np(cols, np.int64)
+    K = X.shape[1]
+    assert W.shape[1] == K and rows.shape == cols.shape
+    assert rows.size == 0 or (0 <= rows.min() and rows.max() < X.shape[0])
+    assert cols.size == 0 or (0 <= cols.min() and cols.max() < W.shape[0])
+    acc = np.empty(rows.size, np.int32)
+    y = np.empty(rows.size, np.float64)
+    rc = lib().oracle_masked_linear_entries(_ptr(X), _ptr(W), float(sx), _ptr(sw),
+                                            _ptr(bias), K, b, _ptr(rows), _ptr(cols),
+                                            rows.size, _ptr(acc), _ptr(y))
+    if rc == EOVERFLOW:
+        raise OverflowError("accumulator outside int32")
+    if rc != OK:
+        raise ValueError(f"oracle_masked_linear_entries rc={rc}")
+    return acc, y
+
+
+def conv3x3(X, Wt, sx: float, sw, b: int, bias=None):
+    """Direct 3x3 / stride 1 / pad 1 NHWC convolution with the masked weight.
+
+    X int8 [H x Wd x Ci], Wt int8 [Co x 3 x 3 x Ci]; returns acc int32 and
+    y fp64, both [H x Wd x Co]."""
+    X = _np(X, np.int8)
+    Wt = _np(Wt, np.int8)
+    sw = _np(sw, np.float32)
+    bias = None if bias is None else _np(bias, np.float32)
+    H, Wd, Ci = X.shape
+    Co = Wt.shape[0]
+    assert Wt.shape == (Co, 3, 3, Ci) and sw.shape == (Co,)
+    acc = np.empty((H, Wd, Co), np.int32)
+    y = np.empty((H, Wd, Co), np.float64)
+    rc = lib().oracle_conv3x3(_ptr(X), _ptr(Wt), float(sx), _ptr(sw), _ptr(bias),
+                              H, Wd, Ci, Co, b, _ptr(acc), _ptr(y))
+    if rc == EOVERFLOW:
+        raise OverflowError("accumulator outside int32")
+    if rc != OK:
+        raise ValueError(f"oracle_conv3x3 rc={rc}")
+    return acc, y
+
+
+def pack_planes(W) -> np.ndarray:
+    """uint32 [8 x N x ceil(K/32)] bit planes, most significant plane first."""
+    W = _np(W, np.int8)
+    N, K = W.shape
+    KW = (K + 31) // 32
+    planes = np.empty((8, N, KW), np.uint32)
+    lib().oracle_pack_planes(_ptr(W), N, K, _ptr(planes))
+    return planes
+
+
+def run_schedule(layers, table, S: int, T: int, t_begin: int, t_end: int, sx: float):
+    """Buffers left by running denoising steps t_begin..t_end-1 of a schedule.
+
+    ``layers`` is a list of dicts with keys X, W, sw, bias (optional) and
+    kind ("linear" or "conv3x3").  Each step t computes every layer at
+    b = table[l][stage(t)] and overwrites that layer's output buffers
+    (Sec. 3.2: one mask per layer and stage).  Returns, per layer, the last
+    (acc, y, b) written, or None if the range is empty (buffers untouched).
+    Literal loop over steps: meant for small shapes.
+    """
+    if not (0 <= t_begin <= t_end <= T):
+        raise ValueError("bad step range")
+    out = [None] * len(layers)
+    for t in range(t_begin, t_end):
+        s = stage_of_step(t, S, T)
+        for l, layer in enumerate(layers):
+            b = int(table[l][s])
+            if layer.get("kind", "linear") == "conv3x3":
+                acc, y = conv3x3(layer["X"], layer["W"], sx, layer["sw"], b,
+                                 layer.get("bias"))
+            else:
+                acc, y = masked_linear(layer["X"], layer["W"], sx, layer["sw"], b,
+                                       layer.get("bias"))
+            out[l] = (acc, y, b)
+    return out

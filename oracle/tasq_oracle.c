@@ -1,0 +1,227 @@
+/*
+ * CPU oracle for the TASQ masked quantized linear layer.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark do.  It shares no code, header, table or helper with
+ * the HIP library.
+ *
+ * Every function is the plain definition written out, with no blocking,
+ * fusion or reordering: integer products are accumulated in int64 in
+ * ascending k, floating point is fp64.  Rows of the output are distributed
+ * over OpenMP threads, which changes no arithmetic.
+ *
+ * Definitions followed (TASQ, arxiv 2608.03057):
+ *  - truncation-consistent quantizer, Sec. 3.1 Eq. (truncquant): a lower
+ *    precision code is the floor of the higher one divided by two;
+ *  - k-bit generalisation, App. G.2 Eqs. (hw_rightshift, hw_multi_lsb): the
+ *    b-bit operand is floor(Q / 2^k), k = B - b, i.e. the top b bit planes;
+ *  - LSB mask, Sec. 3.2.1 Eq. (lsb_masking): the masked weight keeps the
+ *    stored n-bit scale, so the operand the layer multiplies is
+ *    2^k * floor(Q / 2^k);
+ *  - quantized linear, Sec. 3.1 Eq. (qalora): Y = Q(X) Q(W);
+ *  - dequantisation, App. A.1.1-A.1.2: a product of per-tensor activation and
+ *    per-output-channel weight scales (the 2^n/(2^n-1) weight factor folded
+ *    into the channel scale, zero points zero);
+ *  - stages, Sec. 3.2 (contiguous stages) and Sec. 4.1 (20 steps in four
+ *    stages; four steps, one per stage), stage 0 the noisiest (App. D.1).
+ *
+ * Parity pins: every function here is checked by the CPU test suite against
+ * an independent route (the paper's unsigned-code form of the mask applied
+ * one bit at a time, a bitwise mask, hand-derived worked values, numpy's
+ * int64 matmul at b = 8, an im2col convolution, a pure-Python brute force,
+ * and the bit-plane identity).  No function is parity-unpinned.
+ */
+#include <stdint.h>
+#include <stddef.h>
+#include <stdlib.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { ORACLE_OK = 0, ORACLE_EBITS = 1, ORACLE_EOVERFLOW = 2, ORACLE_EDIM = 3 };
+
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* floor(w / 2^k) toward minus infinity, by integer division and correction. */
+static int64_t floor_div_pow2(int64_t w, int k)
+{
+    int64_t d = (int64_t)1 << k;
+    int64_t q = w / d;              /* C truncates toward zero */
+    if (w % d != 0 && w < 0)
+        q -= 1;
+    return q;
+}
+
+/* The masked operand: 2^k * floor(w / 2^k) with k = 8 - b. */
+static int64_t masked_value(int64_t w, int b)
+{
+    int k = 8 - b;
+    return ((int64_t)1 << k) * floor_div_pow2(w, k);
+}
+
+/* The operand at precision b (App. G.2 Eq. hw_rightshift), in the masked
+ * form that keeps the stored scale (Sec. 3.2.1 Eq. lsb_masking). */
+int oracle_mask(const int8_t *W, int64_t n, int b, int8_t *out)
+{
+    if (b < 1 || b > 8)
+        return ORACLE_EBITS;
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = (int8_t)masked_value(W[i], b);
+    return ORACLE_OK;
+}
+
+/* Sec. 3.2 / Sec. 4.1: equal contiguous stages, s = floor(t * S / T). */
+int oracle_stage_of_step(int t, int S, int T)
+{
+    if (S < 1 || T < 1 || S > T || t < 0 || t >= T)
+        return -1;
+    return (int)(((int64_t)t * S) / T);
+}
+
+/*
+ * acc[m][n] = sum_k X[m][k] * (2^(8-b) * floor(W[n][k] / 2^(8-b)))
+ * y[m][n]   = acc[m][n] * sx * sw[n] (+ bias[n])         (fp64)
+ *
+ * X int8 [M][K], W int8 [N][K] (output x input), acc int32 [M][N],
+ * y fp64 [M][N]; bias may be NULL; acc or y may be NULL.
+ * Returns ORACLE_EOVERFLOW if any |acc| >= 2^31 (acc then holds garbage).
+ */
+int oracle_masked_linear(const int8_t *X, const int8_t *W, double sx, const float *sw,
+                         const float *bias, int64_t M, int64_t N, int64_t K, int b,
+                         int32_t *acc, double *y)
+{
+    if (b < 1 || b > 8)
+        return ORACLE_EBITS;
+    if (M < 0 || N < 0 || K < 0)
+        return ORACLE_EDIM;
+    int overflow = 0;
+#pragma omp parallel for schedule(static) reduction(| : overflow)
+    for (int64_t m = 0; m < M; ++m) {
+        for (int64_t n = 0; n < N; ++n) {
+            int64_t s = 0;
+            for (int64_t k = 0; k < K; ++k)
+                s += (int64_t)X[m * K + k] * masked_value(W[n * K + k], b);
+            if (s >= ((int64_t)1 << 31) || s < -((int64_t)1 << 31))
+                overflow = 1;
+            if (acc)
+                acc[m * N + n] = (int32_t)s;
+            if (y) {
+                double v = (double)s * sx * (double)sw[n];
+                if (bias)
+                    v += (double)bias[n];
+                y[m * N + n] = v;
+            }
+        }
+    }
+    return overflow ? ORACLE_EOVERFLOW : ORACLE_OK;
+}
+
+/*
+ * Entries (rows[i], cols[i]) of the same product, one dot product each, for
+ * sampled checks of outputs too large to recompute whole.  X is given as the
+ * full [M][K] array or any [R][K] array addressed by rows[].
+ */
+int oracle_masked_linear_entries(const int8_t *X, const int8_t *W, double sx,
+                                 const float *sw, const float *bias, int64_t K, int b,
+                                 const int64_t *rows, const int64_t *cols, int64_t count,
+                                 int32_t *acc, double *y)
+{
+    if (b < 1 || b > 8)
+        return ORACLE_EBITS;
+    int overflow = 0;
+#pragma omp parallel for schedule(static) reduction(| : overflow)
+    for (int64_t i = 0; i < count; ++i) {
+        int64_t m = rows[i], n = cols[i];
+        int64_t s = 0;
+        for (int64_t k = 0; k < K; ++k)
+            s += (int64_t)X[m * K + k] * masked_value(W[n * K + k], b);
+        if (s >= ((int64_t)1 << 31) || s < -((int64_t)1 << 31))
+            overflow = 1;
+        acc[i] = (int32_t)s;
+        double v = (double)s * sx * (double)sw[n];
+        if (bias)
+            v += (double)bias[n];
+        y[i] = v;
+    }
+    return overflow ? ORACLE_EOVERFLOW : ORACLE_OK;
+}
+
+/*
+ * Direct 3x3 convolution, stride 1, zero padding 1, NHWC, batch 1:
+ * acc[h][w][co] = sum_{r,s,ci} X[h+r-1][w+s-1][ci] * Wb[co][r][s][ci].
+ * Written as the convolution sum, not as a matrix product, so that the
+ * (r, s, ci) ordering of a kernel's implicit GEMM is checked independently.
+ */
+int oracle_conv3x3(const int8_t *X, const int8_t *Wt, double sx, const float *sw,
+                   const float *bias, int64_t H, int64_t Wd, int64_t Ci, int64_t Co, int b,
+                   int32_t *acc, double *y)
+{
+    if (b < 1 || b > 8)
+        return ORACLE_EBITS;
+    int overflow = 0;
+#pragma omp parallel for schedule(static) reduction(| : overflow)
+    for (int64_t h = 0; h < H; ++h) {
+        for (int64_t w = 0; w < Wd; ++w) {
+            for (int64_t co = 0; co < Co; ++co) {
+                int64_t s = 0;
+                for (int64_t r = 0; r < 3; ++r) {
+                    int64_t hh = h + r - 1;
+                    if (hh < 0 || hh >= H)
+                        continue;
+                    for (int64_t q = 0; q < 3; ++q) {
+                        int64_t ww = w + q - 1;
+                        if (ww < 0 || ww >= Wd)
+                            continue;
+                        const int8_t *xp = X + (hh * Wd + ww) * Ci;
+                        const int8_t *wp = Wt + ((co * 3 + r) * 3 + q) * Ci;
+                        for (int64_t ci = 0; ci < Ci; ++ci)
+                            s += (int64_t)xp[ci] * masked_value(wp[ci], b);
+                    }
+                }
+                if (s >= ((int64_t)1 << 31) || s < -((int64_t)1 << 31))
+                    overflow = 1;
+                int64_t o = (h * Wd + w) * Co + co;
+                if (acc)
+                    acc[o] = (int32_t)s;
+                if (y) {
+                    double v = (double)s * sx * (double)sw[co];
+                    if (bias)
+                        v += (double)bias[co];
+                    y[o] = v;
+                }
+            }
+        }
+    }
+    return overflow ? ORACLE_EOVERFLOW : ORACLE_OK;
+}
+
+/*
+ * Bit planes of the stored two's-complement weight (App. G.2: plane p is
+ * bit p of the code, p = 0 the least significant).  Layout
+ * planes[q][n][j / 32], bit (j % 32), with q = 7 - p (most significant plane
+ * first, so the top b planes are one contiguous prefix); words past K are
+ * zero.  KW = ceil(K / 32).
+ */
+int oracle_pack_planes(const int8_t *W, int64_t N, int64_t K, uint32_t *planes)
+{
+    int64_t KW = (K + 31) / 32;
+    for (int64_t i = 0; i < 8 * N * KW; ++i)
+        planes[i] = 0;
+    for (int q = 0; q < 8; ++q) {
+        int p = 7 - q;
+        for (int64_t n = 0; n < N; ++n)
+            for (int64_t j = 0; j < K; ++j) {
+                uint32_t bit = ((uint32_t)(uint8_t)W[n * K + j] >> p) & 1u;
+                planes[(q * N + n) * KW + j / 32] |= bit << (j % 32);
+            }
+    }
+    return ORACLE_OK;
+}

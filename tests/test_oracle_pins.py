@@ -1,0 +1,361 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Each test checks the oracle through a route that does not retype its own
+formula: the paper's unsigned-code mask applied bit by bit (brute.py), a
+bitwise mask, hand-worked values, numpy's int64 matmul, an im2col
+convolution, the bit-plane identity, exact rational dequantisation, and
+properties any correct mask must have.
+"""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import brute
+from conftest import read_golden
+
+from paper_2608_03057_amd import inputs
+
+RNG = np.random.default_rng(12345)
+ALL_W = np.arange(-128, 128, dtype=np.int64)
+
+
+def rand_i8(shape, rng=RNG):
+    return rng.integers(-128, 128, size=shape, dtype=np.int64).astype(np.int8)
+
+
+# ------------------------------------------------------------------ the mask
+
+@pytest.mark.parametrize("b", range(1, 9))
+def test_mask_exhaustive_vs_unsigned_codes(b):
+    """Sec. 3.1 Eq. truncquant + Sec. 3.2.1 Eqs. lsb_extraction/lsb_masking
+    on the unsigned code Q = w + 128, one bit at a time, for every w."""
+    got = oracle.mask(ALL_W.astype(np.int8), b).astype(np.int64)
+    want = np.array([brute.masked_weight(int(w), b) for w in ALL_W])
+    np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("b", range(1, 9))
+def test_mask_exhaustive_vs_bitwise_and(b):
+    """Dropping the k low two's-complement bits is an AND with ~(2^k - 1)."""
+    k = 8 - b
+    got = oracle.mask(ALL_W.astype(np.int8), b)
+    want = (ALL_W & ~((1 << k) - 1)).astype(np.int8)
+    np.testing.assert_array_equal(got, want)
+
+
+def test_mask_worked_values():
+    rows = read_golden("mask_worked_values.txt")
+    assert len(rows) >= 10
+    for w, b, wb in rows:
+        assert int(oracle.mask(np.array([w], np.int8), b)[0]) == wb, (w, b)
+        assert brute.masked_weight(w, b) == wb, (w, b)
+
+
+def test_mask_properties():
+    W = ALL_W.astype(np.int8)
+    for b in range(1, 9):
+        k = 8 - b
+        Wb = oracle.mask(W, b).astype(np.int64)
+        # idempotent
+        np.testing.assert_array_equal(oracle.mask(Wb.astype(np.int8), b), Wb)
+        # bounded: 0 <= W - W_b <= 2^k - 1
+        d = ALL_W - Wb
+        assert d.min() >= 0 and d.max() <= (1 << k) - 1
+        # App. G.2 Eq. hw_multi_lsb: the dropped block is sum_{p<k} 2^p bit_p(W)
+        u = ALL_W & 0xFF
+        lsb = sum(((u >> p) & 1) << p for p in range(k)) if k else 0
+        np.testing.assert_array_equal(d, lsb)
+        # the result has no bit set below position k
+        assert np.all((Wb & ((1 << k) - 1)) == 0)
+        # nested / monotone in b
+        for b2 in range(1, b + 1):
+            Wb2 = oracle.mask(W, b2).astype(np.int64)
+            np.testing.assert_array_equal(oracle.mask(Wb.astype(np.int8), b2), Wb2)
+            assert np.all(Wb2 <= Wb) and np.all(Wb <= ALL_W)
+    # b = 8 is the identity; b = 1 keeps only the sign plane
+    np.testing.assert_array_equal(oracle.mask(W, 8), W)
+    assert set(oracle.mask(W, 1).tolist()) == {-128, 0}
+
+
+@pytest.mark.parametrize("b", [0, 9, -1, 100])
+def test_mask_rejects_bits_outside_1_8(b):
+    with pytest.raises(ValueError):
+        oracle.mask(np.zeros(4, np.int8), b)
+
+
+# --------------------------------------------------------------- the product
+
+@pytest.mark.parametrize("M,N,K", [(1, 1, 1), (3, 5, 7), (17, 33, 64), (40, 24, 1153)])
+def test_b8_equals_numpy_int64_matmul(M, N, K):
+    X, W = rand_i8((M, K)), rand_i8((N, K))
+    acc, _ = oracle.masked_linear(X, W, 1.0, np.ones(N, np.float32), 8)
+    np.testing.assert_array_equal(acc, X.astype(np.int64) @ W.astype(np.int64).T)
+
+
+@pytest.mark.parametrize("b", range(1, 9))
+def test_masked_product_linearity(b):
+    """acc(X, W_b) = X W^T - X (W - W_b)^T, with W_b from a bitwise mask."""
+    M, N, K = 9, 13, 301
+    X, W = rand_i8((M, K)), rand_i8((N, K))
+    k = 8 - b
+    dropped = W.astype(np.int64) & ((1 << k) - 1)
+    want = X.astype(np.int64) @ W.astype(np.int64).T - X.astype(np.int64) @ dropped.T
+    acc, _ = oracle.masked_linear(X, W, 1.0, np.ones(N, np.float32), b)
+    np.testing.assert_array_equal(acc, want)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_brute_force_agreement(seed):
+    rng = np.random.default_rng(seed)
+    M, N, K = (int(v) for v in rng.integers(1, 17, size=3))
+    X, W = rand_i8((M, K), rng), rand_i8((N, K), rng)
+    X[0, 0] = -128
+    W[0, 0] = -128
+    sw = rng.uniform(1e-3, 1e-2, size=N).astype(np.float32)
+    bias = rng.uniform(-1, 1, size=N).astype(np.float32)
+    for b in range(1, 9):
+        acc, y = oracle.masked_linear(X, W, 0.02, sw, b, bias)
+        bacc, by = brute.masked_linear(X.tolist(), W.tolist(), 0.02, sw.tolist(), b,
+                                       bias.tolist())
+        np.testing.assert_array_equal(acc, np.array(bacc))
+        np.testing.assert_allclose(y, np.array(by), rtol=1e-14, atol=1e-14)
+
+
+def test_special_cases():
+    N, K = 7, 40
+    W = rand_i8((N, K))
+    sw = np.ones(N, np.float32)
+    for b in range(1, 9):
+        acc, _ = oracle.masked_linear(np.zeros((3, K), np.int8), W, 1.0, sw, b)
+        assert not acc.any()
+        # a one-hot activation row returns the masked weight column
+        for j in (0, 17, K - 1):
+            x = np.zeros((1, K), np.int8)
+            x[0, j] = 1
+            acc, _ = oracle.masked_linear(x, W, 1.0, sw, b)
+            want = np.array([brute.masked_weight(int(W[n, j]), b) for n in range(N)])
+            np.testing.assert_array_equal(acc[0], want)
+
+
+def test_empty_shapes():
+    acc, y = oracle.masked_linear(np.zeros((0, 5), np.int8), np.zeros((3, 5), np.int8),
+                                  1.0, np.ones(3, np.float32), 4)
+    assert acc.shape == (0, 3)
+    acc, y = oracle.masked_linear(np.zeros((2, 0), np.int8), np.zeros((3, 0), np.int8),
+                                  1.0, np.ones(3, np.float32), 4)
+    assert not acc.any() and not y.any()
+
+
+def test_overflow_bound():
+    """|acc| <= 128 * 128 * K: K = 131071 fits int32, K = 131072 does not."""
+    for K, ok in ((131071, True), (131072, False)):
+        X = np.full((1, K), -128, np.int8)
+        W = np.full((1, K), -128, np.int8)
+        if ok:
+            acc, _ = oracle.masked_linear(X, W, 1.0, np.ones(1, np.float32), 8)
+            assert int(acc[0, 0]) == 16384 * K
+        else:
+            with pytest.raises(OverflowError):
+                oracle.masked_linear(X, W, 1.0, np.ones(1, np.float32), 8)
+
+
+def test_entries_match_full():
+    M, N, K = 20, 30, 77
+    X, W = rand_i8((M, K)), rand_i8((N, K))
+    sw = RNG.uniform(1e-3, 1e-2, size=N).astype(np.float32)
+    bias = RNG.uniform(-1, 1, size=N).astype(np.float32)
+    rows = RNG.integers(0, M, 50)
+    cols = RNG.integers(0, N, 50)
+    for b in (8, 5, 1):
+        acc, y = oracle.masked_linear(X, W, 0.02, sw, b, bias)
+        ea, ey = oracle.masked_linear_entries(X, W, 0.02, sw, b, rows, cols, bias)
+        np.testing.assert_array_equal(ea, acc[rows, cols])
+        np.testing.assert_array_equal(ey, y[rows, cols])
+
+
+# ------------------------------------------------------------ dequantisation
+
+def test_dequant_exact_rational():
+    """y = acc * sx * sw[n] (+ bias): fp64 within 2 roundings of the exact
+    rational value (App. A.1 dequantisation, zero points zero)."""
+    M, N, K = 6, 11, 50
+    X, W = rand_i8((M, K)), rand_i8((N, K))
+    sw = RNG.uniform(1e-3, 1e-2, size=N).astype(np.float32)
+    bias = RNG.uniform(-1, 1, size=N).astype(np.float32)
+    sx = np.float32(0.02)
+    for b in (8, 3):
+        acc, y = oracle.masked_linear(X, W, float(sx), sw, b, bias)
+        for m in range(M):
+            for n in range(N):
+                exact = Fraction(int(acc[m, n])) * Fraction(float(sx)) * Fraction(float(sw[n])) \
+                    + Fraction(float(bias[n]))
+                mag = abs(Fraction(int(acc[m, n])) * Fraction(float(sx)) * Fraction(float(sw[n]))) \
+                    + abs(Fraction(float(bias[n])))
+                assert abs(Fraction(y[m, n]) - exact) <= mag * Fraction(3, 2 ** 53)
+
+
+def test_dequant_power_of_two_scales_exact():
+    M, N, K = 4, 5, 33
+    X, W = rand_i8((M, K)), rand_i8((N, K))
+    sw = np.array([2.0 ** -e for e in range(7, 7 + N)], np.float32)
+    acc, y = oracle.masked_linear(X, W, 0.25, sw, 6)
+    np.testing.assert_array_equal(y, acc.astype(np.float64) * 0.25 * sw.astype(np.float64))
+
+
+# --------------------------------------------------------------- convolution
+
+def im2col_conv(X, Wt, b):
+    """3x3/pad 1 conv as an explicit patch matrix times the masked weight."""
+    H, Wd, Ci = X.shape
+    Co = Wt.shape[0]
+    Xp = np.zeros((H + 2, Wd + 2, Ci), np.int64)
+    Xp[1:-1, 1:-1] = X
+    cols = np.zeros((H * Wd, 9 * Ci), np.int64)
+    for h in range(H):
+        for w in range(Wd):
+            cols[h * Wd + w] = Xp[h:h + 3, w:w + 3, :].reshape(-1)
+    k = 8 - b
+    Wm = Wt.astype(np.int64) & ~((1 << k) - 1)
+    return (cols @ Wm.reshape(Co, -1).T).reshape(H, Wd, Co)
+
+
+@pytest.mark.parametrize("H,Wd,Ci,Co", [(1, 1, 1, 1), (4, 5, 3, 6), (7, 3, 16, 9)])
+def test_conv_direct_vs_im2col(H, Wd, Ci, Co):
+    X = rand_i8((H, Wd, Ci))
+    Wt = rand_i8((Co, 3, 3, Ci))
+    sw = np.ones(Co, np.float32)
+    for b in (8, 6, 2):
+        acc, _ = oracle.conv3x3(X, Wt, 1.0, sw, b)
+        np.testing.assert_array_equal(acc, im2col_conv(X, Wt, b))
+
+
+def test_conv_single_tap():
+    """A centre-only kernel reduces the conv to a per-pixel linear layer."""
+    H, Wd, Ci, Co = 5, 6, 8, 4
+    X = rand_i8((H, Wd, Ci))
+    Wt = np.zeros((Co, 3, 3, Ci), np.int8)
+    Wt[:, 1, 1, :] = rand_i8((Co, Ci))
+    acc, _ = oracle.conv3x3(X, Wt, 1.0, np.ones(Co, np.float32), 5)
+    lin, _ = oracle.masked_linear(X.reshape(-1, Ci), Wt[:, 1, 1, :], 1.0,
+                                  np.ones(Co, np.float32), 5)
+    np.testing.assert_array_equal(acc.reshape(-1, Co), lin)
+
+
+# ---------------------------------------------------------------- bit planes
+
+def unpack(planes, K):
+    """Bit plane q (q = 7 - p) back to a {0,1} int64 array [8 x N x K]."""
+    Q, N, KW = planes.shape
+    j = np.arange(K)
+    return ((planes[:, :, j // 32].astype(np.int64) >> (j % 32)) & 1)
+
+
+@pytest.mark.parametrize("N,K", [(1, 1), (5, 31), (7, 32), (3, 100)])
+def test_planes_round_trip(N, K):
+    W = rand_i8((N, K))
+    W[0, 0] = -128
+    planes = oracle.pack_planes(W)
+    assert planes.shape == (8, N, (K + 31) // 32)
+    bits = unpack(planes, K)
+    coef = np.array([-128] + [1 << p for p in range(6, -1, -1)])   # q = 0 is the sign plane
+    np.testing.assert_array_equal(np.tensordot(coef, bits, 1), W.astype(np.int64))
+    # words past K are zero
+    if K % 32:
+        assert np.all(planes[:, :, -1] >> (K % 32) == 0)
+
+
+@pytest.mark.parametrize("b", range(1, 9))
+def test_bit_plane_identity(b):
+    """X W_b^T = sum_{p >= 8-b} c_p 2^p X P_p^T, c_7 = -1 (App. G.2: read
+    only the top b planes)."""
+    M, N, K = 6, 9, 70
+    X, W = rand_i8((M, K)), rand_i8((N, K))
+    bits = unpack(oracle.pack_planes(W), K)
+    total = np.zeros((M, N), np.int64)
+    for q in range(b):
+        p = 7 - q
+        c = -1 if p == 7 else 1
+        total += c * (1 << p) * (X.astype(np.int64) @ bits[q].T)
+    acc, _ = oracle.masked_linear(X, W, 1.0, np.ones(N, np.float32), b)
+    np.testing.assert_array_equal(acc, total)
+
+
+# ------------------------------------------------------------------ schedule
+
+def test_stage_map_golden():
+    for row in read_golden("stage_map.txt"):
+        T, S, stages = row[0], row[1], row[2:]
+        assert len(stages) == T
+        assert [oracle.stage_of_step(t, S, T) for t in range(T)] == stages
+
+
+@pytest.mark.parametrize("t,S,T", [(-1, 4, 20), (20, 4, 20), (0, 0, 20), (0, 5, 4), (0, 1, 0)])
+def test_stage_map_rejects(t, S, T):
+    with pytest.raises(ValueError):
+        oracle.stage_of_step(t, S, T)
+
+
+def _small_layers(rng):
+    layers = []
+    for (M, K, N) in ((5, 40, 7), (3, 33, 4)):
+        layers.append(dict(X=rand_i8((M, K), rng), W=rand_i8((N, K), rng),
+                           sw=rng.uniform(1e-3, 1e-2, N).astype(np.float32)))
+    layers.append(dict(kind="conv3x3", X=rand_i8((3, 4, 5), rng), W=rand_i8((6, 3, 3, 5), rng),
+                       sw=rng.uniform(1e-3, 1e-2, 6).astype(np.float32)))
+    return layers
+
+
+def test_schedule_properties():
+    rng = np.random.default_rng(7)
+    layers = _small_layers(rng)
+    S, T = 4, 20
+    table = rng.integers(2, 9, size=(len(layers), S))
+    # a constant-8 table equals the static 8-bit layer
+    res = oracle.run_schedule(layers, np.full((len(layers), S), 8), S, T, 0, T, 0.02)
+    for layer, (acc, y, b) in zip(layers, res):
+        if layer.get("kind") == "conv3x3":
+            want = oracle.conv3x3(layer["X"], layer["W"], 0.02, layer["sw"], 8)
+        else:
+            want = oracle.masked_linear(layer["X"], layer["W"], 0.02, layer["sw"], 8)
+        assert b == 8
+        np.testing.assert_array_equal(acc, want[0])
+    # one step per stage leaves that stage's single-layer result
+    for s in range(S):
+        t = s * (T // S) + 2
+        res = oracle.run_schedule(layers, table, S, T, t, t + 1, 0.02)
+        for l, (layer, (acc, y, b)) in enumerate(zip(layers, res)):
+            assert b == table[l][s]
+            if layer.get("kind") == "conv3x3":
+                want = oracle.conv3x3(layer["X"], layer["W"], 0.02, layer["sw"], b)
+            else:
+                want = oracle.masked_linear(layer["X"], layer["W"], 0.02, layer["sw"], b)
+            np.testing.assert_array_equal(acc, want[0])
+            np.testing.assert_array_equal(y, want[1])
+    # an empty range writes nothing
+    assert oracle.run_schedule(layers, table, S, T, 7, 7, 0.02) == [None] * len(layers)
+    with pytest.raises(ValueError):
+        oracle.run_schedule(layers, table, S, T, 5, 21, 0.02)
+
+
+# ----------------------------------------------------------------- generator
+
+def test_generator_published_value_and_ranges():
+    import torch
+    # SplitMix64 from state 0: first output 0xE220A8397B1DCDAF (published)
+    v = int(inputs.splitmix64(torch.tensor([0], dtype=torch.int64))) & (2 ** 64 - 1)
+    assert v == 0xE220A8397B1DCDAF
+    wl = inputs.workload(0)
+    X = inputs.x_full(wl, 0)
+    assert X.shape == (256, 1152) and int(X.min()) >= -127 and int(X.max()) <= 127
+    W = inputs.w_full(wl, 0)
+    assert W.shape == (1152, 1152) and abs(float(W.float().std()) - 32) < 1
+    sw = inputs.sw_full(wl, 0)
+    assert float(sw.min()) >= 1e-3 and float(sw.max()) < 1e-2
+    t = inputs.b_table(inputs.workload(4))
+    assert t.shape == (112, 4) and int(t.min()) == 2 and int(t.max()) == 8
+    assert abs(float(t.float().mean()) - 5) < 0.3
+    # counter-based: sampled rows equal the same rows of the full tensor
+    rows = [0, 17, 255]
+    np.testing.assert_array_equal(inputs.x_rows(wl, 0, rows).numpy(), X[rows].numpy())
