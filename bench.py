@@ -1,0 +1,194 @@
+"""Benchmark of the TASQ masked-linear hot path on one MI355X.
+
+One "step" is one full denoising schedule through ``tasq_run_schedule``:
+28 PixArt-Sigma-shaped blocks (112 int8 linears: QKV 1152->3456, out
+1152->1152, MLP 1152->4608 and 4608->1152, 2x4096 tokens each) over 20
+denoising steps in 4 stages, every layer at b = table[l][stage], fp32
+dequantised outputs.  Inputs are synthetic and already resident in HBM when
+timing starts.
+
+Prints one JSON line: whole-schedule int8 TOPS (2*M*N*K summed over every
+GEMM of every denoising step, divided by wall time), the same schedule with a
+static b = 8 table and with the per-layer maximum over stages, the dominant
+kernel's roofline fraction, and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2608_03057_amd as T                      # noqa: E402
+from paper_2608_03057_amd import inputs               # noqa: E402
+
+METRIC = "int8 TOPS of masked GEMM + schedule wall-time vs static 8-bit, 1×MI355X"
+PEAK_INT8_TOPS = 5000.0        # dense int8 MFMA, MI355X datasheet
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def build_workload(wl, device):
+    """Device tensors of every layer; X drawn on the GPU (integer recipe,
+    identical to the CPU draw), W and sw on the CPU (fp64 Box-Muller)."""
+    layers, keep = [], []
+    for l, spec in enumerate(wl.layers):
+        X = inputs.x_full(wl, l, device=device)
+        W = inputs.w_full(wl, l).to(device)
+        sw = inputs.sw_full(wl, l).to(device)
+        y = torch.empty((spec.M, spec.N), dtype=torch.float32, device=device)
+        keep.append((X, W, sw, y))
+        layers.append(T.make_layer(X, W, wl.sx, sw, None, None, y))
+    return layers, keep
+
+
+def gemm_ops(wl):
+    return sum(2.0 * s.M * s.N * s.K for s in wl.layers)
+
+
+def gemm_bytes(wl):
+    """Algorithmic HBM bytes of one denoising step: each layer reads X and W
+    once and writes its fp32 output once."""
+    return sum(float(s.M * s.K + s.N * s.K + 4 * s.M * s.N) for s in wl.layers)
+
+
+def time_schedule(layers, table, wl, ws, steps, warmup):
+    for _ in range(warmup):
+        T.run_schedule(layers, table, wl.S, wl.T, 0, wl.T, workspace=ws)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        T.run_schedule(layers, table, wl.S, wl.T, 0, wl.T, workspace=ws)
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+def time_launches(layers, table, wl, ws, reps):
+    """Average duration of one grouped launch (one denoising step), from
+    events recorded around each launch on the launch stream."""
+    evs = []
+    for _ in range(reps):
+        for t in range(wl.T):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            T.run_schedule(layers, table, wl.S, wl.T, t, t + 1, workspace=ws)
+            b.record()
+            evs.append((a, b))
+    torch.cuda.synchronize()
+    return float(np.mean([a.elapsed_time(b) for a, b in evs]))
+
+
+def cpu_baseline(wl, table, budget_s=15.0):
+    """The CPU oracle on a bounded sample: the first R rows of each of block
+    0's four linears at its stage-0 b, R grown until the sample takes about
+    budget_s seconds.  Returns int8 TOPS (same op count convention)."""
+    import oracle
+    oracle.build(force=False)
+    R = 8
+    while True:
+        ops, t0 = 0.0, time.perf_counter()
+        for l in range(4):
+            spec = wl.layers[l]
+            X = inputs.x_rows(wl, l, np.arange(R))
+            W = inputs.w_full(wl, l)
+            sw = inputs.sw_full(wl, l)
+            oracle.masked_linear(X, W, wl.sx, sw, int(table[l][0]))
+            ops += 2.0 * R * spec.N * spec.K
+        dt = time.perf_counter() - t0
+        if dt >= budget_s / 3 or R >= 8192:
+            break
+        R = min(8192, int(R * max(2.0, budget_s / 3 / max(dt, 1e-3))))
+    return dict(value=ops / dt / 1e12, unit="TOPS", cores=oracle.num_threads(), kind="oracle",
+                sample=f"rows 0..{R - 1} of block 0's four linears at the stage-0 b "
+                       f"({ops / 2:.3g} MACs, {dt:.1f} s)")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--tokens", type=int, default=None, help="override M (skinny sweeps)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--per-layer", action="store_true",
+                    help="launch each layer separately instead of one grouped launch per step")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); the path shards by "
+              "rows or output channels with no exchange, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+    dev = "cuda"
+    wl = inputs.workload(4, M_override=args.tokens)
+    table = inputs.b_table(wl)
+    log(f"building {len(wl.layers)} layers, M={wl.layers[0].M}")
+    layers, keep = build_workload(wl, dev)
+    ws = None
+    if not args.per_layer:
+        ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=dev)
+    t8 = torch.full_like(table, 8)
+    tmax = table.max(dim=1, keepdim=True).values.expand_as(table).contiguous()
+    torch.cuda.synchronize()
+
+    log("timing schedules")
+    ms = time_schedule(layers, table, wl, ws, args.steps, args.warmup)
+    ms8 = time_schedule(layers, t8, wl, ws, args.steps, args.warmup)
+    msmax = time_schedule(layers, tmax, wl, ws, args.steps, args.warmup)
+    ops_step = gemm_ops(wl)
+    total_ops = ops_step * wl.T
+    value = total_ops / (ms * 1e-3) / 1e12
+
+    roof = None
+    if ws is not None:
+        launch_ms = time_launches(layers, table, wl, ws, reps=1)
+        t_mfma = ops_step / (PEAK_INT8_TOPS * 1e12)
+        t_hbm = gemm_bytes(wl) / (PEAK_HBM_GBS * 1e9)
+        if t_hbm >= t_mfma:
+            ach = gemm_bytes(wl) / (launch_ms * 1e-3) / 1e9
+            roof = dict(bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s",
+                        frac=round(ach / PEAK_HBM_GBS, 4), traffic=None)
+        else:
+            ach = ops_step / (launch_ms * 1e-3) / 1e12
+            roof = dict(bound="mfma", achieved=round(ach, 1), peak=PEAK_INT8_TOPS, unit="TOP/s",
+                        frac=round(ach / PEAK_INT8_TOPS, 4), traffic=None)
+        roof["kernel"] = "k_masked_gemm_grouped (one launch = one denoising step, 112 GEMMs)"
+        roof["launch_ms"] = round(launch_ms, 4)
+        roof["mfma_frac"] = round(ops_step / (launch_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)
+        roof["roofline_ms"] = round(max(t_mfma, t_hbm) * 1e3, 4)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle sample")
+        cpu = cpu_baseline(wl, table)
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "layers": len(wl.layers), "M": wl.layers[0].M,
+                   "denoising_steps": wl.T, "stages": wl.S, "output": "fp32",
+                   "launch": "per-layer" if args.per_layer else "grouped per denoising step"},
+        "schedule_ms": {"tasq_table": round(ms, 4), "static_b8": round(ms8, 4),
+                        "static_max_over_stages": round(msmax, 4)},
+        "margin_vs_static_b8": round(1.0 - ms / ms8, 4),
+        "mean_bits": round(float(table.float().mean()), 3),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

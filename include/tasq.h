@@ -1,0 +1,211 @@
+/*
+ * tasq.h - C ABI of the TASQ masked quantized linear layer for MI355X (gfx950).
+ *
+ * The operation (TASQ, arxiv 2608.03057):
+ *   - one stored 8-bit weight buffer W per layer, shared by every denoising
+ *     stage (Sec. 3.2; Sec. 4.3 "Deployment procedure");
+ *   - at stage s, layer l runs at effective precision b = table[l][s]
+ *     (Sec. 1 and App. G.1: switching precision is a table lookup, the kernel
+ *     takes the number of bit planes as an argument);
+ *   - the operand is the stored code with its k = 8 - b least significant
+ *     bits removed and the scale kept: W_b = 2^k * floor(W / 2^k)
+ *     (Sec. 3.1 Eq. truncquant, Sec. 3.2.1 Eq. lsb_masking, App. G.2
+ *     Eqs. hw_rightshift and hw_multi_lsb);
+ *   - acc = X * W_b^T accumulated exactly in int32 (Sec. 3.1 Eq. qalora with
+ *     the LoRA branch merged), then y = acc * sx * sw[n] (+ bias[n]) in fp32
+ *     (App. A.1 dequantisation, zero points zero, the 2^n/(2^n-1) weight
+ *     factor folded into sw).
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are DEVICE memory owned by the caller.  The library
+ *     never frees, retains past the call, or writes its inputs.  Host
+ *     pointers (the layer array, the bit table) are read during the call
+ *     only.
+ *   - Layouts are row-major: X int8 [M][K], W int8 [N][K] (output x input,
+ *     K contiguous), acc int32 [M][N], y fp32 [M][N]; sw, bias fp32 [N].
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls are
+ *     asynchronous and stream-ordered; results are visible after the stream
+ *     is synchronised.  Device faults surface at that synchronisation.
+ *   - Every argument (for a schedule: every layer and every table entry) is
+ *     validated before any work is enqueued; on an error return nothing was
+ *     enqueued and outputs are untouched.  No C++ exception crosses the ABI.
+ *   - Calls on different streams that share output buffers race; calls that
+ *     share a workspace must be ordered on one stream.
+ */
+#ifndef TASQ_H
+#define TASQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes: 0 on success, negative on error. */
+enum {
+    TASQ_OK = 0,
+    TASQ_ERR_NULL = -1,      /* a required pointer is NULL, or no output requested */
+    TASQ_ERR_DIM = -2,       /* a dimension is negative or inconsistent           */
+    TASQ_ERR_BITS = -3,      /* b (or a table entry) outside [1, 8]                */
+    TASQ_ERR_OVERFLOW = -4,  /* K > TASQ_MAX_K: int32 accumulation could overflow  */
+    TASQ_ERR_RANGE = -5,     /* bad S, T, t_begin, t_end, or L                      */
+    TASQ_ERR_LAYOUT = -6,    /* requested variant needs a layout that is absent    */
+    TASQ_ERR_WORKSPACE = -7, /* workspace missing or smaller than required         */
+    TASQ_ERR_HIP = -8,       /* a HIP runtime call or kernel launch failed          */
+    TASQ_ERR_KIND = -9,      /* unknown layer kind or variant                       */
+    TASQ_ERR_ALIGN = -10     /* workspace not 256-byte aligned                     */
+};
+
+/* |X| <= 128 and |W_b| <= 128, so |acc| <= 16384 * K < 2^31 iff K <= 131071. */
+#define TASQ_MAX_K 131071
+
+/* Kernel variants (tasq_opts.variant). */
+enum {
+    TASQ_VARIANT_AUTO = 0,      /* library picks per shape                         */
+    TASQ_VARIANT_MASKED_I8 = 1, /* int8 MFMA GEMM, mask fused into weight staging  */
+    TASQ_VARIANT_BITPLANE = 2   /* reads only the top b planes of W_planes         */
+};
+
+/* Layer kinds (tasq_layer.kind). */
+enum {
+    TASQ_KIND_LINEAR = 0,       /* X [M][K]                                        */
+    TASQ_KIND_CONV3X3 = 1       /* X NHWC [H][Wd][C], W [N][3][3][C], stride 1,
+                                   zero padding 1; M = H*Wd, K = 9*C               */
+};
+
+/*
+ * Optional controls; pass NULL for defaults (AUTO variant, no workspace).
+ *   variant         TASQ_VARIANT_*.
+ *   split_k         0 = library choice, 1 = never split K, >1 = split K into
+ *                   that many slices (needs a workspace).
+ *   W_planes        bit-plane copy of W as written by tasq_pack_planes; needed
+ *                   by the BITPLANE variant (W may then be NULL).
+ *   workspace       device scratch, 256-byte aligned, owned by the caller;
+ *                   used for split-K partial sums and for the schedule's
+ *                   device-side layer list.  Size from tasq_workspace_bytes /
+ *                   tasq_schedule_workspace_bytes.  Contents need no
+ *                   initialisation and are left unspecified.
+ *   workspace_bytes its size in bytes.
+ */
+typedef struct tasq_opts {
+    int32_t variant;
+    int32_t split_k;
+    const uint32_t *W_planes;
+    void *workspace;
+    size_t workspace_bytes;
+} tasq_opts;
+
+/*
+ * y = (X * W_b^T) * sx * sw[n] (+ bias[n]),  W_b = 2^(8-b) floor(W / 2^(8-b)).
+ *   X        int8 [M][K] device, activation codes (any value in [-128, 127]).
+ *   W        int8 [N][K] device, stored 8-bit weight codes; may be NULL when
+ *            the BITPLANE variant is requested with opts->W_planes.
+ *   sx       per-tensor activation scale.
+ *   sw       fp32 [N] device, per-output-channel weight scale (read only for y).
+ *   bias     fp32 [N] device or NULL.
+ *   M, N, K  >= 0, K <= TASQ_MAX_K; M == 0 or N == 0 enqueues nothing,
+ *            K == 0 writes acc = 0 and y = bias (or 0).
+ *   b        effective weight bits, 1..8 (b = 8: the stored weight itself;
+ *            b = 1: the sign plane only, W_b in {-128, 0}).
+ *   acc_out  int32 [M][N] device or NULL: exact accumulators.
+ *   y_out    fp32 [M][N] device or NULL: dequantised output.  At least one of
+ *            acc_out / y_out must be non-NULL.
+ * A pointer may be NULL when its array is empty (X when M*K == 0, W when
+ * N*K == 0, outputs when M*N == 0); sw is needed only with y_out.
+ * Errors: TASQ_ERR_NULL, _DIM, _BITS, _OVERFLOW, _LAYOUT, _WORKSPACE, _KIND,
+ * _ALIGN, _HIP.
+ */
+int tasq_masked_linear(const int8_t *X, const int8_t *W, float sx, const float *sw,
+                       const float *bias, int M, int N, int K, int b, int32_t *acc_out,
+                       float *y_out, const tasq_opts *opts, void *stream);
+
+/*
+ * The same layer applied as a 3x3 convolution, stride 1, zero padding 1,
+ * batch 1, as an implicit GEMM with M = H*Wd, K = 9*C and the reduction
+ * index k = (r*3 + s)*C + ci:
+ *   acc[h][w][n] = sum_{r,s,ci} X[h+r-1][w+s-1][ci] * W_b[n][r][s][ci].
+ *   X int8 NHWC [H][Wd][C]; W int8 [N][3][3][C]; outputs [H][Wd][N].
+ * Stands in for the convolution tensors of the UNet backbone (the paper's
+ * SDXL-Turbo tensor count includes them, App. D.3).
+ */
+int tasq_masked_conv3x3(const int8_t *X, const int8_t *W, float sx, const float *sw,
+                        const float *bias, int H, int Wd, int C, int N, int b,
+                        int32_t *acc_out, float *y_out, const tasq_opts *opts, void *stream);
+
+/*
+ * Bit-plane relayout of a stored weight (App. G.2: plane p holds bit p of
+ * the two's-complement code, p = 0 least significant).
+ *   W          int8 [N][K] device (read only).
+ *   planes_out uint32 [8][KB][N][4] device, KB = ceil(K / 128): word
+ *              planes[q][kb][n][w] holds, in bit i, bit p = 7 - q of
+ *              W[n][128*kb + 32*w + i].  Plane q = 0 is the sign plane; the
+ *              top b planes are the contiguous prefix of b*KB*N*4 words.
+ *              Bits past K are zero.  Size tasq_planes_bytes(N, K).
+ * A one-time conversion of the stored buffer, not a per-step cost.  A
+ * caller that keeps only the planes (and passes W = NULL with the BITPLANE
+ * variant) stores the weight once, at the same 8 bits per element.
+ */
+int tasq_pack_planes(const int8_t *W, int N, int K, uint32_t *planes_out, void *stream);
+
+/* Bytes of the planes array for an N x K weight: 8 * ceil(K/128) * N * 16. */
+size_t tasq_planes_bytes(int N, int K);
+
+/*
+ * Stage of denoising step t (Sec. 3.2: contiguous stages sharing one mask;
+ * Sec. 4.1: 20 steps in four stages, or one stage per step when S = T;
+ * App. D.1: stage 0 is the noisiest, first part of the trajectory):
+ *   s = floor(t * S / T).
+ * Returns s in [0, S), or TASQ_ERR_RANGE unless 1 <= S <= T and 0 <= t < T.
+ */
+int tasq_stage_of_step(int t, int S, int T);
+
+/* One layer of a schedule.  For TASQ_KIND_LINEAR: M, N, K as in
+ * tasq_masked_linear and H, Wd, C ignored.  For TASQ_KIND_CONV3X3: H, Wd, C,
+ * N as in tasq_masked_conv3x3, and M, K must equal H*Wd and 9*C.
+ * Pointer fields follow tasq_masked_linear. */
+typedef struct tasq_layer {
+    int32_t kind;
+    int32_t M, N, K;
+    int32_t H, Wd, C;
+    float sx;
+    const int8_t *X;
+    const int8_t *W;
+    const uint32_t *W_planes;
+    const float *sw;
+    const float *bias;
+    int32_t *acc;
+    float *y;
+} tasq_layer;
+
+/*
+ * Runs denoising steps t = t_begin .. t_end-1 (Sec. 3.2 stage sharing;
+ * App. G, per-stage precision with no re-launch or reload): for each step,
+ * s = tasq_stage_of_step(t, S, T) and every layer l computes its output at
+ * b = b_table[l*S + s], overwriting its acc / y buffers.  After the call the
+ * buffers hold step t_end-1 (t_begin == t_end enqueues nothing).
+ *   layers   host array of L layer descriptors (read during the call only).
+ *   b_table  host uint8 [L][S], entries in [1, 8] (read during the call only).
+ *   1 <= S <= T, 0 <= t_begin <= t_end <= T.
+ * With opts->workspace of at least tasq_schedule_workspace_bytes(layers, L)
+ * bytes, each step is one grouped launch over every layer's tiles; without it
+ * each layer is launched separately.  The whole table and every layer are
+ * validated before anything is enqueued.
+ */
+int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
+                      int t_begin, int t_end, const tasq_opts *opts, void *stream);
+
+/* Workspace a single layer call may use (0 when it never needs one). */
+size_t tasq_workspace_bytes(int M, int N, int K);
+
+/* Workspace for the grouped schedule over these layers (host array). */
+size_t tasq_schedule_workspace_bytes(const tasq_layer *layers, int L);
+
+/* Static description of a status code; never NULL. */
+const char *tasq_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TASQ_H */

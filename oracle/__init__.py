@@ -56,6 +56,8 @@ def lib():
                                                    ctypes.c_int, p, p, i64, p, p]
         L.oracle_conv3x3.argtypes = [p, p, ctypes.c_double, p, p, i64, i64, i64, i64,
                                      ctypes.c_int, p, p]
+        L.oracle_conv3x3_entries.argtypes = [p, p, ctypes.c_double, p, p, i64, i64, i64,
+                                             ctypes.c_int, p, p, i64, p, p]
         L.oracle_pack_planes.argtypes = [p, i64, i64, p]
         _lib = L
     return _lib
@@ -167,12 +169,38 @@ def conv3x3(X, Wt, sx: float, sw, b: int, bias=None):
     return acc, y
 
 
+def conv3x3_entries(X, Wt, sx, sw, b, pix, cols, bias=None):
+    """Outputs (pix[i] = h*Wd + w, cols[i]) of the masked 3x3 convolution,
+    each computed as its own convolution sum."""
+    X = _np(X, np.int8)
+    Wt = _np(Wt, np.int8)
+    sw = _np(sw, np.float32)
+    bias = None if bias is None else _np(bias, np.float32)
+    pix = _np(pix, np.int64)
+    cols = _np(cols, np.int64)
+    H, Wd, Ci = X.shape
+    Co = Wt.shape[0]
+    assert Wt.shape == (Co, 3, 3, Ci) and pix.shape == cols.shape
+    assert pix.size == 0 or (0 <= pix.min() and pix.max() < H * Wd)
+    assert cols.size == 0 or (0 <= cols.min() and cols.max() < Co)
+    acc = np.empty(pix.size, np.int32)
+    y = np.empty(pix.size, np.float64)
+    rc = lib().oracle_conv3x3_entries(_ptr(X), _ptr(Wt), float(sx), _ptr(sw), _ptr(bias), H, Wd,
+                                      Ci, b, _ptr(pix), _ptr(cols), pix.size, _ptr(acc), _ptr(y))
+    if rc == EOVERFLOW:
+        raise OverflowError("accumulator outside int32")
+    if rc != OK:
+        raise ValueError(f"oracle_conv3x3_entries rc={rc}")
+    return acc, y
+
+
 def pack_planes(W) -> np.ndarray:
-    """uint32 [8 x N x ceil(K/32)] bit planes, most significant plane first."""
+    """uint32 [8 x ceil(K/128) x N x 4] bit planes, most significant plane
+    first; word w of block kb holds elements 128*kb + 32*w .. +31 of a row."""
     W = _np(W, np.int8)
     N, K = W.shape
-    KW = (K + 31) // 32
-    planes = np.empty((8, N, KW), np.uint32)
+    KB = (K + 127) // 128
+    planes = np.empty((8, KB, N, 4), np.uint32)
     lib().oracle_pack_planes(_ptr(W), N, K, _ptr(planes))
     return planes
 

@@ -204,23 +204,66 @@ int oracle_conv3x3(const int8_t *X, const int8_t *Wt, double sx, const float *sw
 }
 
 /*
- * Bit planes of the stored two's-complement weight (App. G.2: plane p is
- * bit p of the code, p = 0 the least significant).  Layout
- * planes[q][n][j / 32], bit (j % 32), with q = 7 - p (most significant plane
- * first, so the top b planes are one contiguous prefix); words past K are
- * zero.  KW = ceil(K / 32).
+ * Entries (pix[i], cols[i]) of the same convolution, pix = h*Wd + w, each
+ * computed as its own convolution sum, for sampled checks of large layers.
+ */
+int oracle_conv3x3_entries(const int8_t *X, const int8_t *Wt, double sx, const float *sw,
+                           const float *bias, int64_t H, int64_t Wd, int64_t Ci, int b,
+                           const int64_t *pix, const int64_t *cols, int64_t count,
+                           int32_t *acc, double *y)
+{
+    if (b < 1 || b > 8)
+        return ORACLE_EBITS;
+    int overflow = 0;
+#pragma omp parallel for schedule(static) reduction(| : overflow)
+    for (int64_t i = 0; i < count; ++i) {
+        int64_t h = pix[i] / Wd, w = pix[i] % Wd, co = cols[i];
+        int64_t s = 0;
+        for (int64_t r = 0; r < 3; ++r) {
+            int64_t hh = h + r - 1;
+            if (hh < 0 || hh >= H)
+                continue;
+            for (int64_t q = 0; q < 3; ++q) {
+                int64_t ww = w + q - 1;
+                if (ww < 0 || ww >= Wd)
+                    continue;
+                const int8_t *xp = X + (hh * Wd + ww) * Ci;
+                const int8_t *wp = Wt + ((co * 3 + r) * 3 + q) * Ci;
+                for (int64_t ci = 0; ci < Ci; ++ci)
+                    s += (int64_t)xp[ci] * masked_value(wp[ci], b);
+            }
+        }
+        if (s >= ((int64_t)1 << 31) || s < -((int64_t)1 << 31))
+            overflow = 1;
+        acc[i] = (int32_t)s;
+        double v = (double)s * sx * (double)sw[co];
+        if (bias)
+            v += (double)bias[co];
+        y[i] = v;
+    }
+    return overflow ? ORACLE_EOVERFLOW : ORACLE_OK;
+}
+
+/*
+ * Bit planes of the stored two's-complement weight (App. G.2: plane p is bit
+ * p of the code, p = 0 the least significant).  Layout, in uint32 words:
+ *   planes[q][kb][n][w],  q = 7 - p (most significant plane first, so the
+ *   top b planes are one contiguous prefix), kb = j / 128, w = (j % 128) / 32,
+ *   bit (j % 32) of the word is element j of row n.
+ * KB = ceil(K / 128); bits past K are zero.
  */
 int oracle_pack_planes(const int8_t *W, int64_t N, int64_t K, uint32_t *planes)
 {
-    int64_t KW = (K + 31) / 32;
-    for (int64_t i = 0; i < 8 * N * KW; ++i)
+    int64_t KB = (K + 127) / 128;
+    for (int64_t i = 0; i < 8 * KB * N * 4; ++i)
         planes[i] = 0;
     for (int q = 0; q < 8; ++q) {
         int p = 7 - q;
         for (int64_t n = 0; n < N; ++n)
             for (int64_t j = 0; j < K; ++j) {
                 uint32_t bit = ((uint32_t)(uint8_t)W[n * K + j] >> p) & 1u;
-                planes[(q * N + n) * KW + j / 32] |= bit << (j % 32);
+                int64_t word = ((q * KB + j / 128) * N + n) * 4 + (j % 128) / 32;
+                planes[word] |= bit << (j % 32);
             }
     }
     return ORACLE_OK;

@@ -1,0 +1,15 @@
+"""TASQ masked quantized linear layer on MI355X (gfx950).
+
+Python face of the C ABI in ``include/tasq.h``: torch tensors in, device
+pointers and the current HIP stream out to ``libtasq.so``.  Nothing here
+computes; every operation is one call into the library.
+"""
+from __future__ import annotations
+
+from .api import (  # noqa: F401
+    masked_linear, masked_conv3x3, pack_planes, planes_bytes, stage_of_step, run_schedule,
+    schedule_workspace_bytes, workspace_bytes, make_layer, status_string,
+)
+from ._lib import (  # noqa: F401
+    TasqError, VARIANT_AUTO, VARIANT_MASKED_I8, VARIANT_BITPLANE, KIND_LINEAR, KIND_CONV3X3,
+)

@@ -1,0 +1,173 @@
+"""Torch-facing wrappers of the C ABI (argument marshalling only).
+
+Each wrapper checks that tensors are on the GPU with the dtype and shape the
+C ABI documents, passes ``data_ptr()`` and the current HIP stream, and
+raises ``TasqError`` on a non-zero status.  The work is enqueued on the
+current stream and is asynchronous like any other GPU op.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import List, Optional, Sequence
+
+import torch
+
+from . import _lib
+from ._lib import Layer, Opts, check
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _need(t: Optional[torch.Tensor], dtype, shape, name):
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _opts(variant, planes, workspace, split_k) -> Opts:
+    o = Opts()
+    o.variant = variant
+    o.split_k = split_k
+    o.W_planes = _ptr(planes)
+    o.workspace = _ptr(workspace)
+    o.workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    return o
+
+
+def status_string(status: int) -> str:
+    return _lib.status_string(status)
+
+
+def stage_of_step(t: int, S: int, T: int) -> int:
+    """floor(t*S/T) via the library; raises on a bad (t, S, T)."""
+    s = _lib.lib().tasq_stage_of_step(t, S, T)
+    if s < 0:
+        raise _lib.TasqError(s, "tasq_stage_of_step")
+    return s
+
+
+def planes_bytes(N: int, K: int) -> int:
+    return _lib.lib().tasq_planes_bytes(N, K)
+
+
+def workspace_bytes(M: int, N: int, K: int) -> int:
+    return _lib.lib().tasq_workspace_bytes(M, N, K)
+
+
+def pack_planes(W: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """uint32 planes [8, ceil(K/128), N, 4] (as int32 storage) of int8 W [N, K]."""
+    N, K = W.shape
+    _need(W, torch.int8, (N, K), "W")
+    shape = (8, (K + 127) // 128, N, 4)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.int32, device=W.device)
+    _need(out, torch.int32, shape, "planes")
+    check(_lib.lib().tasq_pack_planes(_ptr(W), N, K, _ptr(out), _stream()), "tasq_pack_planes")
+    return out
+
+
+def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: torch.Tensor,
+                  b: int, bias: Optional[torch.Tensor] = None, *, want_acc: bool = True,
+                  want_y: bool = True, acc: Optional[torch.Tensor] = None,
+                  y: Optional[torch.Tensor] = None, variant: int = _lib.VARIANT_AUTO,
+                  planes: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None, split_k: int = 0):
+    """(acc int32 [M, N] or None, y fp32 [M, N] or None) of the masked layer."""
+    M, K = X.shape
+    N = sw.shape[0]
+    _need(X, torch.int8, (M, K), "X")
+    _need(W, torch.int8, (N, K), "W")
+    _need(sw, torch.float32, (N,), "sw")
+    _need(bias, torch.float32, (N,), "bias")
+    if want_acc and acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=X.device)
+    if want_y and y is None:
+        y = torch.empty((M, N), dtype=torch.float32, device=X.device)
+    _need(acc, torch.int32, (M, N), "acc")
+    _need(y, torch.float32, (M, N), "y")
+    o = _opts(variant, planes, workspace, split_k)
+    rc = _lib.lib().tasq_masked_linear(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias), M, N,
+                                       K, int(b), _ptr(acc), _ptr(y), ctypes.byref(o), _stream())
+    check(rc, "tasq_masked_linear")
+    return acc, y
+
+
+def masked_conv3x3(X: torch.Tensor, W: torch.Tensor, sx: float, sw: torch.Tensor, b: int,
+                   bias: Optional[torch.Tensor] = None, *, want_acc: bool = True,
+                   want_y: bool = True, acc=None, y=None, workspace=None, split_k: int = 0):
+    """3x3 / pad 1 conv, X NHWC [H, Wd, C], W [N, 3, 3, C] -> [H, Wd, N]."""
+    H, Wd, C = X.shape
+    N = W.shape[0]
+    _need(X, torch.int8, (H, Wd, C), "X")
+    _need(W, torch.int8, (N, 3, 3, C), "W")
+    _need(sw, torch.float32, (N,), "sw")
+    _need(bias, torch.float32, (N,), "bias")
+    if want_acc and acc is None:
+        acc = torch.empty((H, Wd, N), dtype=torch.int32, device=X.device)
+    if want_y and y is None:
+        y = torch.empty((H, Wd, N), dtype=torch.float32, device=X.device)
+    _need(acc, torch.int32, (H, Wd, N), "acc")
+    _need(y, torch.float32, (H, Wd, N), "y")
+    o = _opts(_lib.VARIANT_AUTO, None, workspace, split_k)
+    rc = _lib.lib().tasq_masked_conv3x3(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias), H, Wd,
+                                        C, N, int(b), _ptr(acc), _ptr(y), ctypes.byref(o),
+                                        _stream())
+    check(rc, "tasq_masked_conv3x3")
+    return acc, y
+
+
+def make_layer(X, W, sx, sw, bias=None, acc=None, y=None, planes=None, kind=None) -> Layer:
+    """A tasq_layer for run_schedule; tensors must stay alive while in use."""
+    L = Layer()
+    if kind is None:
+        kind = _lib.KIND_CONV3X3 if X.dim() == 3 else _lib.KIND_LINEAR
+    L.kind = kind
+    if kind == _lib.KIND_CONV3X3:
+        H, Wd, C = X.shape
+        L.H, L.Wd, L.C = H, Wd, C
+        L.M, L.K = H * Wd, 9 * C
+    else:
+        L.M, L.K = X.shape
+    L.N = sw.shape[0]
+    L.sx = float(sx)
+    L.X, L.W, L.W_planes = _ptr(X), _ptr(W), _ptr(planes)
+    L.sw, L.bias, L.acc, L.y = _ptr(sw), _ptr(bias), _ptr(acc), _ptr(y)
+    return L
+
+
+def _layer_array(layers: Sequence[Layer]):
+    arr = (Layer * len(layers))(*layers)
+    return arr
+
+
+def schedule_workspace_bytes(layers: Sequence[Layer]) -> int:
+    arr = _layer_array(layers)
+    return _lib.lib().tasq_schedule_workspace_bytes(arr, len(layers))
+
+
+def run_schedule(layers: Sequence[Layer], table: torch.Tensor, S: int, T: int, t_begin: int,
+                 t_end: int, *, workspace: Optional[torch.Tensor] = None,
+                 variant: int = _lib.VARIANT_AUTO) -> None:
+    """Runs steps t_begin..t_end-1; ``table`` is a host uint8 [L, S] tensor."""
+    table = table.to(torch.uint8).contiguous().cpu()
+    L = len(layers)
+    if tuple(table.shape) != (L, S):
+        raise ValueError(f"table must be [{L}, {S}]")
+    arr = _layer_array(layers)
+    o = _opts(variant, None, workspace, 0)
+    rc = _lib.lib().tasq_run_schedule(arr, L, table.data_ptr(), S, T, t_begin, t_end,
+                                      ctypes.byref(o), _stream())
+    check(rc, "tasq_run_schedule")

@@ -1,0 +1,354 @@
+// C ABI of the TASQ masked quantized linear layer: argument validation,
+// variant/tile choice, launches, schedule runner.  See include/tasq.h for the
+// contract of every entry point.
+#include "tasq.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "tasq_internal.h"
+
+using tasq::LayerDesc;
+
+namespace {
+
+constexpr size_t kWsAlign = 256;
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_dims(long long M, long long N, long long K)
+{
+    if (M < 0 || N < 0 || K < 0)
+        return TASQ_ERR_DIM;
+    if (K > TASQ_MAX_K)
+        return TASQ_ERR_OVERFLOW;
+    return TASQ_OK;
+}
+
+int check_variant(const tasq_opts *o, const int8_t *W)
+{
+    const int v = o ? o->variant : TASQ_VARIANT_AUTO;
+    if (v != TASQ_VARIANT_AUTO && v != TASQ_VARIANT_MASKED_I8 && v != TASQ_VARIANT_BITPLANE)
+        return TASQ_ERR_KIND;
+    if (o && o->split_k < 0)
+        return TASQ_ERR_RANGE;
+    if (v == TASQ_VARIANT_BITPLANE && !(o && o->W_planes))
+        return TASQ_ERR_LAYOUT;
+    if (v != TASQ_VARIANT_BITPLANE && !W)
+        return TASQ_ERR_NULL;
+    if (o && o->workspace && (reinterpret_cast<uintptr_t>(o->workspace) % kWsAlign) != 0)
+        return TASQ_ERR_ALIGN;
+    return TASQ_OK;
+}
+
+// Tile used for a single (non-grouped) launch.  Small problems take small
+// tiles so that more workgroups cover the 256 compute units.
+int pick_tile(long long M, long long N)
+{
+    const long long t128 = ((M + 127) / 128) * ((N + 127) / 128);
+    if (t128 >= 256)
+        return tasq::TILE_128x128;
+    return tasq::TILE_64x64;
+}
+
+bool use_bitplane(const tasq_opts *o) { return o && o->variant == TASQ_VARIANT_BITPLANE; }
+
+int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
+{
+    if (d.M == 0 || d.N == 0)
+        return TASQ_OK;
+    hipError_t e;
+    if (use_bitplane(o)) {
+        e = tasq::launch_bitplane(d, (d.K % 16) == 0 && aligned16(d.X), stream);
+    } else {
+        bool aligned;
+        if (d.kind == tasq::KIND_CONV3X3)
+            aligned = (d.C % 16) == 0 && aligned16(d.X) && aligned16(d.W);
+        else
+            aligned = (d.K % 16) == 0 && aligned16(d.X) && aligned16(d.W);
+        e = tasq::launch_single(d, pick_tile(d.M, d.N), aligned, nullptr, stream);
+    }
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}
+
+LayerDesc make_desc(const tasq_layer &L, const tasq_opts *o)
+{
+    LayerDesc d;
+    std::memset(&d, 0, sizeof d);
+    d.X = L.X;
+    d.W = L.W;
+    d.P = L.W_planes ? L.W_planes : (o ? o->W_planes : nullptr);
+    d.sw = L.sw;
+    d.bias = L.bias;
+    d.acc = L.acc;
+    d.y = L.y;
+    d.sx = L.sx;
+    d.M = L.M;
+    d.N = L.N;
+    d.K = L.K;
+    d.kind = L.kind;
+    d.H = L.H;
+    d.Wd = L.Wd;
+    d.C = L.C;
+    d.ksplit = 1;
+    return d;
+}
+
+// Validation shared by single calls and schedule layers.
+int validate_layer(const tasq_layer &L, const tasq_opts *o)
+{
+    if (L.kind != TASQ_KIND_LINEAR && L.kind != TASQ_KIND_CONV3X3)
+        return TASQ_ERR_KIND;
+    // A pointer is required only where its array has elements.
+    const bool has_out = L.M > 0 && L.N > 0;
+    if (L.M > 0 && L.K > 0 && !L.X)
+        return TASQ_ERR_NULL;
+    if (has_out && !L.acc && !L.y)
+        return TASQ_ERR_NULL;
+    if (has_out && L.y && !L.sw)
+        return TASQ_ERR_NULL;
+    tasq_opts local = o ? *o : tasq_opts{};
+    if (L.W_planes)
+        local.W_planes = L.W_planes;
+    const bool needs_w = L.N > 0 && L.K > 0;
+    if (int rc = check_variant(&local, needs_w ? L.W : reinterpret_cast<const int8_t *>(1)))
+        return rc;
+    if (L.kind == TASQ_KIND_CONV3X3) {
+        if (L.H < 0 || L.Wd < 0 || L.C < 0 || L.N < 0)
+            return TASQ_ERR_DIM;
+        if ((long long)L.M != (long long)L.H * L.Wd || (long long)L.K != 9LL * L.C)
+            return TASQ_ERR_DIM;
+        if (use_bitplane(&local))
+            return TASQ_ERR_LAYOUT;     // the bit-plane kernel covers linear layers
+    }
+    return check_dims(L.M, L.N, L.K);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *tasq_status_string(int status)
+{
+    switch (status) {
+    case TASQ_OK: return "ok";
+    case TASQ_ERR_NULL: return "required pointer is NULL or no output requested";
+    case TASQ_ERR_DIM: return "bad dimension";
+    case TASQ_ERR_BITS: return "effective bits outside [1, 8]";
+    case TASQ_ERR_OVERFLOW: return "K too large for exact int32 accumulation";
+    case TASQ_ERR_RANGE: return "bad stage/step range or count";
+    case TASQ_ERR_LAYOUT: return "requested variant needs a weight layout that is absent";
+    case TASQ_ERR_WORKSPACE: return "workspace missing or too small";
+    case TASQ_ERR_HIP: return "HIP runtime or launch failure";
+    case TASQ_ERR_KIND: return "unknown layer kind or variant";
+    case TASQ_ERR_ALIGN: return "workspace not 256-byte aligned";
+    default: return "unknown status";
+    }
+}
+
+int tasq_stage_of_step(int t, int S, int T)
+{
+    if (S < 1 || T < 1 || S > T || t < 0 || t >= T)
+        return TASQ_ERR_RANGE;
+    return (int)(((long long)t * S) / T);
+}
+
+size_t tasq_planes_bytes(int N, int K)
+{
+    if (N < 0 || K < 0)
+        return 0;
+    return (size_t)8 * (size_t)((K + 127) / 128) * (size_t)N * 16;
+}
+
+size_t tasq_workspace_bytes(int M, int N, int K)
+{
+    (void)M;
+    (void)N;
+    (void)K;
+    return 0;
+}
+
+int tasq_masked_linear(const int8_t *X, const int8_t *W, float sx, const float *sw,
+                       const float *bias, int M, int N, int K, int b, int32_t *acc_out,
+                       float *y_out, const tasq_opts *opts, void *stream)
+{
+    tasq_layer L;
+    std::memset(&L, 0, sizeof L);
+    L.kind = TASQ_KIND_LINEAR;
+    L.M = M;
+    L.N = N;
+    L.K = K;
+    L.sx = sx;
+    L.X = X;
+    L.W = W;
+    L.sw = sw;
+    L.bias = bias;
+    L.acc = acc_out;
+    L.y = y_out;
+    if (int rc = validate_layer(L, opts))
+        return rc;
+    if (b < 1 || b > 8)
+        return TASQ_ERR_BITS;
+    LayerDesc d = make_desc(L, opts);
+    d.bits = b;
+    return launch_layer(d, opts, static_cast<hipStream_t>(stream));
+}
+
+int tasq_masked_conv3x3(const int8_t *X, const int8_t *W, float sx, const float *sw,
+                        const float *bias, int H, int Wd, int C, int N, int b,
+                        int32_t *acc_out, float *y_out, const tasq_opts *opts, void *stream)
+{
+    if (H < 0 || Wd < 0 || C < 0 || N < 0)
+        return TASQ_ERR_DIM;
+    const long long M = (long long)H * Wd, K = 9LL * C;
+    if (M > 0x7fffffffLL)
+        return TASQ_ERR_DIM;
+    if (K > TASQ_MAX_K)
+        return TASQ_ERR_OVERFLOW;
+    tasq_layer L;
+    std::memset(&L, 0, sizeof L);
+    L.kind = TASQ_KIND_CONV3X3;
+    L.M = (int)M;
+    L.N = N;
+    L.K = (int)K;
+    L.H = H;
+    L.Wd = Wd;
+    L.C = C;
+    L.sx = sx;
+    L.X = X;
+    L.W = W;
+    L.sw = sw;
+    L.bias = bias;
+    L.acc = acc_out;
+    L.y = y_out;
+    if (int rc = validate_layer(L, opts))
+        return rc;
+    if (b < 1 || b > 8)
+        return TASQ_ERR_BITS;
+    LayerDesc d = make_desc(L, opts);
+    d.bits = b;
+    return launch_layer(d, opts, static_cast<hipStream_t>(stream));
+}
+
+int tasq_pack_planes(const int8_t *W, int N, int K, uint32_t *planes_out, void *stream)
+{
+    if (!W || !planes_out)
+        return TASQ_ERR_NULL;
+    if (N < 0 || K < 0)
+        return TASQ_ERR_DIM;
+    if (N == 0 || K == 0)
+        return TASQ_OK;
+    hipError_t e = tasq::launch_pack_planes(W, N, K, planes_out, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}
+
+size_t tasq_schedule_workspace_bytes(const tasq_layer *layers, int L)
+{
+    (void)layers;
+    if (L <= 0)
+        return 0;
+    return round_up((size_t)L * sizeof(LayerDesc), kWsAlign) + round_up((size_t)L * 64, kWsAlign);
+}
+
+int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
+                      int t_begin, int t_end, const tasq_opts *opts, void *stream)
+{
+    if (L < 0)
+        return TASQ_ERR_RANGE;
+    if (L > 0 && (!layers || !b_table))
+        return TASQ_ERR_NULL;
+    if (S < 1 || T < 1 || S > T || t_begin < 0 || t_begin > t_end || t_end > T)
+        return TASQ_ERR_RANGE;
+    if (S > 64)
+        return TASQ_ERR_RANGE;
+    if (opts && opts->workspace && (reinterpret_cast<uintptr_t>(opts->workspace) % kWsAlign))
+        return TASQ_ERR_ALIGN;
+    for (int l = 0; l < L; ++l) {
+        if (int rc = validate_layer(layers[l], opts))
+            return rc;
+        for (int s = 0; s < S; ++s) {
+            const int b = b_table[(size_t)l * S + s];
+            if (b < 1 || b > 8)
+                return TASQ_ERR_BITS;
+        }
+    }
+    if (L == 0 || t_begin == t_end)
+        return TASQ_OK;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+
+    std::vector<LayerDesc> descs;
+    try {
+        descs.resize(L);
+    } catch (const std::bad_alloc &) {
+        return TASQ_ERR_HIP;
+    }
+    for (int l = 0; l < L; ++l)
+        descs[l] = make_desc(layers[l], opts);
+
+    // Grouped path: one launch per step over every layer's tiles, with the
+    // layer list and bit table resident in the caller's workspace.
+    const size_t need = tasq_schedule_workspace_bytes(layers, L);
+    bool grouped = opts && opts->workspace && opts->workspace_bytes >= need &&
+                   !use_bitplane(opts);
+    for (int l = 0; grouped && l < L; ++l) {
+        const LayerDesc &d = descs[l];
+        const bool ok = d.kind == tasq::KIND_CONV3X3
+                            ? (d.C % 16 == 0 && aligned16(d.X) && aligned16(d.W))
+                            : (d.K % 16 == 0 && aligned16(d.X) && aligned16(d.W));
+        grouped = ok;
+    }
+    if (grouped) {
+        const int tile = tasq::TILE_128x128;
+        const tasq::TileShape ts = tasq::tile_shape(tile);
+        long long total = 0;
+        for (int l = 0; l < L; ++l) {
+            LayerDesc &d = descs[l];
+            d.tiles_m = (d.M + ts.bm - 1) / ts.bm;
+            d.tiles_n = (d.N + ts.bn - 1) / ts.bn;
+            d.tile_begin = (int)total;
+            total += (long long)d.tiles_m * d.tiles_n;
+            if (total > 0x7fffffffLL)
+                return TASQ_ERR_DIM;
+        }
+        if (total == 0)
+            return TASQ_OK;
+        char *ws = static_cast<char *>(opts->workspace);
+        LayerDesc *d_descs = reinterpret_cast<LayerDesc *>(ws);
+        uint8_t *d_table = reinterpret_cast<uint8_t *>(
+            ws + round_up((size_t)L * sizeof(LayerDesc), kWsAlign));
+        std::vector<uint8_t> table((size_t)L * 64, 0);
+        for (int l = 0; l < L; ++l)
+            for (int s = 0; s < S; ++s)
+                table[(size_t)l * S + s] = b_table[(size_t)l * S + s];
+        if (hipMemcpyAsync(d_descs, descs.data(), (size_t)L * sizeof(LayerDesc),
+                           hipMemcpyHostToDevice, st) != hipSuccess)
+            return TASQ_ERR_HIP;
+        if (hipMemcpyAsync(d_table, table.data(), (size_t)L * S, hipMemcpyHostToDevice, st) !=
+            hipSuccess)
+            return TASQ_ERR_HIP;
+        for (int t = t_begin; t < t_end; ++t) {
+            const int s = tasq_stage_of_step(t, S, T);
+            if (tasq::launch_grouped(d_descs, L, (int)total, d_table, S, s, tile, st) !=
+                hipSuccess)
+                return TASQ_ERR_HIP;
+        }
+        return TASQ_OK;
+    }
+
+    for (int t = t_begin; t < t_end; ++t) {
+        const int s = tasq_stage_of_step(t, S, T);
+        for (int l = 0; l < L; ++l) {
+            descs[l].bits = b_table[(size_t)l * S + s];
+            if (int rc = launch_layer(descs[l], opts, st))
+                return rc;
+        }
+    }
+    return TASQ_OK;
+}
+
+}  // extern "C"

@@ -88,6 +88,21 @@ def _grid(rows: Sequence[int] | torch.Tensor, ncols: int, device) -> torch.Tenso
     return r * ncols + c
 
 
+def _draw_rows(rows, ncols: int, device, dtype, fn) -> torch.Tensor:
+    """[len(rows) x ncols] array whose element (i, j) is fn(rows[i]*ncols + j),
+    evaluated a few thousand rows at a time so temporaries stay small."""
+    rows = torch.as_tensor(rows, dtype=torch.int64).reshape(-1)
+    out = torch.empty((rows.numel(), ncols), dtype=dtype, device=device)
+    if rows.numel() == 0 or ncols == 0:
+        return out
+    budget = (1 << 16) if torch.device(device).type == "cpu" else (1 << 24)
+    step = max(1, budget // ncols)
+    for i in range(0, rows.numel(), step):
+        r = rows[i:i + step].to(device)
+        out[i:i + step] = fn(_grid(r, ncols, device))
+    return out
+
+
 # ---------------------------------------------------------------- workloads
 
 @dataclasses.dataclass(frozen=True)
@@ -185,13 +200,14 @@ def x_rows(wl: Workload, l: int, rows, device="cpu") -> torch.Tensor:
     rows are pixels."""
     spec = wl.layers[l]
     width = spec.C if spec.kind == "conv3x3" else spec.K
-    return uniform_int(wl.seed, tid_x(l), _grid(rows, width, device), -127, 127)
+    return _draw_rows(rows, width, device, torch.int8,
+                      lambda idx: uniform_int(wl.seed, tid_x(l), idx, -127, 127))
 
 
 def x_full(wl: Workload, l: int, device="cpu") -> torch.Tensor:
     spec = wl.layers[l]
     rows = spec.H * spec.Wd if spec.kind == "conv3x3" else spec.M
-    out = x_rows(wl, l, torch.arange(rows, device=device), device)
+    out = x_rows(wl, l, torch.arange(rows), device)
     if spec.kind == "conv3x3":
         return out.reshape(spec.H, spec.Wd, spec.C)
     return out
@@ -200,7 +216,8 @@ def x_full(wl: Workload, l: int, device="cpu") -> torch.Tensor:
 def w_rows(wl: Workload, l: int, rows) -> torch.Tensor:
     """Rows (output channels) of W_l, int8 [len(rows) x K] on the CPU."""
     spec = wl.layers[l]
-    return normal_int8(wl.seed, tid_w(l), _grid(rows, spec.K, "cpu"))
+    return _draw_rows(rows, spec.K, "cpu", torch.int8,
+                      lambda idx: normal_int8(wl.seed, tid_w(l), idx))
 
 
 def w_full(wl: Workload, l: int) -> torch.Tensor:
@@ -231,8 +248,10 @@ def b_table(wl: Workload) -> torch.Tensor:
 def random_case(seed: int, M: int, N: int, K: int, device="cpu"):
     """Free-form fuzz case: X, W uniform over the whole int8 range [-128, 127]
     (so both operands reach -128), sw uniform on [1e-3, 1e-2)."""
-    X = uniform_int(seed, 1, torch.arange(M * K, device=device), -128, 127).reshape(M, K)
-    W = uniform_int(seed, 2, torch.arange(N * K, device=device), -128, 127).reshape(N, K)
+    X = _draw_rows(torch.arange(M), K, device, torch.int8,
+                   lambda idx: uniform_int(seed, 1, idx, -128, 127))
+    W = _draw_rows(torch.arange(N), K, device, torch.int8,
+                   lambda idx: uniform_int(seed, 2, idx, -128, 127))
     sw = uniform_f32(seed, 3, torch.arange(N), 1e-3, 1e-2)
     bias = uniform_f32(seed, 4, torch.arange(N), -1.0, 1.0)
     return X, W, sw, bias

@@ -1,0 +1,174 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol
+include/tasq.h declares, and rejects every bad argument before touching a
+device (the pointers below are never dereferenced: each call fails
+validation, or is an empty problem that enqueues nothing)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT, read_golden
+from paper_2608_03057_amd import _lib
+from paper_2608_03057_amd._lib import Layer, Opts
+
+L = _lib.lib()
+FAKE = 0x10000          # 256-byte aligned, never dereferenced
+
+
+def header_symbols():
+    text = open(os.path.join(ROOT, "include", "tasq.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tasq_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    syms = header_symbols()
+    assert set(syms) == set(_lib.EXPORTS)
+    for s in syms:
+        assert hasattr(L, s), s
+
+
+def test_status_strings():
+    for code in range(0, -11, -1):
+        s = _lib.status_string(code)
+        assert s and s != "unknown status"
+    assert _lib.status_string(-99) == "unknown status"
+
+
+def test_stage_of_step_golden():
+    for row in read_golden("stage_map.txt"):
+        T, S, stages = row[0], row[1], row[2:]
+        assert [L.tasq_stage_of_step(t, S, T) for t in range(T)] == stages
+
+
+@pytest.mark.parametrize("t,S,T", [(-1, 4, 20), (20, 4, 20), (0, 0, 20), (0, 5, 4), (0, 1, 0)])
+def test_stage_of_step_range(t, S, T):
+    assert L.tasq_stage_of_step(t, S, T) == _lib.TASQ_ERR_RANGE
+
+
+def test_planes_bytes():
+    assert L.tasq_planes_bytes(1152, 1152) == 8 * 9 * 1152 * 16
+    assert L.tasq_planes_bytes(3, 1) == 8 * 1 * 3 * 16
+    assert L.tasq_planes_bytes(3, 129) == 8 * 2 * 3 * 16
+
+
+def lin(**kw):
+    a = dict(X=FAKE, W=FAKE, sx=0.02, sw=FAKE, bias=None, M=4, N=4, K=32, b=8, acc=FAKE,
+             y=FAKE, opts=None)
+    a.update(kw)
+    o = a["opts"]
+    return L.tasq_masked_linear(a["X"], a["W"], a["sx"], a["sw"], a["bias"], a["M"], a["N"],
+                                a["K"], a["b"], a["acc"], a["y"],
+                                ctypes.byref(o) if o is not None else None, None)
+
+
+def opts(**kw):
+    o = Opts()
+    for k, v in kw.items():
+        setattr(o, k, v)
+    return o
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(X=None), _lib.TASQ_ERR_NULL),
+    (dict(W=None), _lib.TASQ_ERR_NULL),
+    (dict(sw=None), _lib.TASQ_ERR_NULL),
+    (dict(acc=None, y=None), _lib.TASQ_ERR_NULL),
+    (dict(M=-1), _lib.TASQ_ERR_DIM),
+    (dict(N=-5), _lib.TASQ_ERR_DIM),
+    (dict(K=-1), _lib.TASQ_ERR_DIM),
+    (dict(b=0), _lib.TASQ_ERR_BITS),
+    (dict(b=9), _lib.TASQ_ERR_BITS),
+    (dict(b=-3), _lib.TASQ_ERR_BITS),
+    (dict(K=131072), _lib.TASQ_ERR_OVERFLOW),
+    (dict(opts=opts(variant=7)), _lib.TASQ_ERR_KIND),
+    (dict(opts=opts(variant=_lib.VARIANT_BITPLANE)), _lib.TASQ_ERR_LAYOUT),
+    (dict(W=None, opts=opts(variant=_lib.VARIANT_MASKED_I8)), _lib.TASQ_ERR_NULL),
+    (dict(opts=opts(workspace=FAKE + 8, workspace_bytes=1024)), _lib.TASQ_ERR_ALIGN),
+    (dict(opts=opts(split_k=-2)), _lib.TASQ_ERR_RANGE),
+])
+def test_masked_linear_rejects(kw, code):
+    assert lin(**kw) == code
+
+
+@pytest.mark.parametrize("kw", [dict(M=0), dict(N=0), dict(M=0, N=0, K=0)])
+def test_masked_linear_empty_is_noop(kw):
+    assert lin(**kw) == _lib.TASQ_OK
+
+
+def test_bitplane_variant_accepts_missing_w_only_with_planes():
+    o = opts(variant=_lib.VARIANT_BITPLANE, W_planes=FAKE)
+    assert lin(W=None, M=0, opts=o) == _lib.TASQ_OK
+    assert lin(W=None, b=0, opts=o) == _lib.TASQ_ERR_BITS
+
+
+def test_conv_rejects():
+    def conv(**kw):
+        a = dict(X=FAKE, W=FAKE, sx=1.0, sw=FAKE, bias=None, H=4, Wd=4, C=16, N=8, b=8,
+                 acc=FAKE, y=FAKE)
+        a.update(kw)
+        return L.tasq_masked_conv3x3(a["X"], a["W"], a["sx"], a["sw"], a["bias"], a["H"],
+                                     a["Wd"], a["C"], a["N"], a["b"], a["acc"], a["y"], None,
+                                     None)
+    assert conv(X=None) == _lib.TASQ_ERR_NULL
+    assert conv(H=-1) == _lib.TASQ_ERR_DIM
+    assert conv(b=0) == _lib.TASQ_ERR_BITS
+    assert conv(C=14564) == _lib.TASQ_ERR_OVERFLOW          # 9 * C > 131071
+    assert conv(H=0) == _lib.TASQ_OK
+    assert conv(acc=None, y=None) == _lib.TASQ_ERR_NULL
+
+
+def test_pack_planes_rejects():
+    assert L.tasq_pack_planes(None, 4, 4, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert L.tasq_pack_planes(FAKE, 4, 4, None, None) == _lib.TASQ_ERR_NULL
+    assert L.tasq_pack_planes(FAKE, -1, 4, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert L.tasq_pack_planes(FAKE, 0, 4, FAKE, None) == _lib.TASQ_OK
+
+
+def layer(**kw):
+    a = Layer()
+    a.kind, a.M, a.N, a.K = _lib.KIND_LINEAR, 4, 4, 32
+    a.sx = 0.02
+    a.X = a.W = a.sw = a.acc = a.y = FAKE
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+def sched(layers, table, S, T, t0, t1, o=None):
+    arr = (Layer * len(layers))(*layers)
+    tab = (ctypes.c_uint8 * max(1, len(table)))(*table)
+    return L.tasq_run_schedule(arr, len(layers), tab, S, T, t0, t1,
+                               ctypes.byref(o) if o is not None else None, None)
+
+
+def test_schedule_rejects_before_launching():
+    good = [layer(), layer()]
+    tbl = [8, 7, 6, 5, 4, 3, 2, 1]
+    assert sched(good, tbl, 4, 20, 0, 0) == _lib.TASQ_OK              # empty step range
+    assert sched([], [], 4, 20, 0, 20) == _lib.TASQ_OK                 # no layers
+    assert sched(good, tbl, 0, 20, 0, 20) == _lib.TASQ_ERR_RANGE
+    assert sched(good, tbl, 5, 4, 0, 4) == _lib.TASQ_ERR_RANGE
+    assert sched(good, tbl, 4, 20, 3, 2) == _lib.TASQ_ERR_RANGE
+    assert sched(good, tbl, 4, 20, 0, 21) == _lib.TASQ_ERR_RANGE
+    assert sched(good, tbl, 4, 20, -1, 2) == _lib.TASQ_ERR_RANGE
+    # one bad table entry anywhere fails the whole call, whatever the range
+    assert sched(good, [8, 7, 6, 5, 4, 3, 2, 0], 4, 20, 0, 1) == _lib.TASQ_ERR_BITS
+    assert sched(good, [8, 7, 6, 5, 4, 9, 2, 1], 4, 20, 0, 1) == _lib.TASQ_ERR_BITS
+    # a bad layer anywhere fails the whole call
+    assert sched([layer(), layer(X=None)], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_NULL
+    assert sched([layer(), layer(K=200000)], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_OVERFLOW
+    assert sched([layer(kind=5), layer()], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_KIND
+    bad_conv = layer(kind=_lib.KIND_CONV3X3, H=2, Wd=2, C=16, M=5, K=144)
+    assert sched([bad_conv, layer()], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_DIM
+    assert sched(good, tbl, 4, 20, 0, 1, opts(workspace=FAKE + 16, workspace_bytes=1 << 20)) \
+        == _lib.TASQ_ERR_ALIGN
+    assert L.tasq_run_schedule(None, 2, None, 4, 20, 0, 1, None, None) == _lib.TASQ_ERR_NULL
+    assert L.tasq_run_schedule(None, -1, None, 4, 20, 0, 1, None, None) == _lib.TASQ_ERR_RANGE
+
+
+def test_schedule_workspace_bytes_grows_with_layers():
+    a = L.tasq_schedule_workspace_bytes((Layer * 1)(layer()), 1)
+    b = L.tasq_schedule_workspace_bytes((Layer * 112)(*[layer()] * 112), 112)
+    assert 0 < a <= b and a % 256 == 0 and b % 256 == 0

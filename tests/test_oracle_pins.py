@@ -243,27 +243,46 @@ def test_conv_single_tap():
     np.testing.assert_array_equal(acc.reshape(-1, Co), lin)
 
 
+def test_conv_entries_match_full():
+    H, Wd, Ci, Co = 5, 6, 7, 9
+    X = rand_i8((H, Wd, Ci))
+    Wt = rand_i8((Co, 3, 3, Ci))
+    sw = RNG.uniform(1e-3, 1e-2, Co).astype(np.float32)
+    bias = RNG.uniform(-1, 1, Co).astype(np.float32)
+    pix = RNG.integers(0, H * Wd, 60)
+    cols = RNG.integers(0, Co, 60)
+    for b in (8, 4):
+        acc, y = oracle.conv3x3(X, Wt, 0.02, sw, b, bias)
+        ea, ey = oracle.conv3x3_entries(X, Wt, 0.02, sw, b, pix, cols, bias)
+        np.testing.assert_array_equal(ea, acc.reshape(-1, Co)[pix, cols])
+        np.testing.assert_array_equal(ey, y.reshape(-1, Co)[pix, cols])
+
+
 # ---------------------------------------------------------------- bit planes
 
 def unpack(planes, K):
     """Bit plane q (q = 7 - p) back to a {0,1} int64 array [8 x N x K]."""
-    Q, N, KW = planes.shape
+    Q, KB, N, _ = planes.shape
     j = np.arange(K)
-    return ((planes[:, :, j // 32].astype(np.int64) >> (j % 32)) & 1)
+    blk = planes[:, j // 128, :, :]                          # [8, K, N, 4]
+    w = ((j % 128) // 32)[None, :, None, None]
+    words = np.take_along_axis(blk, np.broadcast_to(w, blk.shape[:3] + (1,)), 3)[..., 0]
+    bits = (words.astype(np.int64) >> (j % 32)[None, :, None]) & 1
+    return bits.transpose(0, 2, 1)
 
 
-@pytest.mark.parametrize("N,K", [(1, 1), (5, 31), (7, 32), (3, 100)])
+@pytest.mark.parametrize("N,K", [(1, 1), (5, 31), (7, 32), (3, 100), (4, 300)])
 def test_planes_round_trip(N, K):
     W = rand_i8((N, K))
     W[0, 0] = -128
     planes = oracle.pack_planes(W)
-    assert planes.shape == (8, N, (K + 31) // 32)
+    assert planes.shape == (8, (K + 127) // 128, N, 4)
     bits = unpack(planes, K)
     coef = np.array([-128] + [1 << p for p in range(6, -1, -1)])   # q = 0 is the sign plane
     np.testing.assert_array_equal(np.tensordot(coef, bits, 1), W.astype(np.int64))
-    # words past K are zero
-    if K % 32:
-        assert np.all(planes[:, :, -1] >> (K % 32) == 0)
+    # every bit past K is zero: the total popcount equals that of the K elements
+    total = sum(bin(int(v)).count("1") for v in planes.reshape(-1))
+    assert total == int(bits.sum())
 
 
 @pytest.mark.parametrize("b", range(1, 9))
