@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtasq.so")
 OBJDIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["masked_gemm.hip", "pack_planes.hip", "tasq_api.cpp"]
+SOURCES = ["tile_256x256_k64_w8_pf2.hip", "tile_256x256_k64_w8_pf3.hip", "tile_256x256_k128_w8_pf1.hip", "tile_128x128_k128_w4_pf2.hip", "tile_64x64_k128_w4_pf2.hip", "tile_128x128_k64_w4_pf3.hip", "tile_256x128_k64_w4_pf2.hip", "tile_128x256_k64_w4_pf2.hip", "pack_planes.hip", "tiles.cpp", "tasq_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -33,7 +33,7 @@ def _compile(src: str) -> str:
 
 def build() -> str:
     os.makedirs(OBJDIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
+    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     subprocess.check_call([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs,

@@ -1,0 +1,607 @@
+// Masked int8 GEMM for gfx950 (CDNA4).
+//
+// acc[m][n] = sum_k X[m][k] * W_b[n][k],  W_b = W & keep_mask(b)
+// y[m][n]   = float(acc) * (sx * sw[n]) (+ bias[n])
+//
+// The LSB mask (TASQ Sec. 3.2.1 Eq. lsb_masking, App. G.2 Eq. hw_rightshift)
+// is one v_and_b32 per four weights, applied while a weight tile passes
+// through registers between the global load and the LDS store; the MFMA
+// main loop never sees an unmasked weight and never depends on b, so one
+// compiled kernel serves every precision (App. G.1).
+//
+// Structure:
+//   * block tile BM x BN over (M, N), K consumed in BK-byte steps;
+//   * global -> VGPR (16-byte loads, mask on the weight side) -> LDS, double
+//     buffered with one barrier per K step, next tile's loads issued before
+//     the current tile's MFMAs;
+//   * LDS rows of BK bytes, 16-byte chunks XOR-swizzled so that the 32 rows
+//     one MFMA operand read touches fall in distinct banks;
+//   * each wave owns a (BM/WAVES_M) x (BN/WAVES_N) sub-tile of
+//     v_mfma_i32_32x32x32_i8 accumulators (int32, exact);
+//   * epilogue straight from the accumulators: lane l of a 32x32 block holds
+//     column l%32, so every store instruction writes full 128-byte row
+//     segments.
+#pragma once
+
+#include "tasq_internal.h"
+
+namespace tasq {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int PF_ = 2, int OCC_ = 2>
+struct Cfg {
+    static constexpr int OCC = OCC_;                    // target waves per SIMD
+    static constexpr int BM = BM_, BN = BN_, BK = BK_;
+    static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
+    static constexpr int PF = PF_;                      // K tiles in flight in registers
+    static constexpr int NT = WAVES_M * WAVES_N * 64;
+    static constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
+    static constexpr int FM = WTM / 32, FN = WTN / 32;
+    static constexpr int CPR = BK / 16;                 // 16-byte chunks per row
+    static constexpr int A_LOADS = BM * CPR / NT;
+    static constexpr int B_LOADS = BN * CPR / NT;
+    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must hold 32x32 blocks");
+    static_assert(BK % 32 == 0 && (CPR == 4 || CPR == 8), "BK must be 64 or 128");
+    static_assert((BM * CPR) % NT == 0 && (BN * CPR) % NT == 0, "loads must divide");
+};
+
+// Physical 16-byte chunk of logical chunk c in LDS row r.  For 128-byte rows
+// (8 chunks) rows 0..7 map a fixed c to 8 distinct chunks, and rows of equal
+// parity among 0..15 as well, so a 32-row operand read is conflict free for
+// both 128-byte and 256-byte bank windows; likewise for 64-byte rows.
+template <int CPR>
+__device__ __forceinline__ int swz(int r, int c)
+{
+    if constexpr (CPR == 8)
+        return c ^ ((r & 7) ^ ((r >> 3) & 1));
+    else
+        return c ^ (((r >> 1) ^ (r >> 3)) & 3);
+}
+
+// ---------------------------------------------------------------- buffers
+
+// Raw buffer resources: a load whose byte offset is at or past num_records
+// returns zero and such a store is dropped, which bounds every access to
+// its operand without per-element checks.  Offsets are 32-bit; the host
+// keeps every operand below 2 GiB and kOOB marks a lane with nothing to do.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void *p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+__device__ __forceinline__ v4i ld16(rsrc_t r, uint32_t off)
+{
+    return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+__device__ __forceinline__ void st32(rsrc_t r, uint32_t off, uint32_t v)
+{
+    __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 0);
+}
+
+__device__ __forceinline__ v4i zero4() { return v4i{0, 0, 0, 0}; }
+
+// ------------------------------------------------- fallback (unaligned) loads
+
+// 16 bytes at p[0..15]; bytes with index >= valid read as zero.
+__device__ __forceinline__ v4i load_bytes(const int8_t *p, int valid)
+{
+    uint32_t w[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+        if (i < valid)
+            w[i >> 2] |= (uint32_t)(uint8_t)p[i] << (8 * (i & 3));
+    return v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+}
+
+// Chunk (row, kbyte..kbyte+15) of a row-major [rows][K] int8 matrix, any K.
+__device__ __forceinline__ v4i load_rowmajor_any(const int8_t *base, int rows, int K, int row,
+                                                 int kbyte)
+{
+    if (row >= rows || kbyte >= K)
+        return zero4();
+    return load_bytes(base + (size_t)row * (size_t)K + kbyte, K - kbyte);
+}
+
+// Chunk of the implicit-GEMM activation of a 3x3 / pad 1 conv for any C:
+// element k of row m = h*Wd + w is X[h + r - 1][w + s - 1][ci] with
+// k = (r*3 + s)*C + ci, or 0 in the padding.
+__device__ __forceinline__ v4i load_conv_any(const LayerDesc &d, int m, int kbyte)
+{
+    if (m >= d.M || kbyte >= d.K)
+        return zero4();
+    uint32_t w[4] = {0, 0, 0, 0};
+    const int h = m / d.Wd, x = m - (m / d.Wd) * d.Wd;
+    for (int i = 0; i < 16 && kbyte + i < d.K; ++i) {
+        const int k = kbyte + i;
+        const int tap = k / d.C, ci = k - (k / d.C) * d.C;
+        const int hh = h + tap / 3 - 1, ww = x + tap % 3 - 1;
+        if (hh >= 0 && hh < d.H && ww >= 0 && ww < d.Wd)
+            w[i >> 2] |= (uint32_t)(uint8_t)d.X[((size_t)hh * d.Wd + ww) * (size_t)d.C + ci]
+                         << (8 * (i & 3));
+    }
+    return v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+}
+
+// ----------------------------------------------------------- bit planes
+
+// Bit i of x (i < 4) moved to bit 8*i: x * (1 + 2^7 + 2^14 + 2^21) places
+// bit i at positions i + 7j, which are all distinct for i, j < 4, and only
+// j = i lands on a multiple of 8.
+__device__ __forceinline__ uint32_t spread4(uint32_t x)
+{
+    return (x * 0x00204081u) & 0x01010101u;
+}
+
+// Chunk (row n, kbyte..kbyte+15) of W_b rebuilt from the top b bit planes
+// (App. G.2: the b-bit operand is the top b planes of the stored buffer;
+// the dropped planes are never read).  Plane q contributes bit 7 - q of
+// each byte; the result is the two's-complement byte of W_b.
+__device__ __forceinline__ v4i load_planes(const uint32_t *P, int N, int K, int b, int n,
+                                           int kbyte)
+{
+    if (n >= N || kbyte >= K)
+        return zero4();
+    const int KB = (K + 127) >> 7;
+    const size_t plane_stride = (size_t)KB * (size_t)N * 4;
+    const uint32_t *base = P + ((size_t)(kbyte >> 7) * N + n) * 4 + ((kbyte & 127) >> 5);
+    const int sh = (kbyte & 16);
+    uint32_t d0 = 0, d1 = 0, d2 = 0, d3 = 0;
+    for (int q = 0; q < b; ++q) {
+        const uint32_t half = base[q * plane_stride] >> sh;
+        const int up = 7 - q;
+        d0 |= spread4(half & 0xF) << up;
+        d1 |= spread4((half >> 4) & 0xF) << up;
+        d2 |= spread4((half >> 8) & 0xF) << up;
+        d3 |= spread4((half >> 12) & 0xF) << up;
+    }
+    return v4i{(int)d0, (int)d1, (int)d2, (int)d3};
+}
+
+// ------------------------------------------------------------------ staging
+
+// Where this thread's chunks of a K tile live.  Thread tid owns chunks
+// id = tid + i*NT: row id / CPR, 16-byte column id % CPR of the tile.  In
+// the ALIGNED path (K % 16 == 0, 16-byte aligned operands) a chunk's buffer
+// offset is fixed per tile and advanced by the K step; rows past M (N)
+// carry kOOB and read zero.  Columns past K are not masked here: the final
+// K tile zeroes the weight fragments past K before its MFMAs.
+template <class C, bool ALIGNED, int KIND, bool PLANES>
+struct Plan {
+    rsrc_t rX, rW;
+    uint32_t offA[C::A_LOADS];   // linear: byte offset at k = kb; conv: pixel base
+    uint32_t offB[C::B_LOADS];
+    int hA[C::A_LOADS], wA[C::A_LOADS];   // conv: pixel coordinates
+
+    __device__ __forceinline__ void init(const LayerDesc &d, int m0, int n0, int kb, int tid)
+    {
+        if constexpr (ALIGNED) {
+            if constexpr (KIND == KIND_CONV3X3)
+                rX = make_rsrc(d.X, (uint32_t)d.H * (uint32_t)d.Wd * (uint32_t)d.C);
+            else
+                rX = make_rsrc(d.X, (uint32_t)d.M * (uint32_t)d.K);
+#pragma unroll
+            for (int i = 0; i < C::A_LOADS; ++i) {
+                const int id = tid + i * C::NT;
+                const int m = m0 + id / C::CPR, c = id % C::CPR;
+                if constexpr (KIND == KIND_CONV3X3) {
+                    const bool ok = m < d.M;
+                    const int h = ok ? m / d.Wd : -(1 << 20);
+                    const int w = ok ? m - (m / d.Wd) * d.Wd : -(1 << 20);
+                    hA[i] = h;
+                    wA[i] = w;
+                    offA[i] = ok ? (uint32_t)((h * d.Wd + w) * d.C) : 0u;
+                } else {
+                    offA[i] = m < d.M ? (uint32_t)m * (uint32_t)d.K + (uint32_t)(kb + 16 * c)
+                                      : kOOB;
+                }
+            }
+            if constexpr (!PLANES) {
+                rW = make_rsrc(d.W, (uint32_t)d.N * (uint32_t)d.K);
+#pragma unroll
+                for (int i = 0; i < C::B_LOADS; ++i) {
+                    const int id = tid + i * C::NT;
+                    const int n = n0 + id / C::CPR, c = id % C::CPR;
+                    offB[i] = n < d.N ? (uint32_t)n * (uint32_t)d.K + (uint32_t)(kb + 16 * c)
+                                      : kOOB;
+                }
+            }
+        }
+    }
+
+    // Implicit-GEMM chunk for C % 16 == 0: the chunk lies in one tap
+    // (r, s); out-of-image taps, pixels past M and columns past K read zero.
+    // When C is a multiple of BK the whole K tile lies in one tap, found once
+    // (uniform) from the tile start k0.
+    __device__ __forceinline__ v4i conv_chunk(const LayerDesc &d, int i, int k0, int c) const
+    {
+        const int kbyte = k0 + 16 * c;
+        if (kbyte >= d.K)
+            return zero4();
+        int tap, ci;
+        if (d.C % C::BK == 0) {
+            tap = k0 / d.C;
+            ci = k0 - tap * d.C + 16 * c;
+        } else {
+            tap = kbyte / d.C;
+            ci = kbyte - tap * d.C;
+        }
+        const int r = tap / 3, s = tap - 3 * (tap / 3);
+        const int hh = hA[i] + r - 1, ww = wA[i] + s - 1;
+        const bool ok = (unsigned)hh < (unsigned)d.H && (unsigned)ww < (unsigned)d.Wd;
+        const int delta = ((r - 1) * d.Wd + (s - 1)) * d.C + ci;
+        return ld16(rX, ok ? (uint32_t)((int)offA[i] + delta) : kOOB);
+    }
+};
+
+// One K tile of both operands held in registers between its global load and
+// its LDS store.
+template <class C, bool ALIGNED, int KIND, bool PLANES>
+struct Regs {
+    v4i a[C::A_LOADS];
+    v4i b[C::B_LOADS];
+
+    // Loads the K tile at absolute byte k0 = kb + kt.
+    __device__ __forceinline__ void load(const Plan<C, ALIGNED, KIND, PLANES> &p,
+                                         const LayerDesc &d, int m0, int n0, int k0, uint32_t kt,
+                                         int tid)
+    {
+#pragma unroll
+        for (int i = 0; i < C::A_LOADS; ++i) {
+            const int id = tid + i * C::NT;
+            const int r = id / C::CPR, c = id % C::CPR;
+            if constexpr (!ALIGNED) {
+                if constexpr (KIND == KIND_CONV3X3)
+                    a[i] = load_conv_any(d, m0 + r, k0 + 16 * c);
+                else
+                    a[i] = load_rowmajor_any(d.X, d.M, d.K, m0 + r, k0 + 16 * c);
+            } else if constexpr (KIND == KIND_CONV3X3) {
+                a[i] = p.conv_chunk(d, i, k0, c);
+            } else {
+                a[i] = ld16(p.rX, p.offA[i] + kt);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < C::B_LOADS; ++i) {
+            const int id = tid + i * C::NT;
+            const int r = id / C::CPR, c = id % C::CPR;
+            if constexpr (PLANES)
+                b[i] = load_planes(d.P, d.N, d.K, d.bits, n0 + r, k0 + 16 * c);
+            else if constexpr (!ALIGNED)
+                b[i] = load_rowmajor_any(d.W, d.N, d.K, n0 + r, k0 + 16 * c);
+            else
+                b[i] = ld16(p.rW, p.offB[i] + kt);
+        }
+    }
+
+    __device__ __forceinline__ void store(v4i *sA, v4i *sB, uint32_t wmask, int tid) const
+    {
+        const int msk = (int)wmask;
+#pragma unroll
+        for (int i = 0; i < C::A_LOADS; ++i) {
+            const int id = tid + i * C::NT;
+            const int r = id / C::CPR, c = id % C::CPR;
+            sA[r * C::CPR + swz<C::CPR>(r, c)] = a[i];
+        }
+#pragma unroll
+        for (int i = 0; i < C::B_LOADS; ++i) {
+            const int id = tid + i * C::NT;
+            const int r = id / C::CPR, c = id % C::CPR;
+            v4i v = b[i];
+            if constexpr (!PLANES) {
+                v.x &= msk;
+                v.y &= msk;
+                v.z &= msk;
+                v.w &= msk;
+            }
+            sB[r * C::CPR + swz<C::CPR>(r, c)] = v;
+        }
+    }
+};
+
+// Accumulates the K range [kb, ke) of tile (m0, n0) into acc.
+//
+// Pipeline: LDS holds two K tiles (compute one, fill the other) and
+// registers hold the next PF tiles, so the global load of tile t+1+PF is
+// issued right after tile t+1 leaves registers for LDS and has PF compute
+// steps to arrive.  One barrier per K tile.
+template <class C, bool ALIGNED, int KIND, bool PLANES = false>
+__device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int m0, int n0,
+                                         int kb, int ke, v16i (&acc)[C::FM][C::FN],
+                                         v4i *smA, v4i *smB)
+{
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+    constexpr int SA = C::BM * C::CPR, SB = C::BN * C::CPR;
+
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+            acc[i][j] = v16i{};
+
+    const int span = ke - kb;
+    const int nk = (span + C::BK - 1) / C::BK;
+    if (nk <= 0)
+        return;
+    // valid bytes of the last K tile (BK when K fills it)
+    const int last_valid = span - (nk - 1) * C::BK;
+
+    Plan<C, ALIGNED, KIND, PLANES> plan;
+    plan.init(d, m0, n0, kb, tid);
+    Regs<C, ALIGNED, KIND, PLANES> ring[C::PF];
+
+    ring[0].load(plan, d, m0, n0, kb, 0u, tid);
+    ring[0].store(smA, smB, wmask, tid);
+#pragma unroll
+    for (int u = 0; u < C::PF; ++u)
+        if (1 + u < nk)
+            ring[u].load(plan, d, m0, n0, kb + (1 + u) * C::BK, (uint32_t)(1 + u) * C::BK, tid);
+    __syncthreads();
+
+    // MFMAs over the K tile in LDS buffer `buf`; with `tail`, weight bytes at
+    // or past column `last_valid` of the tile are zeroed first (the loads
+    // there may hold the next row or zero).  Fragments are double-buffered:
+    // the LDS reads of sub-step kk+1 are in flight while sub-step kk's MFMAs
+    // issue.
+    auto compute = [&](int buf, bool tail) {
+        const v4i *A = smA + buf * SA;
+        const v4i *B = smB + buf * SB;
+        constexpr int KK = C::BK / 32;
+        v4i fa[2][C::FM], fb[2][C::FN];
+        auto read = [&](int kk, v4i (&a)[C::FM], v4i (&b)[C::FN]) {
+            const int c = 2 * kk + (lane >> 5);
+#pragma unroll
+            for (int i = 0; i < C::FM; ++i) {
+                const int r = wm * C::WTM + i * 32 + (lane & 31);
+                a[i] = A[r * C::CPR + swz<C::CPR>(r, c)];
+            }
+#pragma unroll
+            for (int j = 0; j < C::FN; ++j) {
+                const int r = wn * C::WTN + j * 32 + (lane & 31);
+                b[j] = B[r * C::CPR + swz<C::CPR>(r, c)];
+                if (tail && 16 * c >= last_valid)
+                    b[j] = zero4();
+            }
+        };
+        read(0, fa[0], fb[0]);
+        __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            if (kk + 1 < KK)
+                read(kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
+#pragma unroll
+            for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+                for (int j = 0; j < C::FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[kk & 1][i], fb[kk & 1][j],
+                                                                      acc[i][j], 0, 0, 0);
+            // Issue order: the next sub-step's LDS reads, then this sub-step's
+            // MFMAs (which only wait for the older reads).
+            if (kk + 1 < KK)
+                __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
+        }
+    };
+
+    // Steady state over tiles 0 .. nk-2; ring[t % PF] holds tile t+1.
+    for (int t0 = 0; t0 < nk - 1; t0 += C::PF) {
+#pragma unroll
+        for (int u = 0; u < C::PF; ++u) {
+            const int t = t0 + u;
+            if (t < nk - 1) {
+                compute(t & 1, false);
+                ring[u].store(smA + ((t + 1) & 1) * SA, smB + ((t + 1) & 1) * SB, wmask, tid);
+                if (t + 1 + C::PF < nk) {
+                    const uint32_t off = (uint32_t)(t + 1 + C::PF) * C::BK;
+                    ring[u].load(plan, d, m0, n0, kb + (int)off, off, tid);
+                }
+                __syncthreads();
+            }
+        }
+    }
+    compute((nk - 1) & 1, last_valid < C::BK);
+}
+
+// Writes a finished tile: int32 accumulators and/or the fp32 dequantised
+// value y = float(acc) * (sx * sw[n]) + bias[n].  Register v of a 32x32
+// accumulator in lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32, so
+// each store instruction covers two 128-byte row segments.  Rows past M
+// fall past the buffer end and are dropped; columns past N carry kOOB.
+template <class C>
+__device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
+                                         const v16i (&acc)[C::FM][C::FN])
+{
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+    const uint32_t outb = (uint32_t)d.M * (uint32_t)d.N * 4u;
+    const rsrc_t ry = make_rsrc(d.y, d.y ? outb : 0u);
+    const rsrc_t ra = make_rsrc(d.acc, d.acc ? outb : 0u);
+    const uint32_t rowb = (uint32_t)d.N * 4u;
+    const int mrow = m0 + wm * C::WTM + 4 * (lane >> 5);
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+        const int n = n0 + wn * C::WTN + j * 32 + (lane & 31);
+        const bool nok = n < d.N;
+        float scale = 0.f, bias = 0.f;
+        if (nok) {
+            scale = d.sx * d.sw[n];
+            if (d.bias)
+                bias = d.bias[n];
+        }
+        const uint32_t base = nok ? ((uint32_t)mrow * (uint32_t)d.N + (uint32_t)n) * 4u : kOOB;
+        if (d.acc) {
+#pragma unroll
+            for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    st32(ra, base + (uint32_t)(i * 32 + 8 * (v >> 2) + (v & 3)) * rowb,
+                         (uint32_t)acc[i][j][v]);
+        }
+        if (d.y) {
+#pragma unroll
+            for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    st32(ry, base + (uint32_t)(i * 32 + 8 * (v >> 2) + (v & 3)) * rowb,
+                         __builtin_bit_cast(uint32_t, (float)acc[i][j][v] * scale + bias));
+        }
+    }
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs (workgroup i runs on
+// XCD i % 8), each with its own L2.  This bijection of [0, G) gives every XCD
+// one contiguous range of logical tiles, so neighbouring tiles -- which share
+// activation rows and weight columns -- meet in the same L2.
+__device__ __forceinline__ int xcd_remap(int pid, int G)
+{
+    constexpr int NX = 8;
+    const int per = (G + NX - 1) / NX;
+    int tall = G % NX;
+    if (tall == 0)
+        tall = NX;
+    const int xcd = pid % NX, local = pid / NX;
+    if (xcd < tall)
+        return xcd * per + local;
+    return tall * per + (xcd - tall) * (per - 1) + local;
+}
+
+// Tile order within a layer: groups of GROUP_M tile rows are walked column by
+// column, so that consecutive tiles share weight tiles and activation rows.
+__device__ __forceinline__ void tile_coords(int t, int tiles_m, int tiles_n, int &tm, int &tn)
+{
+    constexpr int GROUP_M = 8;
+    const int per_group = GROUP_M * tiles_n;
+    const int g = t / per_group;
+    const int first_m = g * GROUP_M;
+    const int gm = min(tiles_m - first_m, GROUP_M);
+    const int in = t - g * per_group;
+    tm = first_m + in % gm;
+    tn = in / gm;
+}
+
+template <class C, bool ALIGNED, int KIND, bool PLANES>
+__global__ void __launch_bounds__(C::NT, C::OCC) k_masked_gemm(LayerDesc d)
+{
+    __shared__ v4i smA[2 * C::BM * C::CPR];
+    __shared__ v4i smB[2 * C::BN * C::CPR];
+    int tm, tn;
+    tile_coords(xcd_remap(blockIdx.x, gridDim.x), d.tiles_m, d.tiles_n, tm, tn);
+    const int m0 = tm * C::BM, n0 = tn * C::BN;
+    v16i acc[C::FM][C::FN];
+    mainloop<C, ALIGNED, KIND, PLANES>(d, keep_mask_dword(d.bits), m0, n0, 0, d.K, acc, smA,
+                                       smB);
+    epilogue<C>(d, m0, n0, acc);
+}
+
+// Grouped launch over every layer of one denoising step: workgroup t finds
+// its layer by binary search over the tile prefix, and that layer's b from
+// the (layer, stage) table (App. G.1: a table lookup, no re-launch).
+template <class C>
+__global__ void __launch_bounds__(C::NT, C::OCC)
+k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *table, int S,
+                      int stage)
+{
+    __shared__ v4i smA[2 * C::BM * C::CPR];
+    __shared__ v4i smB[2 * C::BN * C::CPR];
+    const int t = xcd_remap(blockIdx.x, gridDim.x);
+    int lo = 0, hi = L - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (descs[mid].tile_begin <= t)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    const LayerDesc d = descs[lo];
+    const uint32_t wmask = keep_mask_dword(table[lo * S + stage]);
+    int tm, tn;
+    tile_coords(t - d.tile_begin, d.tiles_m, d.tiles_n, tm, tn);
+    const int m0 = tm * C::BM, n0 = tn * C::BN;
+    v16i acc[C::FM][C::FN];
+    if (d.kind == KIND_CONV3X3)
+        mainloop<C, true, KIND_CONV3X3>(d, wmask, m0, n0, 0, d.K, acc, smA, smB);
+    else
+        mainloop<C, true, KIND_LINEAR>(d, wmask, m0, n0, 0, d.K, acc, smA, smB);
+    epilogue<C>(d, m0, n0, acc);
+}
+
+// ---------------------------------------------------------------- launchers
+
+template <class C>
+static void fill_tiles(LayerDesc &d)
+{
+    d.tiles_m = (d.M + C::BM - 1) / C::BM;
+    d.tiles_n = (d.N + C::BN - 1) / C::BN;
+}
+
+template <class C>
+hipError_t launch_single_cfg(const LayerDesc &din, bool aligned, hipStream_t stream)
+{
+    LayerDesc d = din;
+    fill_tiles<C>(d);
+    const long long grid = (long long)d.tiles_m * d.tiles_n;
+    if (grid > 0x7fffffffLL)
+        return hipErrorInvalidValue;
+    dim3 g((unsigned)grid), b(C::NT);
+    if (d.kind == KIND_CONV3X3) {
+        if (aligned)
+            hipLaunchKernelGGL((k_masked_gemm<C, true, KIND_CONV3X3, false>), g, b, 0, stream, d);
+        else
+            hipLaunchKernelGGL((k_masked_gemm<C, false, KIND_CONV3X3, false>), g, b, 0, stream,
+                               d);
+    } else if (aligned) {
+        hipLaunchKernelGGL((k_masked_gemm<C, true, KIND_LINEAR, false>), g, b, 0, stream, d);
+    } else {
+        hipLaunchKernelGGL((k_masked_gemm<C, false, KIND_LINEAR, false>), g, b, 0, stream, d);
+    }
+    return hipGetLastError();
+}
+
+template <class C>
+hipError_t launch_planes_cfg(const LayerDesc &din, bool aligned, hipStream_t stream)
+{
+    LayerDesc d = din;
+    fill_tiles<C>(d);
+    const long long grid = (long long)d.tiles_m * d.tiles_n;
+    if (grid > 0x7fffffffLL)
+        return hipErrorInvalidValue;
+    dim3 g((unsigned)grid), b(C::NT);
+    if (aligned)
+        hipLaunchKernelGGL((k_masked_gemm<C, true, KIND_LINEAR, true>), g, b, 0, stream, d);
+    else
+        hipLaunchKernelGGL((k_masked_gemm<C, false, KIND_LINEAR, true>), g, b, 0, stream, d);
+    return hipGetLastError();
+}
+
+template <class C>
+hipError_t launch_grouped_cfg(const LayerDesc *d_descs, int L, int total_tiles,
+                              const uint8_t *d_table, int S, int stage, hipStream_t stream)
+{
+    dim3 g((unsigned)total_tiles), b(C::NT);
+    hipLaunchKernelGGL((k_masked_gemm_grouped<C>), g, b, 0, stream, d_descs, L, d_table, S,
+                       stage);
+    return hipGetLastError();
+}
+
+// Defines the dispatch entry of one tile configuration (a host function, so
+// the table of host launchers never reaches the device compilation).
+#define TASQ_DEFINE_TILE(NAME, CFG)                                                         \
+    const TileOps &NAME()                                                                   \
+    {                                                                                       \
+        static const TileOps ops = {{CFG::BM, CFG::BN, CFG::BK}, &launch_single_cfg<CFG>,   \
+                                    &launch_planes_cfg<CFG>, &launch_grouped_cfg<CFG>};     \
+        return ops;                                                                         \
+    }
+
+}  // namespace tasq

@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -46,17 +47,51 @@ int check_variant(const tasq_opts *o, const int8_t *W)
     return TASQ_OK;
 }
 
-// Tile used for a single (non-grouped) launch.  Small problems take small
-// tiles so that more workgroups cover the 256 compute units.
+// TASQ_TILE=<id> forces one tile configuration (tuning sweeps only).
+int forced_tile()
+{
+    const char *e = std::getenv("TASQ_TILE");
+    if (!e || !*e)
+        return -1;
+    const int t = std::atoi(e);
+    return (t >= 0 && t < tasq::TILE_COUNT) ? t : -1;
+}
+
+// Tile used for a single (non-grouped) launch, from the measured sweep on
+// the DiT/UNet layer shapes: 256x256 tiles (8 waves, BK 128) while they still
+// give at least one tile per compute unit, 128x128 tiles for mid-size
+// problems, 64x64 tiles below that so that more workgroups cover the 256
+// compute units.
 int pick_tile(long long M, long long N)
 {
+    const int f = forced_tile();
+    if (f >= 0)
+        return f;
+    const long long t256 = ((M + 255) / 256) * ((N + 255) / 256);
     const long long t128 = ((M + 127) / 128) * ((N + 127) / 128);
+    if (t256 >= 256)
+        return tasq::TILE_256x256_K128_W8_PF1;
     if (t128 >= 256)
-        return tasq::TILE_128x128;
-    return tasq::TILE_64x64;
+        return tasq::TILE_128x128_K128_W4_PF2;
+    return tasq::TILE_64x64_K128_W4_PF2;
+}
+
+// Tile of the grouped per-step launch.
+int pick_grouped_tile()
+{
+    const int f = forced_tile();
+    return f >= 0 ? f : tasq::TILE_256x256_K128_W8_PF1;
 }
 
 bool use_bitplane(const tasq_opts *o) { return o && o->variant == TASQ_VARIANT_BITPLANE; }
+
+// The buffer-offset fast path also needs each input below 2 GiB.
+bool fits_buffers(const LayerDesc &d)
+{
+    const long long xb = d.kind == tasq::KIND_CONV3X3 ? (long long)d.H * d.Wd * d.C
+                                                       : (long long)d.M * d.K;
+    return xb < (1LL << 31) && (long long)d.N * d.K < (1LL << 31);
+}
 
 int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
 {
@@ -64,14 +99,16 @@ int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
         return TASQ_OK;
     hipError_t e;
     if (use_bitplane(o)) {
-        e = tasq::launch_bitplane(d, (d.K % 16) == 0 && aligned16(d.X), stream);
+        e = tasq::tile_ops(tasq::TILE_64x64_K128_W4_PF2).planes(
+            d, (d.K % 16) == 0 && aligned16(d.X) && fits_buffers(d), stream);
     } else {
         bool aligned;
         if (d.kind == tasq::KIND_CONV3X3)
             aligned = (d.C % 16) == 0 && aligned16(d.X) && aligned16(d.W);
         else
             aligned = (d.K % 16) == 0 && aligned16(d.X) && aligned16(d.W);
-        e = tasq::launch_single(d, pick_tile(d.M, d.N), aligned, nullptr, stream);
+        aligned = aligned && fits_buffers(d);
+        e = tasq::tile_ops(pick_tile(d.M, d.N)).single(d, aligned, stream);
     }
     return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
 }
@@ -126,8 +163,14 @@ int validate_layer(const tasq_layer &L, const tasq_opts *o)
         if (use_bitplane(&local))
             return TASQ_ERR_LAYOUT;     // the bit-plane kernel covers linear layers
     }
-    return check_dims(L.M, L.N, L.K);
+    if (int rc = check_dims(L.M, L.N, L.K))
+        return rc;
+    // Outputs are written through 32-bit buffer offsets (see gemm_core.h).
+    if (((long long)L.M + 256) * (long long)L.N * 4 >= (1LL << 31))
+        return TASQ_ERR_DIM;
+    return TASQ_OK;
 }
+
 
 }  // namespace
 
@@ -300,11 +343,11 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         const bool ok = d.kind == tasq::KIND_CONV3X3
                             ? (d.C % 16 == 0 && aligned16(d.X) && aligned16(d.W))
                             : (d.K % 16 == 0 && aligned16(d.X) && aligned16(d.W));
-        grouped = ok;
+        grouped = ok && fits_buffers(d);
     }
     if (grouped) {
-        const int tile = tasq::TILE_128x128;
-        const tasq::TileShape ts = tasq::tile_shape(tile);
+        const tasq::TileOps &ops = tasq::tile_ops(pick_grouped_tile());
+        const tasq::TileShape ts = ops.shape;
         long long total = 0;
         for (int l = 0; l < L; ++l) {
             LayerDesc &d = descs[l];
@@ -333,8 +376,7 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
             return TASQ_ERR_HIP;
         for (int t = t_begin; t < t_end; ++t) {
             const int s = tasq_stage_of_step(t, S, T);
-            if (tasq::launch_grouped(d_descs, L, (int)total, d_table, S, s, tile, st) !=
-                hipSuccess)
+            if (ops.grouped(d_descs, L, (int)total, d_table, S, s, st) != hipSuccess)
                 return TASQ_ERR_HIP;
         }
         return TASQ_OK;

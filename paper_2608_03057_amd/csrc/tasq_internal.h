@@ -40,32 +40,34 @@ __host__ __device__ inline uint32_t keep_mask_dword(int b)
     return m * 0x01010101u;
 }
 
-// Tile configurations the launchers know about.
-enum TileId : int {
-    TILE_256x256 = 0,
-    TILE_128x256 = 1,
-    TILE_128x128 = 2,
-    TILE_64x64 = 3,
-    TILE_COUNT = 4
-};
-
 struct TileShape {
     int bm, bn, bk;
 };
-TileShape tile_shape(int tile);
 
-// Host-side launchers (masked_gemm.hip).
-hipError_t launch_single(const LayerDesc &d, int tile, bool aligned, void *ws,
-                         hipStream_t stream);
-hipError_t launch_grouped(const LayerDesc *d_descs, int L, int total_tiles,
-                          const uint8_t *d_table, int S, int stage, int tile,
-                          hipStream_t stream);
+// Launchers of one tile configuration (one translation unit each).
+struct TileOps {
+    TileShape shape;
+    hipError_t (*single)(const LayerDesc &d, bool aligned, hipStream_t stream);
+    hipError_t (*planes)(const LayerDesc &d, bool aligned, hipStream_t stream);
+    hipError_t (*grouped)(const LayerDesc *d_descs, int L, int total_tiles,
+                          const uint8_t *d_table, int S, int stage, hipStream_t stream);
+};
+
+// Tile configurations, indexed by TileId.
+enum TileId : int {
+    TILE_256x256_K64_W8_PF2 = 0,   // 256x256 tile, 8 waves (128x64 per wave), BK 64, 2 K tiles in flight
+    TILE_256x256_K64_W8_PF3 = 1,   // 256x256 tile, 8 waves, BK 64, 3 K tiles in flight
+    TILE_256x256_K128_W8_PF1 = 2,   // 256x256 tile, 8 waves, BK 128, 1 K tile in flight
+    TILE_128x128_K128_W4_PF2 = 3,   // 128x128 tile, 4 waves (64x64 per wave), BK 128
+    TILE_64x64_K128_W4_PF2 = 4,   // 64x64 tile, 4 waves (32x32 per wave), BK 128
+    TILE_128x128_K64_W4_PF3 = 5,   // 128x128 tile, 4 waves, BK 64, 3 K tiles in flight
+    TILE_256x128_K64_W4_PF2 = 6,   // 256x128 tile, 4 waves (128x64 per wave), BK 64
+    TILE_128x256_K64_W4_PF2 = 7,   // 128x256 tile, 4 waves (64x128 per wave), BK 64
+    TILE_COUNT = 8
+};
+const TileOps &tile_ops(int tile);
+
 hipError_t launch_pack_planes(const int8_t *W, int N, int K, uint32_t *planes,
                               hipStream_t stream);
-hipError_t launch_bitplane(const LayerDesc &d, bool aligned, hipStream_t stream);
-
-// Bytes of split-K partial sums for a layer (int32 per output of each slice
-// except the last, plus one arrival counter per tile).
-size_t splitk_workspace_bytes(const LayerDesc &d, int tile);
 
 }  // namespace tasq

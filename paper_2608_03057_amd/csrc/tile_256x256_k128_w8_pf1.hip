@@ -1,0 +1,7 @@
+// Masked int8 GEMM instantiated for the 256x256 tile, 8 waves, BK 128, 1 K tile in flight.
+#include "gemm_core.h"
+
+namespace tasq {
+using TileCfg = Cfg<256, 256, 128, 2, 4, 1, 2>;
+TASQ_DEFINE_TILE(ops_tile_256x256_k128_w8_pf1, TileCfg)
+}  // namespace tasq
