@@ -15,6 +15,8 @@ kernel's roofline fraction, and the CPU oracle timed on a bounded sample.
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -36,6 +38,33 @@ PEAK_HBM_GBS = 8000.0
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_masked_gemm_grouped_pixart28_traffic.json")
+
+
+def kernel_source_sha256() -> str:
+    """Hash of the HIP sources; ties recorded counter readings to the code."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2608_03057_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode())
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic():
+    """HBM bytes per grouped launch from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE readings (already scaled by the copy calibration), or None when
+    the kernel sources changed since they were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256") != kernel_source_sha256():
+        return None
+    return rec.get("fetch_bytes_per_launch", 0) + rec.get("write_bytes_per_launch", 0)
 
 
 def build_workload(wl, device):
@@ -124,10 +153,15 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--per-layer", action="store_true",
                     help="launch each layer separately instead of one grouped launch per step")
+    ap.add_argument("--print-source-hash", action="store_true",
+                    help="print the HIP source hash that recorded counter readings refer to")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy a 1 GiB buffer (reference for the FETCH_SIZE/WRITE_SIZE "
                          "counters) and exit")
     args = ap.parse_args()
+    if args.print_source_hash:
+        print(kernel_source_sha256())
+        return
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -168,15 +202,17 @@ def main():
         if t_hbm >= t_mfma:
             ach = gemm_bytes(wl) / (launch_ms * 1e-3) / 1e9
             roof = dict(bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s",
-                        frac=round(ach / PEAK_HBM_GBS, 4), traffic=None)
+                        frac=round(ach / PEAK_HBM_GBS, 4), traffic=recorded_traffic())
         else:
             ach = ops_step / (launch_ms * 1e-3) / 1e12
             roof = dict(bound="mfma", achieved=round(ach, 1), peak=PEAK_INT8_TOPS, unit="TOP/s",
-                        frac=round(ach / PEAK_INT8_TOPS, 4), traffic=None)
+                        frac=round(ach / PEAK_INT8_TOPS, 4), traffic=recorded_traffic())
         roof["kernel"] = "k_masked_gemm_grouped (one launch = one denoising step, 112 GEMMs)"
         roof["launch_ms"] = round(launch_ms, 4)
         roof["mfma_frac"] = round(ops_step / (launch_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)
         roof["roofline_ms"] = round(max(t_mfma, t_hbm) * 1e3, 4)
+        roof["algorithmic_bytes"] = gemm_bytes(wl)
+        roof["algorithmic_ops"] = ops_step
 
     cpu = None
     if not args.no_cpu_baseline:

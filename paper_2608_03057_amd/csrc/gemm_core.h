@@ -80,9 +80,13 @@ __device__ __forceinline__ v4i ld16(rsrc_t r, uint32_t off)
     return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
+// Output stores carry the non-temporal hint (cache-policy bit 1 on gfx950):
+// the outputs are written once and never re-read by the kernel, and without
+// the hint they evict the activation and weight tiles that neighbouring
+// workgroups are still reading from L2.
 __device__ __forceinline__ void st32(rsrc_t r, uint32_t off, uint32_t v)
 {
-    __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 2);
 }
 
 __device__ __forceinline__ v4i zero4() { return v4i{0, 0, 0, 0}; }
