@@ -196,7 +196,8 @@ def conv3x3_entries(X, Wt, sx, sw, b, pix, cols, bias=None):
 
 def pack_planes(W) -> np.ndarray:
     """uint32 [8 x ceil(K/128) x N x 4] bit planes, most significant plane
-    first; word w of block kb holds elements 128*kb + 32*w .. +31 of a row."""
+    first; word w of block kb holds elements 128*kb + 32*w .. +31 of a row,
+    element e of the word at bit 8*(e % 4) + e // 4."""
     W = _np(W, np.int8)
     N, K = W.shape
     KB = (K + 127) // 128

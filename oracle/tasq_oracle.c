@@ -248,8 +248,9 @@ int oracle_conv3x3_entries(const int8_t *X, const int8_t *Wt, double sx, const f
  * Bit planes of the stored two's-complement weight (App. G.2: plane p is bit
  * p of the code, p = 0 the least significant).  Layout, in uint32 words:
  *   planes[q][kb][n][w],  q = 7 - p (most significant plane first, so the
- *   top b planes are one contiguous prefix), kb = j / 128, w = (j % 128) / 32,
- *   bit (j % 32) of the word is element j of row n.
+ *   top b planes are one contiguous prefix), kb = j / 128, w = (j % 128) / 32.
+ * Within a word, element e = j % 32 of the word's 32 elements sits at bit
+ * 8 * (e % 4) + e / 4 (group of four e / 4 in bit e / 4 of each byte).
  * KB = ceil(K / 128); bits past K are zero.
  */
 int oracle_pack_planes(const int8_t *W, int64_t N, int64_t K, uint32_t *planes)
@@ -263,7 +264,8 @@ int oracle_pack_planes(const int8_t *W, int64_t N, int64_t K, uint32_t *planes)
             for (int64_t j = 0; j < K; ++j) {
                 uint32_t bit = ((uint32_t)(uint8_t)W[n * K + j] >> p) & 1u;
                 int64_t word = ((q * KB + j / 128) * N + n) * 4 + (j % 128) / 32;
-                planes[word] |= bit << (j % 32);
+                int e = (int)(j % 32);
+                planes[word] |= bit << (8 * (e % 4) + e / 4);
             }
     }
     return ORACLE_OK;

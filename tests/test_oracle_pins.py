@@ -267,8 +267,23 @@ def unpack(planes, K):
     blk = planes[:, j // 128, :, :]                          # [8, K, N, 4]
     w = ((j % 128) // 32)[None, :, None, None]
     words = np.take_along_axis(blk, np.broadcast_to(w, blk.shape[:3] + (1,)), 3)[..., 0]
-    bits = (words.astype(np.int64) >> (j % 32)[None, :, None]) & 1
+    e = j % 32
+    pos = 8 * (e % 4) + e // 4                               # bit of element e in its word
+    bits = (words.astype(np.int64) >> pos[None, :, None]) & 1
     return bits.transpose(0, 2, 1)
+
+
+def test_planes_bit_position_worked_example():
+    """Word 0 of a row whose elements 0..31 are 1, 0, 0, ..., 0 except element
+    5 = -128: element 0 sets bit 0 of plane p=0 (q=7); element 5 (group 1,
+    byte 1) sets bit 8*1 + 1 = 9 of the sign plane (q=0)."""
+    W = np.zeros((1, 32), np.int8)
+    W[0, 0] = 1
+    W[0, 5] = -128
+    planes = oracle.pack_planes(W)
+    assert int(planes[7, 0, 0, 0]) == 1 << 0
+    assert int(planes[0, 0, 0, 0]) == 1 << 9
+    assert not planes[1:7].any()
 
 
 @pytest.mark.parametrize("N,K", [(1, 1), (5, 31), (7, 32), (3, 100), (4, 300)])
