@@ -98,6 +98,10 @@ def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: tor
         y = torch.empty((M, N), dtype=torch.float32, device=X.device)
     _need(acc, torch.int32, (M, N), "acc")
     _need(y, torch.float32, (M, N), "y")
+    if workspace is None and acc is None and M > 0 and N > 0:
+        wb = workspace_bytes(M, N, K)
+        if wb:
+            workspace = torch.empty(wb, dtype=torch.uint8, device=X.device)
     o = _opts(variant, planes, workspace, split_k)
     rc = _lib.lib().tasq_masked_linear(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias), M, N,
                                        K, int(b), _ptr(acc), _ptr(y), ctypes.byref(o), _stream())

@@ -30,9 +30,11 @@ namespace tasq {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int PF_ = 2, int OCC_ = 2>
+template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int PF_ = 2, int OCC_ = 2,
+          int NSTAGE_ = 2>
 struct Cfg {
     static constexpr int OCC = OCC_;                    // target waves per SIMD
+    static constexpr int NSTAGE = NSTAGE_;              // K tiles resident in LDS
     static constexpr int BM = BM_, BN = BN_, BK = BK_;
     static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
     static constexpr int PF = PF_;                      // K tiles in flight in registers
@@ -45,6 +47,8 @@ struct Cfg {
     static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must hold 32x32 blocks");
     static_assert(BK % 32 == 0 && (CPR == 4 || CPR == 8), "BK must be 64 or 128");
     static_assert((BM * CPR) % NT == 0 && (BN * CPR) % NT == 0, "loads must divide");
+    static_assert(NSTAGE == 2 || NSTAGE == 3, "two or three LDS stages");
+    static_assert(BK / 32 % 2 == 0, "an even number of 32-wide sub-steps per K tile");
 };
 
 // Physical 16-byte chunk of logical chunk c in LDS row r.  For 128-byte rows
@@ -135,12 +139,15 @@ __device__ __forceinline__ v4i load_conv_any(const LayerDesc &d, int m, int kbyt
 
 // ----------------------------------------------------------- bit planes
 
-// Bit i of x (i < 4) moved to bit 8*i: x * (1 + 2^7 + 2^14 + 2^21) places
-// bit i at positions i + 7j, which are all distinct for i, j < 4, and only
-// j = i lands on a multiple of 8.
-__device__ __forceinline__ uint32_t spread4(uint32_t x)
+// Four consecutive weights of plane q, placed at bit 7 - q of four bytes and
+// OR-ed into acc.  Plane words keep element 4s + j at bit 8j + s, so rotating
+// right by s - (7 - q) moves the bits of elements 4s .. 4s+3 to bit 7 - q of
+// bytes 0..3 (other bits are masked off): one v_alignbit_b32 and one
+// v_and_or_b32 per four weights per plane.
+__device__ __forceinline__ uint32_t plane_group(uint32_t word, int s, int up, uint32_t acc)
 {
-    return (x * 0x00204081u) & 0x01010101u;
+    const uint32_t rot = __builtin_amdgcn_alignbit(word, word, (uint32_t)(s - up) & 31u);
+    return (rot & (0x01010101u << up)) | acc;
 }
 
 // Chunk (row n, kbyte..kbyte+15) of W_b rebuilt from the top b bit planes
@@ -155,15 +162,15 @@ __device__ __forceinline__ v4i load_planes(const uint32_t *P, int N, int K, int 
     const int KB = (K + 127) >> 7;
     const size_t plane_stride = (size_t)KB * (size_t)N * 4;
     const uint32_t *base = P + ((size_t)(kbyte >> 7) * N + n) * 4 + ((kbyte & 127) >> 5);
-    const int sh = (kbyte & 16);
+    const int s0 = (kbyte & 16) >> 2;        // groups 0..3 or 4..7 of the word
     uint32_t d0 = 0, d1 = 0, d2 = 0, d3 = 0;
     for (int q = 0; q < b; ++q) {
-        const uint32_t half = base[q * plane_stride] >> sh;
+        const uint32_t w = base[q * plane_stride];
         const int up = 7 - q;
-        d0 |= spread4(half & 0xF) << up;
-        d1 |= spread4((half >> 4) & 0xF) << up;
-        d2 |= spread4((half >> 8) & 0xF) << up;
-        d3 |= spread4((half >> 12) & 0xF) << up;
+        d0 = plane_group(w, s0 + 0, up, d0);
+        d1 = plane_group(w, s0 + 1, up, d1);
+        d2 = plane_group(w, s0 + 2, up, d2);
+        d3 = plane_group(w, s0 + 3, up, d3);
     }
     return v4i{(int)d0, (int)d1, (int)d2, (int)d3};
 }
@@ -311,10 +318,14 @@ struct Regs {
 
 // Accumulates the K range [kb, ke) of tile (m0, n0) into acc.
 //
-// Pipeline: LDS holds two K tiles (compute one, fill the other) and
-// registers hold the next PF tiles, so the global load of tile t+1+PF is
-// issued right after tile t+1 leaves registers for LDS and has PF compute
-// steps to arrive.  One barrier per K tile.
+// Pipeline: LDS holds NSTAGE K tiles and registers hold the next PF tiles;
+// the global load of a tile is issued PF K steps before it is stored to LDS.
+// One barrier per K tile.  With two stages the tile being filled is the one
+// computed last step; with three stages tile t+1 is complete while tile t is
+// computed, so the fragments of t+1's first sub-step are read during t's
+// last MFMAs and the barrier is off the MFMA critical path.  Fragments are
+// double-buffered across sub-steps: the LDS reads of sub-step kk+1 are in
+// flight while sub-step kk's MFMAs issue.
 template <class C, bool ALIGNED, int KIND, bool PLANES = false>
 __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int m0, int n0,
                                          int kb, int ke, v16i (&acc)[C::FM][C::FN],
@@ -325,6 +336,9 @@ __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int
     const int wave = tid >> 6;
     const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
     constexpr int SA = C::BM * C::CPR, SB = C::BN * C::CPR;
+    constexpr int NS = C::NSTAGE;
+    constexpr int KK = C::BK / 32;
+    constexpr bool XPF = NS >= 3;       // cross-tile fragment prefetch
 
 #pragma unroll
     for (int i = 0; i < C::FM; ++i)
@@ -338,81 +352,104 @@ __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int
         return;
     // valid bytes of the last K tile (BK when K fills it)
     const int last_valid = span - (nk - 1) * C::BK;
+    const bool has_tail = last_valid < C::BK;
 
     Plan<C, ALIGNED, KIND, PLANES> plan;
     plan.init(d, m0, n0, kb, tid);
     Regs<C, ALIGNED, KIND, PLANES> ring[C::PF];
 
-    ring[0].load(plan, d, m0, n0, kb, 0u, tid);
-    ring[0].store(smA, smB, wmask, tid);
+    // Prologue: tiles 0 .. NS-2 into LDS stages 0 .. NS-2, then the next PF
+    // tiles into the register ring.
 #pragma unroll
-    for (int u = 0; u < C::PF; ++u)
-        if (1 + u < nk)
-            ring[u].load(plan, d, m0, n0, kb + (1 + u) * C::BK, (uint32_t)(1 + u) * C::BK, tid);
+    for (int p = 0; p < NS - 1; ++p) {
+        if (p < nk) {
+            ring[0].load(plan, d, m0, n0, kb + p * C::BK, (uint32_t)p * C::BK, tid);
+            ring[0].store(smA + p * SA, smB + p * SB, wmask, tid);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < C::PF; ++u) {
+        const int tt = NS - 1 + u;
+        if (tt < nk)
+            ring[u].load(plan, d, m0, n0, kb + tt * C::BK, (uint32_t)tt * C::BK, tid);
+    }
     __syncthreads();
 
-    // MFMAs over the K tile in LDS buffer `buf`; with `tail`, weight bytes at
-    // or past column `last_valid` of the tile are zeroed first (the loads
-    // there may hold the next row or zero).  Fragments are double-buffered:
-    // the LDS reads of sub-step kk+1 are in flight while sub-step kk's MFMAs
-    // issue.
-    auto compute = [&](int buf, bool tail) {
-        const v4i *A = smA + buf * SA;
-        const v4i *B = smB + buf * SB;
-        constexpr int KK = C::BK / 32;
-        v4i fa[2][C::FM], fb[2][C::FN];
-        auto read = [&](int kk, v4i (&a)[C::FM], v4i (&b)[C::FN]) {
-            const int c = 2 * kk + (lane >> 5);
+    v4i fa[2][C::FM], fb[2][C::FN];
+    // Fragments of sub-step kk of the tile in `stage`; with `tail`, weight
+    // bytes at or past column last_valid of the tile read as zero (the loads
+    // there may hold the next row or zero).
+    auto read = [&](int stage, int kk, bool tail, v4i (&a)[C::FM], v4i (&b)[C::FN]) {
+        const v4i *A = smA + stage * SA;
+        const v4i *B = smB + stage * SB;
+        const int c = 2 * kk + (lane >> 5);
 #pragma unroll
-            for (int i = 0; i < C::FM; ++i) {
-                const int r = wm * C::WTM + i * 32 + (lane & 31);
-                a[i] = A[r * C::CPR + swz<C::CPR>(r, c)];
-            }
+        for (int i = 0; i < C::FM; ++i) {
+            const int r = wm * C::WTM + i * 32 + (lane & 31);
+            a[i] = A[r * C::CPR + swz<C::CPR>(r, c)];
+        }
 #pragma unroll
-            for (int j = 0; j < C::FN; ++j) {
-                const int r = wn * C::WTN + j * 32 + (lane & 31);
-                b[j] = B[r * C::CPR + swz<C::CPR>(r, c)];
-                if (tail && 16 * c >= last_valid)
-                    b[j] = zero4();
-            }
-        };
-        read(0, fa[0], fb[0]);
-        __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
+        for (int j = 0; j < C::FN; ++j) {
+            const int r = wn * C::WTN + j * 32 + (lane & 31);
+            b[j] = B[r * C::CPR + swz<C::CPR>(r, c)];
+            if (tail && 16 * c >= last_valid)
+                b[j] = zero4();
+        }
+    };
+    auto mfmas = [&](v4i (&a)[C::FM], v4i (&b)[C::FN]) {
+#pragma unroll
+        for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::FN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+    // All sub-steps of tile t (in `stage`).  Sub-step 0's fragments are
+    // already in fa[0]/fb[0] when XPF; with has_next, `next` is the stage of tile t+1
+    // whose first fragments are read during the last sub-step.
+    auto compute = [&](int stage, bool tail, bool has_next, int next, bool next_tail) {
+        if (!XPF) {
+            read(stage, 0, tail, fa[0], fb[0]);
+            __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
+        }
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-            if (kk + 1 < KK)
-                read(kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
-#pragma unroll
-            for (int i = 0; i < C::FM; ++i)
-#pragma unroll
-                for (int j = 0; j < C::FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[kk & 1][i], fb[kk & 1][j],
-                                                                      acc[i][j], 0, 0, 0);
-            // Issue order: the next sub-step's LDS reads, then this sub-step's
-            // MFMAs (which only wait for the older reads).
-            if (kk + 1 < KK)
+            const bool more = kk + 1 < KK;
+            if (more)
+                read(stage, kk + 1, tail, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
+            else if (XPF && has_next)
+                read(next, 0, next_tail, fa[0], fb[0]);
+            mfmas(fa[kk & 1], fb[kk & 1]);
+            if (more || (XPF && has_next))
                 __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
             __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
         }
     };
 
-    // Steady state over tiles 0 .. nk-2; ring[t % PF] holds tile t+1.
+    if (XPF)
+        read(0, 0, nk == 1 && has_tail, fa[0], fb[0]);
+    // Steady state over tiles 0 .. nk-2: ring[t % PF] holds tile t+NS-1.
+    int stage = 0;                  // stage of tile t
     for (int t0 = 0; t0 < nk - 1; t0 += C::PF) {
 #pragma unroll
         for (int u = 0; u < C::PF; ++u) {
             const int t = t0 + u;
             if (t < nk - 1) {
-                compute(t & 1, false);
-                ring[u].store(smA + ((t + 1) & 1) * SA, smB + ((t + 1) & 1) * SB, wmask, tid);
-                if (t + 1 + C::PF < nk) {
-                    const uint32_t off = (uint32_t)(t + 1 + C::PF) * C::BK;
-                    ring[u].load(plan, d, m0, n0, kb + (int)off, off, tid);
+                const int next = stage + 1 == NS ? 0 : stage + 1;
+                const int fill = stage == 0 ? NS - 1 : stage - 1;   // stage of tile t+NS-1
+                compute(stage, false, true, next, t + 1 == nk - 1 && has_tail);
+                if (t + NS - 1 < nk) {
+                    ring[u].store(smA + fill * SA, smB + fill * SB, wmask, tid);
+                    if (t + NS - 1 + C::PF < nk) {
+                        const uint32_t off = (uint32_t)(t + NS - 1 + C::PF) * C::BK;
+                        ring[u].load(plan, d, m0, n0, kb + (int)off, off, tid);
+                    }
                 }
                 __syncthreads();
+                stage = next;
             }
         }
     }
-    compute((nk - 1) & 1, last_valid < C::BK);
+    compute(stage, has_tail, false, 0, false);
 }
 
 // Writes a finished tile: int32 accumulators and/or the fp32 dequantised
@@ -497,8 +534,8 @@ __device__ __forceinline__ void tile_coords(int t, int tiles_m, int tiles_n, int
 template <class C, bool ALIGNED, int KIND, bool PLANES>
 __global__ void __launch_bounds__(C::NT, C::OCC) k_masked_gemm(LayerDesc d)
 {
-    __shared__ v4i smA[2 * C::BM * C::CPR];
-    __shared__ v4i smB[2 * C::BN * C::CPR];
+    __shared__ v4i smA[C::NSTAGE * C::BM * C::CPR];
+    __shared__ v4i smB[C::NSTAGE * C::BN * C::CPR];
     int tm, tn;
     tile_coords(xcd_remap(blockIdx.x, gridDim.x), d.tiles_m, d.tiles_n, tm, tn);
     const int m0 = tm * C::BM, n0 = tn * C::BN;
@@ -516,8 +553,8 @@ __global__ void __launch_bounds__(C::NT, C::OCC)
 k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *table, int S,
                       int stage)
 {
-    __shared__ v4i smA[2 * C::BM * C::CPR];
-    __shared__ v4i smB[2 * C::BN * C::CPR];
+    __shared__ v4i smA[C::NSTAGE * C::BM * C::CPR];
+    __shared__ v4i smB[C::NSTAGE * C::BN * C::CPR];
     const int t = xcd_remap(blockIdx.x, gridDim.x);
     int lo = 0, hi = L - 1;
     while (lo < hi) {
@@ -604,7 +641,8 @@ hipError_t launch_grouped_cfg(const LayerDesc *d_descs, int L, int total_tiles,
     const TileOps &NAME()                                                                   \
     {                                                                                       \
         static const TileOps ops = {{CFG::BM, CFG::BN, CFG::BK}, &launch_single_cfg<CFG>,   \
-                                    &launch_planes_cfg<CFG>, &launch_grouped_cfg<CFG>};     \
+                                    &launch_planes_cfg<CFG>, &launch_grouped_cfg<CFG>,      \
+                                    false};                                                 \
         return ops;                                                                         \
     }
 

@@ -1,8 +1,10 @@
 // Bit-plane relayout of the stored weight buffer (one-time).
 //
-// planes[q][kb][n][w] bit i = bit (7 - q) of W[n][128*kb + 32*w + i]
-// (App. G.2: plane p is bit p of the two's-complement code; most significant
-// plane first so that the top b planes form one contiguous prefix).
+// planes[q][kb][n][w]: bit 8*(e%4) + e/4 holds bit (7 - q) of element
+// W[n][128*kb + 32*w + e] (App. G.2: plane p is bit p of the two's-complement
+// code; most significant plane first so that the top b planes form one
+// contiguous prefix).  With this order, (word >> s) & 0x01010101 puts the
+// bits of elements 4s .. 4s+3 in the low bit of four consecutive bytes.
 #include "tasq_internal.h"
 
 namespace tasq {
@@ -25,9 +27,10 @@ __global__ void k_pack_planes(const int8_t *__restrict__ W, int N, int K, int KB
         for (int i = 0; i < 32; ++i) {
             const int j = j0 + i;
             const uint32_t v = j < K ? (uint32_t)(uint8_t)row[j] : 0u;
+            const int pos = 8 * (i & 3) + (i >> 2);
 #pragma unroll
             for (int p = 0; p < 8; ++p)
-                pw[p] |= ((v >> p) & 1u) << i;
+                pw[p] |= ((v >> p) & 1u) << pos;
         }
 #pragma unroll
         for (int p = 0; p < 8; ++p)

@@ -93,11 +93,40 @@ bool fits_buffers(const LayerDesc &d)
     return xb < (1LL << 31) && (long long)d.N * d.K < (1LL << 31);
 }
 
+// Weight-streaming path for skinny activations: needs an int32 [M][N]
+// buffer to accumulate into (acc_out, else the caller's workspace).
+int32_t *skinny_accbuf(const LayerDesc &d, const tasq_opts *o)
+{
+    if (d.acc)
+        return d.acc;
+    const size_t need = (size_t)d.M * (size_t)d.N * 4;
+    if (o && o->workspace && o->workspace_bytes >= need)
+        return static_cast<int32_t *>(o->workspace);
+    return nullptr;
+}
+
+bool skinny_ok(const LayerDesc &d, bool planes)
+{
+    if (d.kind != tasq::KIND_LINEAR || d.M > tasq::kSkinnyMaxM || d.K % 16 != 0 ||
+        !aligned16(d.X) || !fits_buffers(d))
+        return false;
+    if (planes)
+        return d.P && (long long)8 * ((d.K + 127) / 128) * d.N * 16 < (1LL << 31);
+    return aligned16(d.W);
+}
+
 int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
 {
     if (d.M == 0 || d.N == 0)
         return TASQ_OK;
     hipError_t e;
+    const bool want_planes = use_bitplane(o);
+    if (d.M <= tasq::kSkinnyMaxM && skinny_ok(d, want_planes)) {
+        if (int32_t *accbuf = skinny_accbuf(d, o)) {
+            e = tasq::launch_skinny(d, want_planes, accbuf, stream);
+            return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+        }
+    }
     if (use_bitplane(o)) {
         e = tasq::tile_ops(tasq::TILE_64x64_K128_W4_PF2).planes(
             d, (d.K % 16) == 0 && aligned16(d.X) && fits_buffers(d), stream);
@@ -108,7 +137,10 @@ int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
         else
             aligned = (d.K % 16) == 0 && aligned16(d.X) && aligned16(d.W);
         aligned = aligned && fits_buffers(d);
-        e = tasq::tile_ops(pick_tile(d.M, d.N)).single(d, aligned, stream);
+        const tasq::TileOps *ops = &tasq::tile_ops(pick_tile(d.M, d.N));
+        if (ops->linear_only && (!aligned || d.kind != tasq::KIND_LINEAR))
+            ops = &tasq::tile_ops(tasq::TILE_256x256_K128_W8_PF1);
+        e = ops->single(d, aligned, stream);
     }
     return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
 }
@@ -210,10 +242,10 @@ size_t tasq_planes_bytes(int N, int K)
 
 size_t tasq_workspace_bytes(int M, int N, int K)
 {
-    (void)M;
-    (void)N;
     (void)K;
-    return 0;
+    if (M <= 0 || N <= 0 || M > tasq::kSkinnyMaxM)
+        return 0;
+    return (size_t)M * (size_t)N * 4;   // int32 accumulators of the skinny path
 }
 
 int tasq_masked_linear(const int8_t *X, const int8_t *W, float sx, const float *sw,
@@ -346,7 +378,13 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         grouped = ok && fits_buffers(d);
     }
     if (grouped) {
-        const tasq::TileOps &ops = tasq::tile_ops(pick_grouped_tile());
+        bool any_conv = false;
+        for (int l = 0; l < L; ++l)
+            any_conv = any_conv || descs[l].kind == tasq::KIND_CONV3X3;
+        const tasq::TileOps *opsp = &tasq::tile_ops(pick_grouped_tile());
+        if (opsp->linear_only && any_conv)
+            opsp = &tasq::tile_ops(tasq::TILE_256x256_K128_W8_PF1);
+        const tasq::TileOps &ops = *opsp;
         const tasq::TileShape ts = ops.shape;
         long long total = 0;
         for (int l = 0; l < L; ++l) {

@@ -51,6 +51,7 @@ struct TileOps {
     hipError_t (*planes)(const LayerDesc &d, bool aligned, hipStream_t stream);
     hipError_t (*grouped)(const LayerDesc *d_descs, int L, int total_tiles,
                           const uint8_t *d_table, int S, int stage, hipStream_t stream);
+    bool linear_only;      // aligned linear layers only (no conv, no bit planes)
 };
 
 // Tile configurations, indexed by TileId.
@@ -63,11 +64,25 @@ enum TileId : int {
     TILE_128x128_K64_W4_PF3 = 5,   // 128x128 tile, 4 waves, BK 64, 3 K tiles in flight
     TILE_256x128_K64_W4_PF2 = 6,   // 256x128 tile, 4 waves (128x64 per wave), BK 64
     TILE_128x256_K64_W4_PF2 = 7,   // 128x256 tile, 4 waves (64x128 per wave), BK 64
-    TILE_COUNT = 8
+    TILE_256x256_K64_W8_S3 = 8,   // 256x256 tile, 8 waves, BK 64, 3 LDS stages
+    TILE_128x128_K64_W4_S3 = 9,   // 128x128 tile, 4 waves, BK 64, 3 LDS stages
+    TILE_256x256_DIRECT_K64_S4 = 10,   // direct-to-LDS, 4 waves of 128x128, BK 64, 4 stages
+    TILE_256x256_DIRECT_K64_S3 = 11,   // direct-to-LDS, BK 64, 3 stages
+    TILE_256x256_DIRECT_K128_S2 = 12,  // direct-to-LDS, BK 128, 2 stages
+    TILE_256x256_DIRECT_K64_S4_W8 = 13,  // direct-to-LDS, 8 waves of 128x64, BK 64, 4 stages
+    TILE_256x256_DIRECT_K64_S3_W8 = 14,  // direct-to-LDS, 8 waves of 128x64, BK 64, 3 stages
+    TILE_256x256_BDIRECT_K128_W8 = 15,  // weights fed from registers, 8 waves, BK 128
+    TILE_COUNT = 16
 };
 const TileOps &tile_ops(int tile);
 
 hipError_t launch_pack_planes(const int8_t *W, int N, int K, uint32_t *planes,
                               hipStream_t stream);
+
+// Weight-streaming kernels for M <= 64 (skinny.hip): int8 rows (masked) or
+// the top b bit planes; int32 partial sums are added into `accbuf`
+// (M x N, zeroed by the launcher), then dequantised into d.y.
+constexpr int kSkinnyMaxM = 64;
+hipError_t launch_skinny(const LayerDesc &d, bool planes, int32_t *accbuf, hipStream_t stream);
 
 }  // namespace tasq

@@ -268,6 +268,39 @@ def test_bitplane_variant(M, N, K):
                       f"bitplane {M}x{N}x{K} b={b}")
 
 
+# ---------------------------------------------------- skinny (M <= 64) paths
+
+SKINNY = [(1, 37, 1152), (5, 300, 1040), (16, 1152, 144), (32, 33, 16), (33, 257, 1152),
+          (64, 130, 528), (16, 4608, 1152)]
+
+
+@pytest.mark.parametrize("case", range(len(SKINNY)))
+@pytest.mark.parametrize("planes", [False, True])
+def test_skinny_weight_streaming(case, planes):
+    """M <= 64 runs the weight-streaming kernels (int8 rows or the top b bit
+    planes), with and without an int32 output."""
+    M, N, K = SKINNY[case]
+    X, W, sw, bias = inputs.random_case(300 + case, M, N, K)
+    X[0, 0] = -128
+    W[0, 0] = -128
+    Xd, Wd, swd, bd = X.to(DEV), W.to(DEV), sw.to(DEV), bias.to(DEV)
+    P = T.pack_planes(Wd) if planes else None
+    kw = dict(variant=T.VARIANT_BITPLANE, planes=P) if planes else {}
+    sx = f32(0.02)
+    for b in range(1, 9):
+        use_bias = bd if b % 3 == 0 else None
+        ra, ry = oracle.masked_linear(X, W, sx, sw, b, bias if b % 3 == 0 else None)
+        acc, y = T.masked_linear(Xd, None if planes else Wd, sx, swd, b, use_bias, **kw)
+        torch.cuda.synchronize()
+        check_outputs(acc, y, ra, ry, sx, sw, bias if b % 3 == 0 else None,
+                      f"skinny {M}x{N}x{K} planes={planes} b={b}")
+        _, y2 = T.masked_linear(Xd, None if planes else Wd, sx, swd, b, use_bias,
+                                want_acc=False, **kw)
+        torch.cuda.synchronize()
+        check_outputs(None, y2, ra, ry, sx, sw, bias if b % 3 == 0 else None,
+                      f"skinny y-only {M}x{N}x{K} planes={planes} b={b}")
+
+
 # ------------------------------------------------------------------- schedule
 
 def small_schedule_layers(seed):
