@@ -13,7 +13,18 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtasq.so")
 OBJDIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["tile_256x256_k64_w8_pf2.hip", "tile_256x256_k64_w8_pf3.hip", "tile_256x256_k128_w8_pf1.hip", "tile_128x128_k128_w4_pf2.hip", "tile_64x64_k128_w4_pf2.hip", "tile_128x128_k64_w4_pf3.hip", "tile_256x128_k64_w4_pf2.hip", "tile_128x256_k64_w4_pf2.hip", "tile_256x256_k64_w8_s3.hip", "tile_128x128_k64_w4_s3.hip", "tile_256x256_direct_k64_s4.hip", "tile_256x256_direct_k64_s3.hip", "tile_256x256_direct_k128_s2.hip", "tile_256x256_direct_k64_s4_w8.hip", "tile_256x256_direct_k64_s3_w8.hip", "tile_256x256_bdirect_k128_w8.hip", "pack_planes.hip", "skinny.hip", "tiles.cpp", "tasq_api.cpp"]
+SOURCES = [
+    "tile_256x256_k128_w8_pf1.hip",
+    "tile_256x256_k64_w8_pf2.hip",
+    "tile_128x128_k128_w4_pf2.hip",
+    "tile_64x64_k128_w4_pf2.hip",
+    "tile_256x128_k64_w4_pf2.hip",
+    "tile_128x256_k64_w4_pf2.hip",
+    "pack_planes.hip",
+    "skinny.hip",
+    "tiles.cpp",
+    "tasq_api.cpp",
+]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

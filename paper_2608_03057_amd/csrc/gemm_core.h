@@ -11,9 +11,9 @@
 //
 // Structure:
 //   * block tile BM x BN over (M, N), K consumed in BK-byte steps;
-//   * global -> VGPR (16-byte loads, mask on the weight side) -> LDS, double
-//     buffered with one barrier per K step, next tile's loads issued before
-//     the current tile's MFMAs;
+//   * global -> VGPR (16-byte loads, mask on the weight side) -> LDS, two
+//     LDS stages and a ring of PF K tiles in flight in registers, one barrier
+//     per K step placed so that MFMAs cover it (see mainloop);
 //   * LDS rows of BK bytes, 16-byte chunks XOR-swizzled so that the 32 rows
 //     one MFMA operand read touches fall in distinct banks;
 //   * each wave owns a (BM/WAVES_M) x (BN/WAVES_N) sub-tile of
@@ -30,11 +30,10 @@ namespace tasq {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int PF_ = 2, int OCC_ = 2,
-          int NSTAGE_ = 2>
+template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int PF_ = 2, int OCC_ = 2>
 struct Cfg {
     static constexpr int OCC = OCC_;                    // target waves per SIMD
-    static constexpr int NSTAGE = NSTAGE_;              // K tiles resident in LDS
+    static constexpr int NSTAGE = 2;                    // K tiles resident in LDS
     static constexpr int BM = BM_, BN = BN_, BK = BK_;
     static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
     static constexpr int PF = PF_;                      // K tiles in flight in registers
@@ -47,7 +46,6 @@ struct Cfg {
     static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must hold 32x32 blocks");
     static_assert(BK % 32 == 0 && (CPR == 4 || CPR == 8), "BK must be 64 or 128");
     static_assert((BM * CPR) % NT == 0 && (BN * CPR) % NT == 0, "loads must divide");
-    static_assert(NSTAGE == 2 || NSTAGE == 3, "two or three LDS stages");
     static_assert(BK / 32 % 2 == 0, "an even number of 32-wide sub-steps per K tile");
 };
 
@@ -181,17 +179,21 @@ __device__ __forceinline__ v4i load_planes(const uint32_t *P, int N, int K, int 
 // id = tid + i*NT: row id / CPR, 16-byte column id % CPR of the tile.  In
 // the ALIGNED path (K % 16 == 0, 16-byte aligned operands) a chunk's buffer
 // offset is fixed per tile and advanced by the K step; rows past M (N)
-// carry kOOB and read zero.  Columns past K are not masked here: the final
-// K tile zeroes the weight fragments past K before its MFMAs.
+// carry kOOB and read zero.  Weight chunks at or past the end of the K range
+// read zero as well, so the MFMAs of a ragged last K tile need no masking
+// (the activation bytes there meet zero weights).
 template <class C, bool ALIGNED, int KIND, bool PLANES>
 struct Plan {
     rsrc_t rX, rW;
     uint32_t offA[C::A_LOADS];   // linear: byte offset at k = kb; conv: pixel base
     uint32_t offB[C::B_LOADS];
     int hA[C::A_LOADS], wA[C::A_LOADS];   // conv: pixel coordinates
+    int kend;                             // end of the K range (bytes)
 
-    __device__ __forceinline__ void init(const LayerDesc &d, int m0, int n0, int kb, int tid)
+    __device__ __forceinline__ void init(const LayerDesc &d, int m0, int n0, int kb, int ke,
+                                         int tid)
     {
+        kend = ke;
         if constexpr (ALIGNED) {
             if constexpr (KIND == KIND_CONV3X3)
                 rX = make_rsrc(d.X, (uint32_t)d.H * (uint32_t)d.Wd * (uint32_t)d.C);
@@ -287,7 +289,7 @@ struct Regs {
             else if constexpr (!ALIGNED)
                 b[i] = load_rowmajor_any(d.W, d.N, d.K, n0 + r, k0 + 16 * c);
             else
-                b[i] = ld16(p.rW, p.offB[i] + kt);
+                b[i] = ld16(p.rW, k0 + 16 * c < p.kend ? p.offB[i] + kt : kOOB);
         }
     }
 
@@ -316,29 +318,31 @@ struct Regs {
     }
 };
 
-// Accumulates the K range [kb, ke) of tile (m0, n0) into acc.
+// Accumulates the K range [kb, ke) of tile (m0, n0) into acc, two LDS stages.
 //
-// Pipeline: LDS holds NSTAGE K tiles and registers hold the next PF tiles;
-// the global load of a tile is issued PF K steps before it is stored to LDS.
-// One barrier per K tile.  With two stages the tile being filled is the one
-// computed last step; with three stages tile t+1 is complete while tile t is
-// computed, so the fragments of t+1's first sub-step are read during t's
-// last MFMAs and the barrier is off the MFMA critical path.  Fragments are
-// double-buffered across sub-steps: the LDS reads of sub-step kk+1 are in
-// flight while sub-step kk's MFMAs issue.
+// K tile t lives in LDS stage t % 2 while tile t+1 is written into the other
+// stage and tiles t+2 .. t+PF are in flight in the register ring.  Within
+// tile t, the LDS reads of sub-step kk+1 are in flight while the MFMAs of
+// sub-step kk issue.  The one barrier per K tile sits before the last
+// sub-step: by then every wave has read all of tile t's fragments and
+// written its share of tile t+1, so the last sub-step's MFMAs (operands
+// already in registers) cover the barrier and the reads of tile t+1's first
+// fragments.  Tile t+1 is stored from the ring half-way through tile t and
+// the ring slot is refilled right away, so a global load has PF whole K
+// tiles to land.
 template <class C, bool ALIGNED, int KIND, bool PLANES = false>
 __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int m0, int n0,
-                                         int kb, int ke, v16i (&acc)[C::FM][C::FN],
-                                         v4i *smA, v4i *smB)
+                                         int kb, int ke, v16i (&acc)[C::FM][C::FN], v4i *smA,
+                                         v4i *smB)
 {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
     constexpr int SA = C::BM * C::CPR, SB = C::BN * C::CPR;
-    constexpr int NS = C::NSTAGE;
     constexpr int KK = C::BK / 32;
-    constexpr bool XPF = NS >= 3;       // cross-tile fragment prefetch
+    constexpr int WRITE_KK = KK / 2 - 1;      // sub-step that stores tile t+1
+    constexpr int NW = C::A_LOADS + C::B_LOADS;
 
 #pragma unroll
     for (int i = 0; i < C::FM; ++i)
@@ -350,36 +354,22 @@ __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int
     const int nk = (span + C::BK - 1) / C::BK;
     if (nk <= 0)
         return;
-    // valid bytes of the last K tile (BK when K fills it)
-    const int last_valid = span - (nk - 1) * C::BK;
-    const bool has_tail = last_valid < C::BK;
 
     Plan<C, ALIGNED, KIND, PLANES> plan;
-    plan.init(d, m0, n0, kb, tid);
+    plan.init(d, m0, n0, kb, ke, tid);
     Regs<C, ALIGNED, KIND, PLANES> ring[C::PF];
 
-    // Prologue: tiles 0 .. NS-2 into LDS stages 0 .. NS-2, then the next PF
-    // tiles into the register ring.
+    // Prologue: tile 0 into stage 0, tiles 1 .. PF into the ring.
+    ring[0].load(plan, d, m0, n0, kb, 0u, tid);
+    ring[0].store(smA, smB, wmask, tid);
 #pragma unroll
-    for (int p = 0; p < NS - 1; ++p) {
-        if (p < nk) {
-            ring[0].load(plan, d, m0, n0, kb + p * C::BK, (uint32_t)p * C::BK, tid);
-            ring[0].store(smA + p * SA, smB + p * SB, wmask, tid);
-        }
-    }
-#pragma unroll
-    for (int u = 0; u < C::PF; ++u) {
-        const int tt = NS - 1 + u;
-        if (tt < nk)
-            ring[u].load(plan, d, m0, n0, kb + tt * C::BK, (uint32_t)tt * C::BK, tid);
-    }
+    for (int u = 0; u < C::PF; ++u)
+        if (1 + u < nk)
+            ring[u].load(plan, d, m0, n0, kb + (1 + u) * C::BK, (uint32_t)(1 + u) * C::BK, tid);
     __syncthreads();
 
     v4i fa[2][C::FM], fb[2][C::FN];
-    // Fragments of sub-step kk of the tile in `stage`; with `tail`, weight
-    // bytes at or past column last_valid of the tile read as zero (the loads
-    // there may hold the next row or zero).
-    auto read = [&](int stage, int kk, bool tail, v4i (&a)[C::FM], v4i (&b)[C::FN]) {
+    auto read = [&](int stage, int kk, v4i (&a)[C::FM], v4i (&b)[C::FN]) {
         const v4i *A = smA + stage * SA;
         const v4i *B = smB + stage * SB;
         const int c = 2 * kk + (lane >> 5);
@@ -392,8 +382,6 @@ __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int
         for (int j = 0; j < C::FN; ++j) {
             const int r = wn * C::WTN + j * 32 + (lane & 31);
             b[j] = B[r * C::CPR + swz<C::CPR>(r, c)];
-            if (tail && 16 * c >= last_valid)
-                b[j] = zero4();
         }
     };
     auto mfmas = [&](v4i (&a)[C::FM], v4i (&b)[C::FN]) {
@@ -403,53 +391,54 @@ __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int
             for (int j = 0; j < C::FN; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[i], b[j], acc[i][j], 0, 0, 0);
     };
-    // All sub-steps of tile t (in `stage`).  Sub-step 0's fragments are
-    // already in fa[0]/fb[0] when XPF; with has_next, `next` is the stage of tile t+1
-    // whose first fragments are read during the last sub-step.
-    auto compute = [&](int stage, bool tail, bool has_next, int next, bool next_tail) {
-        if (!XPF) {
-            read(stage, 0, tail, fa[0], fb[0]);
-            __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
-        }
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-            const bool more = kk + 1 < KK;
-            if (more)
-                read(stage, kk + 1, tail, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
-            else if (XPF && has_next)
-                read(next, 0, next_tail, fa[0], fb[0]);
-            mfmas(fa[kk & 1], fb[kk & 1]);
-            if (more || (XPF && has_next))
-                __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
-        }
-    };
 
-    if (XPF)
-        read(0, 0, nk == 1 && has_tail, fa[0], fb[0]);
-    // Steady state over tiles 0 .. nk-2: ring[t % PF] holds tile t+NS-1.
-    int stage = 0;                  // stage of tile t
+    read(0, 0, fa[0], fb[0]);
+    int stage = 0;
     for (int t0 = 0; t0 < nk - 1; t0 += C::PF) {
 #pragma unroll
         for (int u = 0; u < C::PF; ++u) {
             const int t = t0 + u;
             if (t < nk - 1) {
-                const int next = stage + 1 == NS ? 0 : stage + 1;
-                const int fill = stage == 0 ? NS - 1 : stage - 1;   // stage of tile t+NS-1
-                compute(stage, false, true, next, t + 1 == nk - 1 && has_tail);
-                if (t + NS - 1 < nk) {
-                    ring[u].store(smA + fill * SA, smB + fill * SB, wmask, tid);
-                    if (t + NS - 1 + C::PF < nk) {
-                        const uint32_t off = (uint32_t)(t + NS - 1 + C::PF) * C::BK;
-                        ring[u].load(plan, d, m0, n0, kb + (int)off, off, tid);
+#pragma unroll
+                for (int kk = 0; kk + 1 < KK; ++kk) {
+                    read(stage, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
+                    mfmas(fa[kk & 1], fb[kk & 1]);
+                    __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
+                    if (kk == WRITE_KK) {
+                        ring[u].store(smA + (stage ^ 1) * SA, smB + (stage ^ 1) * SB, wmask, tid);
+                        if (t + 1 + C::PF < nk) {
+                            const uint32_t off = (uint32_t)(t + 1 + C::PF) * C::BK;
+                            ring[u].load(plan, d, m0, n0, kb + (int)off, off, tid);
+                        }
+#pragma unroll
+                        for (int i = 0; i < C::FM * C::FN; ++i) {
+                            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                            if (i < NW)
+                                __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+                        }
+                    } else {
+                        __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
                     }
                 }
                 __syncthreads();
-                stage = next;
+                read(stage ^ 1, 0, fa[0], fb[0]);
+                mfmas(fa[(KK - 1) & 1], fb[(KK - 1) & 1]);
+                __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
+                stage ^= 1;
             }
         }
     }
-    compute(stage, has_tail, false, 0, false);
+    // Last K tile.
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+        if (kk + 1 < KK)
+            read(stage, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
+        mfmas(fa[kk & 1], fb[kk & 1]);
+        if (kk + 1 < KK)
+            __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
+    }
 }
 
 // Writes a finished tile: int32 accumulators and/or the fp32 dequantised
@@ -547,8 +536,10 @@ __global__ void __launch_bounds__(C::NT, C::OCC) k_masked_gemm(LayerDesc d)
 
 // Grouped launch over every layer of one denoising step: workgroup t finds
 // its layer by binary search over the tile prefix, and that layer's b from
-// the (layer, stage) table (App. G.1: a table lookup, no re-launch).
-template <class C>
+// the (layer, stage) table (App. G.1: a table lookup, no re-launch).  CONV
+// adds the implicit-GEMM path for 3x3 conv layers; without it every layer
+// must be linear.
+template <class C, bool CONV>
 __global__ void __launch_bounds__(C::NT, C::OCC)
 k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *table, int S,
                       int stage)
@@ -570,7 +561,7 @@ k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
     tile_coords(t - d.tile_begin, d.tiles_m, d.tiles_n, tm, tn);
     const int m0 = tm * C::BM, n0 = tn * C::BN;
     v16i acc[C::FM][C::FN];
-    if (d.kind == KIND_CONV3X3)
+    if (CONV && d.kind == KIND_CONV3X3)
         mainloop<C, true, KIND_CONV3X3>(d, wmask, m0, n0, 0, d.K, acc, smA, smB);
     else
         mainloop<C, true, KIND_LINEAR>(d, wmask, m0, n0, 0, d.K, acc, smA, smB);
@@ -627,11 +618,16 @@ hipError_t launch_planes_cfg(const LayerDesc &din, bool aligned, hipStream_t str
 
 template <class C>
 hipError_t launch_grouped_cfg(const LayerDesc *d_descs, int L, int total_tiles,
-                              const uint8_t *d_table, int S, int stage, hipStream_t stream)
+                              const uint8_t *d_table, int S, int stage, bool any_conv,
+                              hipStream_t stream)
 {
     dim3 g((unsigned)total_tiles), b(C::NT);
-    hipLaunchKernelGGL((k_masked_gemm_grouped<C>), g, b, 0, stream, d_descs, L, d_table, S,
-                       stage);
+    if (any_conv)
+        hipLaunchKernelGGL((k_masked_gemm_grouped<C, true>), g, b, 0, stream, d_descs, L, d_table,
+                           S, stage);
+    else
+        hipLaunchKernelGGL((k_masked_gemm_grouped<C, false>), g, b, 0, stream, d_descs, L,
+                           d_table, S, stage);
     return hipGetLastError();
 }
 
@@ -641,8 +637,7 @@ hipError_t launch_grouped_cfg(const LayerDesc *d_descs, int L, int total_tiles,
     const TileOps &NAME()                                                                   \
     {                                                                                       \
         static const TileOps ops = {{CFG::BM, CFG::BN, CFG::BK}, &launch_single_cfg<CFG>,   \
-                                    &launch_planes_cfg<CFG>, &launch_grouped_cfg<CFG>,      \
-                                    false};                                                 \
+                                    &launch_planes_cfg<CFG>, &launch_grouped_cfg<CFG>};     \
         return ops;                                                                         \
     }
 

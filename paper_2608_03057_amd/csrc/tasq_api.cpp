@@ -137,10 +137,7 @@ int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
         else
             aligned = (d.K % 16) == 0 && aligned16(d.X) && aligned16(d.W);
         aligned = aligned && fits_buffers(d);
-        const tasq::TileOps *ops = &tasq::tile_ops(pick_tile(d.M, d.N));
-        if (ops->linear_only && (!aligned || d.kind != tasq::KIND_LINEAR))
-            ops = &tasq::tile_ops(tasq::TILE_256x256_K128_W8_PF1);
-        e = ops->single(d, aligned, stream);
+        e = tasq::tile_ops(pick_tile(d.M, d.N)).single(d, aligned, stream);
     }
     return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
 }
@@ -381,10 +378,7 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         bool any_conv = false;
         for (int l = 0; l < L; ++l)
             any_conv = any_conv || descs[l].kind == tasq::KIND_CONV3X3;
-        const tasq::TileOps *opsp = &tasq::tile_ops(pick_grouped_tile());
-        if (opsp->linear_only && any_conv)
-            opsp = &tasq::tile_ops(tasq::TILE_256x256_K128_W8_PF1);
-        const tasq::TileOps &ops = *opsp;
+        const tasq::TileOps &ops = tasq::tile_ops(pick_grouped_tile());
         const tasq::TileShape ts = ops.shape;
         long long total = 0;
         for (int l = 0; l < L; ++l) {
@@ -414,7 +408,7 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
             return TASQ_ERR_HIP;
         for (int t = t_begin; t < t_end; ++t) {
             const int s = tasq_stage_of_step(t, S, T);
-            if (ops.grouped(d_descs, L, (int)total, d_table, S, s, st) != hipSuccess)
+            if (ops.grouped(d_descs, L, (int)total, d_table, S, s, any_conv, st) != hipSuccess)
                 return TASQ_ERR_HIP;
         }
         return TASQ_OK;

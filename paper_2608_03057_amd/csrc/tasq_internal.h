@@ -49,30 +49,22 @@ struct TileOps {
     TileShape shape;
     hipError_t (*single)(const LayerDesc &d, bool aligned, hipStream_t stream);
     hipError_t (*planes)(const LayerDesc &d, bool aligned, hipStream_t stream);
+    // One launch over every layer's tiles; any_conv selects the kernel that
+    // also handles 3x3 conv layers.
     hipError_t (*grouped)(const LayerDesc *d_descs, int L, int total_tiles,
-                          const uint8_t *d_table, int S, int stage, hipStream_t stream);
-    bool linear_only;      // aligned linear layers only (no conv, no bit planes)
+                          const uint8_t *d_table, int S, int stage, bool any_conv,
+                          hipStream_t stream);
 };
 
 // Tile configurations, indexed by TileId.
 enum TileId : int {
-    TILE_256x256_K64_W8_PF2 = 0,   // 256x256 tile, 8 waves (128x64 per wave), BK 64, 2 K tiles in flight
-    TILE_256x256_K64_W8_PF3 = 1,   // 256x256 tile, 8 waves, BK 64, 3 K tiles in flight
-    TILE_256x256_K128_W8_PF1 = 2,   // 256x256 tile, 8 waves, BK 128, 1 K tile in flight
-    TILE_128x128_K128_W4_PF2 = 3,   // 128x128 tile, 4 waves (64x64 per wave), BK 128
-    TILE_64x64_K128_W4_PF2 = 4,   // 64x64 tile, 4 waves (32x32 per wave), BK 128
-    TILE_128x128_K64_W4_PF3 = 5,   // 128x128 tile, 4 waves, BK 64, 3 K tiles in flight
-    TILE_256x128_K64_W4_PF2 = 6,   // 256x128 tile, 4 waves (128x64 per wave), BK 64
-    TILE_128x256_K64_W4_PF2 = 7,   // 128x256 tile, 4 waves (64x128 per wave), BK 64
-    TILE_256x256_K64_W8_S3 = 8,   // 256x256 tile, 8 waves, BK 64, 3 LDS stages
-    TILE_128x128_K64_W4_S3 = 9,   // 128x128 tile, 4 waves, BK 64, 3 LDS stages
-    TILE_256x256_DIRECT_K64_S4 = 10,   // direct-to-LDS, 4 waves of 128x128, BK 64, 4 stages
-    TILE_256x256_DIRECT_K64_S3 = 11,   // direct-to-LDS, BK 64, 3 stages
-    TILE_256x256_DIRECT_K128_S2 = 12,  // direct-to-LDS, BK 128, 2 stages
-    TILE_256x256_DIRECT_K64_S4_W8 = 13,  // direct-to-LDS, 8 waves of 128x64, BK 64, 4 stages
-    TILE_256x256_DIRECT_K64_S3_W8 = 14,  // direct-to-LDS, 8 waves of 128x64, BK 64, 3 stages
-    TILE_256x256_BDIRECT_K128_W8 = 15,  // weights fed from registers, 8 waves, BK 128
-    TILE_COUNT = 16
+    TILE_256x256_K128_W8_PF1 = 0,  // 256x256 tile, 8 waves (128x64 per wave), BK 128
+    TILE_256x256_K64_W8_PF2 = 1,   // 256x256 tile, 8 waves, BK 64, 2 K tiles in flight
+    TILE_128x128_K128_W4_PF2 = 2,  // 128x128 tile, 4 waves (64x64 per wave), BK 128
+    TILE_64x64_K128_W4_PF2 = 3,    // 64x64 tile, 4 waves (32x32 per wave), BK 128
+    TILE_256x128_K64_W4_PF2 = 4,   // 256x128 tile, 4 waves (128x64 per wave), BK 64
+    TILE_128x256_K64_W4_PF2 = 5,   // 128x256 tile, 4 waves (64x128 per wave), BK 64
+    TILE_COUNT = 6
 };
 const TileOps &tile_ops(int tile);
 

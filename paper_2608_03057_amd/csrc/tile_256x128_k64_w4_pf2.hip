@@ -1,4 +1,4 @@
-// Masked int8 GEMM instantiated for the 256x128 tile, 4 waves (128x64 per wave), BK 64.
+// Masked int8 GEMM instantiated for the 256x128 tile, 4 waves (128x64 per wave, two workgroups per CU), BK 64.
 #include "gemm_core.h"
 
 namespace tasq {

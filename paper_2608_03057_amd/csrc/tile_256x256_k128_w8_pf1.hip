@@ -1,4 +1,4 @@
-// Masked int8 GEMM instantiated for the 256x256 tile, 8 waves, BK 128, 1 K tile in flight.
+// Masked int8 GEMM instantiated for the 256x256 tile, 8 waves (128x64 per wave), BK 128, 1 K tile in flight.
 #include "gemm_core.h"
 
 namespace tasq {

@@ -1,4 +1,4 @@
-// Masked int8 GEMM instantiated for the 64x64 tile, 4 waves (32x32 per wave), BK 128.
+// Masked int8 GEMM instantiated for the 64x64 tile, 4 waves (32x32 per wave), BK 128, 2 K tiles in flight.
 #include "gemm_core.h"
 
 namespace tasq {

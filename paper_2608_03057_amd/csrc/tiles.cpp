@@ -3,41 +3,21 @@
 
 namespace tasq {
 
-const TileOps &ops_tile_256x256_k64_w8_pf2();
-const TileOps &ops_tile_256x256_k64_w8_pf3();
 const TileOps &ops_tile_256x256_k128_w8_pf1();
+const TileOps &ops_tile_256x256_k64_w8_pf2();
 const TileOps &ops_tile_128x128_k128_w4_pf2();
 const TileOps &ops_tile_64x64_k128_w4_pf2();
-const TileOps &ops_tile_128x128_k64_w4_pf3();
 const TileOps &ops_tile_256x128_k64_w4_pf2();
 const TileOps &ops_tile_128x256_k64_w4_pf2();
-const TileOps &ops_tile_256x256_k64_w8_s3();
-const TileOps &ops_tile_128x128_k64_w4_s3();
-const TileOps &ops_tile_256x256_direct_k64_s4();
-const TileOps &ops_tile_256x256_direct_k64_s3();
-const TileOps &ops_tile_256x256_direct_k128_s2();
-const TileOps &ops_tile_256x256_direct_k64_s4_w8();
-const TileOps &ops_tile_256x256_direct_k64_s3_w8();
-const TileOps &ops_tile_256x256_bdirect_k128_w8();
 
 using OpsFn = const TileOps &(*)();
 static const OpsFn kTiles[TILE_COUNT] = {
-    &ops_tile_256x256_k64_w8_pf2,
-    &ops_tile_256x256_k64_w8_pf3,
     &ops_tile_256x256_k128_w8_pf1,
+    &ops_tile_256x256_k64_w8_pf2,
     &ops_tile_128x128_k128_w4_pf2,
     &ops_tile_64x64_k128_w4_pf2,
-    &ops_tile_128x128_k64_w4_pf3,
     &ops_tile_256x128_k64_w4_pf2,
-    &ops_tile_128x256_k64_w4_pf2,
-    &ops_tile_256x256_k64_w8_s3,
-    &ops_tile_128x128_k64_w4_s3,
-    &ops_tile_256x256_direct_k64_s4,
-    &ops_tile_256x256_direct_k64_s3,
-    &ops_tile_256x256_direct_k128_s2,
-    &ops_tile_256x256_direct_k64_s4_w8,
-    &ops_tile_256x256_direct_k64_s3_w8,
-    &ops_tile_256x256_bdirect_k128_w8};
+    &ops_tile_128x256_k64_w4_pf2};
 
 const TileOps &tile_ops(int tile)
 {
