@@ -40,7 +40,8 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_masked_gemm_grouped_pixart28_traffic.json")
+def traffic_file(kernel: str) -> str:
+    return os.path.join(ROOT, "profiles", f"{kernel}_pixart28_traffic.json")
 
 
 def kernel_source_sha256() -> str:
@@ -53,12 +54,12 @@ def kernel_source_sha256() -> str:
     return h.hexdigest()
 
 
-def recorded_traffic():
+def recorded_traffic(kernel: str):
     """HBM bytes per grouped launch from the committed rocprofv3 FETCH_SIZE /
     WRITE_SIZE readings (already scaled by the copy calibration), or None when
     the kernel sources changed since they were taken."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(kernel)) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
@@ -67,17 +68,26 @@ def recorded_traffic():
     return rec.get("fetch_bytes_per_launch", 0) + rec.get("write_bytes_per_launch", 0)
 
 
-def build_workload(wl, device):
+def build_workload(wl, device, packed=True):
     """Device tensors of every layer; X drawn on the GPU (integer recipe,
-    identical to the CPU draw), W and sw on the CPU (fp64 Box-Muller)."""
+    identical to the CPU draw), W and sw on the CPU (fp64 Box-Muller).  With
+    ``packed`` each layer keeps only its packed weight buffer (the one stored
+    8-bit copy, in the matrix-instruction operand order)."""
     layers, keep = [], []
     for l, spec in enumerate(wl.layers):
         X = inputs.x_full(wl, l, device=device)
         W = inputs.w_full(wl, l).to(device)
         sw = inputs.sw_full(wl, l).to(device)
         y = torch.empty((spec.M, spec.N), dtype=torch.float32, device=device)
-        keep.append((X, W, sw, y))
-        layers.append(T.make_layer(X, W, wl.sx, sw, None, None, y))
+        if packed:
+            P = T.pack_weights(W)
+            torch.cuda.synchronize()
+            del W
+            keep.append((X, P, sw, y))
+            layers.append(T.make_layer(X, None, wl.sx, sw, None, None, y, packed=P))
+        else:
+            keep.append((X, W, sw, y))
+            layers.append(T.make_layer(X, W, wl.sx, sw, None, None, y))
     return layers, keep
 
 
@@ -153,6 +163,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--per-layer", action="store_true",
                     help="launch each layer separately instead of one grouped launch per step")
+    ap.add_argument("--weights", choices=("packed", "rowmajor"), default="rowmajor",
+                    help="weight buffer layout: packed (operand order, no LDS staging of "
+                         "weights) or row-major [N][K] (weights staged through LDS)")
     ap.add_argument("--print-source-hash", action="store_true",
                     help="print the HIP source hash that recorded counter readings refer to")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -178,7 +191,7 @@ def main():
     wl = inputs.workload(4, M_override=args.tokens)
     table = inputs.b_table(wl)
     log(f"building {len(wl.layers)} layers, M={wl.layers[0].M}")
-    layers, keep = build_workload(wl, dev)
+    layers, keep = build_workload(wl, dev, packed=args.weights == "packed")
     ws = None
     if not args.per_layer:
         ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=dev)
@@ -195,6 +208,7 @@ def main():
     value = total_ops / (ms * 1e-3) / 1e12
 
     roof = None
+    kname = "k_gemm_packed_grouped" if args.weights == "packed" else "k_masked_gemm_grouped"
     if ws is not None:
         launch_ms = time_launches(layers, table, wl, ws, reps=1)
         t_mfma = ops_step / (PEAK_INT8_TOPS * 1e12)
@@ -202,12 +216,12 @@ def main():
         if t_hbm >= t_mfma:
             ach = gemm_bytes(wl) / (launch_ms * 1e-3) / 1e9
             roof = dict(bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s",
-                        frac=round(ach / PEAK_HBM_GBS, 4), traffic=recorded_traffic())
+                        frac=round(ach / PEAK_HBM_GBS, 4), traffic=recorded_traffic(kname))
         else:
             ach = ops_step / (launch_ms * 1e-3) / 1e12
             roof = dict(bound="mfma", achieved=round(ach, 1), peak=PEAK_INT8_TOPS, unit="TOP/s",
-                        frac=round(ach / PEAK_INT8_TOPS, 4), traffic=recorded_traffic())
-        roof["kernel"] = "k_masked_gemm_grouped (one launch = one denoising step, 112 GEMMs)"
+                        frac=round(ach / PEAK_INT8_TOPS, 4), traffic=recorded_traffic(kname))
+        roof["kernel"] = f"{kname} (one launch = one denoising step, 112 GEMMs)"
         roof["launch_ms"] = round(launch_ms, 4)
         roof["mfma_frac"] = round(ops_step / (launch_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)
         roof["roofline_ms"] = round(max(t_mfma, t_hbm) * 1e3, 4)
@@ -226,7 +240,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "layers": len(wl.layers), "M": wl.layers[0].M,
                    "denoising_steps": wl.T, "stages": wl.S, "output": "fp32",
-                   "launch": "per-layer" if args.per_layer else "grouped per denoising step"},
+                   "launch": "per-layer" if args.per_layer else "grouped per denoising step",
+                   "weights": args.weights},
         "schedule_ms": {"tasq_table": round(ms, 4), "static_b8": round(ms8, 4),
                         "static_max_over_stages": round(msmax, 4)},
         "margin_vs_static_b8": round(1.0 - ms / ms8, 4),

@@ -54,7 +54,8 @@ enum {
     TASQ_ERR_WORKSPACE = -7, /* workspace missing or smaller than required         */
     TASQ_ERR_HIP = -8,       /* a HIP runtime call or kernel launch failed          */
     TASQ_ERR_KIND = -9,      /* unknown layer kind or variant                       */
-    TASQ_ERR_ALIGN = -10     /* workspace not 256-byte aligned                     */
+    TASQ_ERR_ALIGN = -10     /* workspace not 256-byte aligned, or a packed weight
+                                not 16-byte aligned                                */
 };
 
 /* |X| <= 128 and |W_b| <= 128, so |acc| <= 16384 * K < 2^31 iff K <= 131071. */
@@ -64,7 +65,8 @@ enum {
 enum {
     TASQ_VARIANT_AUTO = 0,      /* library picks per shape                         */
     TASQ_VARIANT_MASKED_I8 = 1, /* int8 MFMA GEMM, mask fused into weight staging  */
-    TASQ_VARIANT_BITPLANE = 2   /* reads only the top b planes of W_planes         */
+    TASQ_VARIANT_BITPLANE = 2,  /* reads only the top b planes of W_planes         */
+    TASQ_VARIANT_PACKED = 3     /* int8 MFMA GEMM on W_packed (tasq_pack_weights)  */
 };
 
 /* Layer kinds (tasq_layer.kind). */
@@ -81,6 +83,9 @@ enum {
  *                   that many slices (needs a workspace).
  *   W_planes        bit-plane copy of W as written by tasq_pack_planes; needed
  *                   by the BITPLANE variant (W may then be NULL).
+ *   W_packed        W in the MFMA operand order as written by
+ *                   tasq_pack_weights; used by the PACKED variant and chosen
+ *                   by AUTO when present (W may then be NULL).
  *   workspace       device scratch, 256-byte aligned, owned by the caller;
  *                   used for split-K partial sums and for the schedule's
  *                   device-side layer list.  Size from tasq_workspace_bytes /
@@ -94,13 +99,15 @@ typedef struct tasq_opts {
     const uint32_t *W_planes;
     void *workspace;
     size_t workspace_bytes;
+    const int8_t *W_packed;
 } tasq_opts;
 
 /*
  * y = (X * W_b^T) * sx * sw[n] (+ bias[n]),  W_b = 2^(8-b) floor(W / 2^(8-b)).
  *   X        int8 [M][K] device, activation codes (any value in [-128, 127]).
  *   W        int8 [N][K] device, stored 8-bit weight codes; may be NULL when
- *            the BITPLANE variant is requested with opts->W_planes.
+ *            the BITPLANE variant is requested with opts->W_planes, or when
+ *            opts->W_packed is given (AUTO or PACKED variant).
  *   sx       per-tensor activation scale.
  *   sw       fp32 [N] device, per-output-channel weight scale (read only for y).
  *   bias     fp32 [N] device or NULL.
@@ -154,6 +161,29 @@ int tasq_pack_planes(const int8_t *W, int N, int K, uint32_t *planes_out, void *
 size_t tasq_planes_bytes(int N, int K);
 
 /*
+ * Relayout of a stored weight into the operand order of the int8 matrix
+ * instruction (the codes themselves are unchanged; the mask to b bits is
+ * applied when the kernels read them, so the packed buffer is the one 8-bit
+ * copy shared by every stage, Sec. 3.2 / Sec. 4.3).
+ *   W           int8 [N][K] device (read only).
+ *   packed_out  int8 device, tasq_packed_weight_bytes(N, K) bytes, 16-byte
+ *               aligned: unit (nb, ks) of 1024 bytes, nb < ceil(N/32),
+ *               ks < KS = 4 * ceil(K/128), starts at byte (nb*KS + ks)*1024;
+ *               its bytes 16*l .. 16*l+15 (l = 0..63) hold
+ *               W[32*nb + l%32][32*ks + 16*(l/32) .. +15].  Bytes past row N
+ *               or column K are zero.
+ * The kernels then fetch each 32 x 32 weight fragment with one contiguous
+ * 1 KB load and need no LDS for the weights.  A one-time conversion; a
+ * caller that keeps only the packed buffer (W = NULL) stores the weight once.
+ * Errors: TASQ_ERR_NULL, _DIM, _OVERFLOW, _ALIGN (packed_out not 16-byte
+ * aligned), _HIP.
+ */
+int tasq_pack_weights(const int8_t *W, int N, int K, int8_t *packed_out, void *stream);
+
+/* Bytes of the packed weight: 32 * ceil(N/32) * 128 * ceil(K/128). */
+size_t tasq_packed_weight_bytes(int N, int K);
+
+/*
  * Stage of denoising step t (Sec. 3.2: contiguous stages sharing one mask;
  * Sec. 4.1: 20 steps in four stages, or one stage per step when S = T;
  * App. D.1: stage 0 is the noisiest, first part of the trajectory):
@@ -178,6 +208,7 @@ typedef struct tasq_layer {
     const float *bias;
     int32_t *acc;
     float *y;
+    const int8_t *W_packed;     /* packed copy of W or NULL (tasq_pack_weights) */
 } tasq_layer;
 
 /*
@@ -191,7 +222,8 @@ typedef struct tasq_layer {
  *   1 <= S <= T, 0 <= t_begin <= t_end <= T.
  * With opts->workspace of at least tasq_schedule_workspace_bytes(layers, L)
  * bytes, each step is one grouped launch over every layer's tiles; without it
- * each layer is launched separately.  The whole table and every layer are
+ * each layer is launched separately.  When every layer carries W_packed the
+ * grouped launch reads the packed weights (W may then be NULL).  The whole table and every layer are
  * validated before anything is enqueued.
  */
 int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,

@@ -59,6 +59,7 @@ def lib():
         L.oracle_conv3x3_entries.argtypes = [p, p, ctypes.c_double, p, p, i64, i64, i64,
                                              ctypes.c_int, p, p, i64, p, p]
         L.oracle_pack_planes.argtypes = [p, i64, i64, p]
+        L.oracle_pack_weights.argtypes = [p, i64, i64, p]
         _lib = L
     return _lib
 
@@ -204,6 +205,17 @@ def pack_planes(W) -> np.ndarray:
     planes = np.empty((8, KB, N, 4), np.uint32)
     lib().oracle_pack_planes(_ptr(W), N, K, _ptr(planes))
     return planes
+
+
+def pack_weights(W) -> np.ndarray:
+    """Flat int8 buffer of W [N, K] in the int8 matrix-instruction operand
+    order: W[n][k] at byte ((n//32 * KS + k//32) * 64 + n%32 + 32*((k%32)//16)) * 16
+    + k%16, KS = 4*ceil(K/128), zeros elsewhere."""
+    W = _np(W, np.int8)
+    N, K = W.shape
+    out = np.empty(32 * ((N + 31) // 32) * 128 * ((K + 127) // 128), np.int8)
+    lib().oracle_pack_weights(_ptr(W), N, K, _ptr(out))
+    return out
 
 
 def run_schedule(layers, table, S: int, T: int, t_begin: int, t_end: int, sx: float):

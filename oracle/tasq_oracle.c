@@ -270,3 +270,27 @@ int oracle_pack_planes(const int8_t *W, int64_t N, int64_t K, uint32_t *planes)
     }
     return ORACLE_OK;
 }
+
+/*
+ * The stored weight in the operand order of the int8 matrix instruction (a
+ * storage layout of the same codes; the paper's one 8-bit buffer).  Element
+ * W[n][k] goes to byte
+ *   ((nb * KS + ks) * 64 + l) * 16 + (k % 16),
+ *   nb = n / 32, ks = k / 32, l = n % 32 + 32 * ((k % 32) / 16),
+ * with KS = 4 * ceil(K / 128); the buffer holds 32 * ceil(N / 32) rows by
+ * 128 * ceil(K / 128) columns' worth of bytes, zero where no element lands.
+ */
+int oracle_pack_weights(const int8_t *W, int64_t N, int64_t K, int8_t *packed)
+{
+    int64_t KS = 4 * ((K + 127) / 128);
+    int64_t bytes = 32 * ((N + 31) / 32) * 128 * ((K + 127) / 128);
+    for (int64_t i = 0; i < bytes; ++i)
+        packed[i] = 0;
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t k = 0; k < K; ++k) {
+            int64_t nb = n / 32, ks = k / 32;
+            int64_t l = n % 32 + 32 * ((k % 32) / 16);
+            packed[((nb * KS + ks) * 64 + l) * 16 + k % 16] = W[n * K + k];
+        }
+    return ORACLE_OK;
+}

@@ -7,9 +7,11 @@ computes; every operation is one call into the library.
 from __future__ import annotations
 
 from .api import (  # noqa: F401
-    masked_linear, masked_conv3x3, pack_planes, planes_bytes, stage_of_step, run_schedule,
-    schedule_workspace_bytes, workspace_bytes, make_layer, status_string,
+    masked_linear, masked_conv3x3, pack_planes, planes_bytes, pack_weights, packed_weight_bytes,
+    stage_of_step, run_schedule, schedule_workspace_bytes, workspace_bytes, make_layer,
+    status_string,
 )
 from ._lib import (  # noqa: F401
-    TasqError, VARIANT_AUTO, VARIANT_MASKED_I8, VARIANT_BITPLANE, KIND_LINEAR, KIND_CONV3X3,
+    TasqError, VARIANT_AUTO, VARIANT_MASKED_I8, VARIANT_BITPLANE, VARIANT_PACKED, KIND_LINEAR,
+    KIND_CONV3X3,
 )

@@ -37,13 +37,14 @@ def _need(t: Optional[torch.Tensor], dtype, shape, name):
         raise ValueError(f"{name} must be contiguous")
 
 
-def _opts(variant, planes, workspace, split_k) -> Opts:
+def _opts(variant, planes, workspace, split_k, packed=None) -> Opts:
     o = Opts()
     o.variant = variant
     o.split_k = split_k
     o.W_planes = _ptr(planes)
     o.workspace = _ptr(workspace)
     o.workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    o.W_packed = _ptr(packed)
     return o
 
 
@@ -79,17 +80,36 @@ def pack_planes(W: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Te
     return out
 
 
+def packed_weight_bytes(N: int, K: int) -> int:
+    return _lib.lib().tasq_packed_weight_bytes(N, K)
+
+
+def pack_weights(W: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """int8 W [N, K] (or conv W [N, 3, 3, C]) in the MFMA operand order,
+    a flat int8 buffer of packed_weight_bytes(N, K) bytes."""
+    N = W.shape[0]
+    K = W.numel() // N if N else 0
+    _need(W, torch.int8, tuple(W.shape), "W")
+    nbytes = packed_weight_bytes(N, K)
+    if out is None:
+        out = torch.empty(nbytes, dtype=torch.int8, device=W.device)
+    _need(out, torch.int8, (nbytes,), "packed")
+    check(_lib.lib().tasq_pack_weights(_ptr(W), N, K, _ptr(out), _stream()), "tasq_pack_weights")
+    return out
+
+
 def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: torch.Tensor,
                   b: int, bias: Optional[torch.Tensor] = None, *, want_acc: bool = True,
                   want_y: bool = True, acc: Optional[torch.Tensor] = None,
                   y: Optional[torch.Tensor] = None, variant: int = _lib.VARIANT_AUTO,
-                  planes: Optional[torch.Tensor] = None,
+                  planes: Optional[torch.Tensor] = None, packed: Optional[torch.Tensor] = None,
                   workspace: Optional[torch.Tensor] = None, split_k: int = 0):
     """(acc int32 [M, N] or None, y fp32 [M, N] or None) of the masked layer."""
     M, K = X.shape
     N = sw.shape[0]
     _need(X, torch.int8, (M, K), "X")
     _need(W, torch.int8, (N, K), "W")
+    _need(packed, torch.int8, (packed_weight_bytes(N, K),), "packed")
     _need(sw, torch.float32, (N,), "sw")
     _need(bias, torch.float32, (N,), "bias")
     if want_acc and acc is None:
@@ -102,21 +122,23 @@ def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: tor
         wb = workspace_bytes(M, N, K)
         if wb:
             workspace = torch.empty(wb, dtype=torch.uint8, device=X.device)
-    o = _opts(variant, planes, workspace, split_k)
+    o = _opts(variant, planes, workspace, split_k, packed)
     rc = _lib.lib().tasq_masked_linear(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias), M, N,
                                        K, int(b), _ptr(acc), _ptr(y), ctypes.byref(o), _stream())
     check(rc, "tasq_masked_linear")
     return acc, y
 
 
-def masked_conv3x3(X: torch.Tensor, W: torch.Tensor, sx: float, sw: torch.Tensor, b: int,
-                   bias: Optional[torch.Tensor] = None, *, want_acc: bool = True,
-                   want_y: bool = True, acc=None, y=None, workspace=None, split_k: int = 0):
+def masked_conv3x3(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: torch.Tensor,
+                   b: int, bias: Optional[torch.Tensor] = None, *, want_acc: bool = True,
+                   want_y: bool = True, acc=None, y=None, workspace=None, split_k: int = 0,
+                   packed: Optional[torch.Tensor] = None, variant: int = _lib.VARIANT_AUTO):
     """3x3 / pad 1 conv, X NHWC [H, Wd, C], W [N, 3, 3, C] -> [H, Wd, N]."""
     H, Wd, C = X.shape
-    N = W.shape[0]
+    N = sw.shape[0]
     _need(X, torch.int8, (H, Wd, C), "X")
     _need(W, torch.int8, (N, 3, 3, C), "W")
+    _need(packed, torch.int8, (packed_weight_bytes(N, 9 * C),), "packed")
     _need(sw, torch.float32, (N,), "sw")
     _need(bias, torch.float32, (N,), "bias")
     if want_acc and acc is None:
@@ -125,7 +147,7 @@ def masked_conv3x3(X: torch.Tensor, W: torch.Tensor, sx: float, sw: torch.Tensor
         y = torch.empty((H, Wd, N), dtype=torch.float32, device=X.device)
     _need(acc, torch.int32, (H, Wd, N), "acc")
     _need(y, torch.float32, (H, Wd, N), "y")
-    o = _opts(_lib.VARIANT_AUTO, None, workspace, split_k)
+    o = _opts(variant, None, workspace, split_k, packed)
     rc = _lib.lib().tasq_masked_conv3x3(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias), H, Wd,
                                         C, N, int(b), _ptr(acc), _ptr(y), ctypes.byref(o),
                                         _stream())
@@ -133,7 +155,8 @@ def masked_conv3x3(X: torch.Tensor, W: torch.Tensor, sx: float, sw: torch.Tensor
     return acc, y
 
 
-def make_layer(X, W, sx, sw, bias=None, acc=None, y=None, planes=None, kind=None) -> Layer:
+def make_layer(X, W, sx, sw, bias=None, acc=None, y=None, planes=None, kind=None,
+               packed=None) -> Layer:
     """A tasq_layer for run_schedule; tensors must stay alive while in use."""
     L = Layer()
     if kind is None:
@@ -149,6 +172,7 @@ def make_layer(X, W, sx, sw, bias=None, acc=None, y=None, planes=None, kind=None
     L.sx = float(sx)
     L.X, L.W, L.W_planes = _ptr(X), _ptr(W), _ptr(planes)
     L.sw, L.bias, L.acc, L.y = _ptr(sw), _ptr(bias), _ptr(acc), _ptr(y)
+    L.W_packed = _ptr(packed)
     return L
 
 

@@ -20,7 +20,15 @@ SOURCES = [
     "tile_64x64_k128_w4_pf2.hip",
     "tile_256x128_k64_w4_pf2.hip",
     "tile_128x256_k64_w4_pf2.hip",
+    "ptile_256x256_k128_w8.hip",
+    "ptile_256x256_k64_w8.hip",
+    "ptile_128x256_k128_w4.hip",
+    "ptile_128x256_k64_w4.hip",
+    "ptile_256x128_k64_w4.hip",
+    "ptile_128x128_k64_w4.hip",
+    "ptile_64x64_k128_w4.hip",
     "pack_planes.hip",
+    "pack_weights.hip",
     "skinny.hip",
     "tiles.cpp",
     "tasq_api.cpp",

@@ -1,0 +1,7 @@
+// Packed-weight masked int8 GEMM instantiated for the 256x128 tile, 4 waves (128x64 per wave), BK 64.
+#include "gemm_packed.h"
+
+namespace tasq {
+using TileCfg = CfgP<256, 128, 64, 2, 2>;
+TASQ_DEFINE_PACKED_TILE(ops_ptile_256x128_k64_w4, TileCfg)
+}  // namespace tasq

@@ -34,27 +34,73 @@ int check_dims(long long M, long long N, long long K)
 int check_variant(const tasq_opts *o, const int8_t *W)
 {
     const int v = o ? o->variant : TASQ_VARIANT_AUTO;
-    if (v != TASQ_VARIANT_AUTO && v != TASQ_VARIANT_MASKED_I8 && v != TASQ_VARIANT_BITPLANE)
+    if (v != TASQ_VARIANT_AUTO && v != TASQ_VARIANT_MASKED_I8 && v != TASQ_VARIANT_BITPLANE &&
+        v != TASQ_VARIANT_PACKED)
         return TASQ_ERR_KIND;
     if (o && o->split_k < 0)
         return TASQ_ERR_RANGE;
-    if (v == TASQ_VARIANT_BITPLANE && !(o && o->W_planes))
+    const bool planes = o && o->W_planes, packed = o && o->W_packed;
+    if (v == TASQ_VARIANT_BITPLANE && !planes)
         return TASQ_ERR_LAYOUT;
-    if (v != TASQ_VARIANT_BITPLANE && !W)
+    if (v == TASQ_VARIANT_PACKED && !packed)
+        return TASQ_ERR_LAYOUT;
+    // The row-major weight is needed unless the chosen variant reads another
+    // copy: the planes (BITPLANE) or the packed buffer (PACKED, or AUTO when
+    // one is given).
+    const bool other = v == TASQ_VARIANT_BITPLANE ||
+                       (packed && (v == TASQ_VARIANT_PACKED || v == TASQ_VARIANT_AUTO));
+    if (!other && !W)
         return TASQ_ERR_NULL;
+    if (packed && !aligned16(o->W_packed))
+        return TASQ_ERR_ALIGN;
     if (o && o->workspace && (reinterpret_cast<uintptr_t>(o->workspace) % kWsAlign) != 0)
         return TASQ_ERR_ALIGN;
     return TASQ_OK;
 }
 
-// TASQ_TILE=<id> forces one tile configuration (tuning sweeps only).
-int forced_tile()
+// TASQ_TILE=<id> / TASQ_PTILE=<id> force one tile configuration of the
+// staged / packed-weight kernels (tuning sweeps only).
+int forced(const char *name, int count)
 {
-    const char *e = std::getenv("TASQ_TILE");
+    const char *e = std::getenv(name);
     if (!e || !*e)
         return -1;
     const int t = std::atoi(e);
-    return (t >= 0 && t < tasq::TILE_COUNT) ? t : -1;
+    return (t >= 0 && t < count) ? t : -1;
+}
+
+int forced_tile() { return forced("TASQ_TILE", tasq::TILE_COUNT); }
+
+int forced_ptile() { return forced("TASQ_PTILE", tasq::PTILE_COUNT); }
+
+// Packed-weight tile of a single launch, from a measured sweep over the
+// DiT/UNet layer shapes: the 256x256 tile for very large products and for
+// long K with enough tiles, the 128x128 tile for narrow layers (N <= 1280)
+// with many tokens, the 4-wave 128x256 tile (two workgroups per CU) while
+// it gives a tile per CU, and 64x64 tiles below that.
+int pick_packed_tile(long long M, long long N, long long K)
+{
+    const int f = forced_ptile();
+    if (f >= 0)
+        return f;
+    const long long t256 = ((M + 255) / 256) * ((N + 255) / 256);
+    const long long t128x256 = ((M + 127) / 128) * ((N + 255) / 256);
+    if (M * N * K >= (1LL << 38))
+        return tasq::PTILE_256x256_K128_W8;
+    if (N <= 1280 && M >= 2048)
+        return tasq::PTILE_128x128_K64_W4;
+    if (K >= 4096 && t256 >= 128)
+        return tasq::PTILE_256x256_K128_W8;
+    if (t128x256 >= 256)
+        return tasq::PTILE_128x256_K128_W4;
+    return tasq::PTILE_64x64_K128_W4;
+}
+
+// Packed-weight tile of the grouped per-step launch.
+int pick_packed_grouped_tile()
+{
+    const int f = forced_ptile();
+    return f >= 0 ? f : tasq::PTILE_256x256_K128_W8;
 }
 
 // Tile used for a single (non-grouped) launch, from the measured sweep on
@@ -85,12 +131,26 @@ int pick_grouped_tile()
 
 bool use_bitplane(const tasq_opts *o) { return o && o->variant == TASQ_VARIANT_BITPLANE; }
 
+// The packed-weight kernels run when the layer has a packed buffer and the
+// variant allows it (PACKED, or AUTO).
+bool use_packed(const LayerDesc &d, const tasq_opts *o)
+{
+    const int v = o ? o->variant : TASQ_VARIANT_AUTO;
+    return d.Wp && (v == TASQ_VARIANT_PACKED || v == TASQ_VARIANT_AUTO);
+}
+
 // The buffer-offset fast path also needs each input below 2 GiB.
 bool fits_buffers(const LayerDesc &d)
 {
     const long long xb = d.kind == tasq::KIND_CONV3X3 ? (long long)d.H * d.Wd * d.C
                                                        : (long long)d.M * d.K;
     return xb < (1LL << 31) && (long long)d.N * d.K < (1LL << 31);
+}
+
+// The packed buffer is addressed with 32-bit offsets.
+bool packed_fits(const LayerDesc &d)
+{
+    return tasq::packed_weight_bytes_host(d.N, d.K) < (1ULL << 31);
 }
 
 // Weight-streaming path for skinny activations: needs an int32 [M][N]
@@ -112,7 +172,14 @@ bool skinny_ok(const LayerDesc &d, bool planes)
         return false;
     if (planes)
         return d.P && (long long)8 * ((d.K + 127) / 128) * d.N * 16 < (1LL << 31);
-    return aligned16(d.W);
+    return d.W && aligned16(d.W);
+}
+
+// Activation operand on the 16-byte buffer fast path.
+bool x_aligned(const LayerDesc &d)
+{
+    const int inner = d.kind == tasq::KIND_CONV3X3 ? d.C : d.K;
+    return inner % 16 == 0 && aligned16(d.X) && fits_buffers(d);
 }
 
 int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
@@ -121,13 +188,18 @@ int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
         return TASQ_OK;
     hipError_t e;
     const bool want_planes = use_bitplane(o);
-    if (d.M <= tasq::kSkinnyMaxM && skinny_ok(d, want_planes)) {
+    const bool forced_packed = o && o->variant == TASQ_VARIANT_PACKED;
+    if (d.M <= tasq::kSkinnyMaxM && !forced_packed && skinny_ok(d, want_planes)) {
         if (int32_t *accbuf = skinny_accbuf(d, o)) {
             e = tasq::launch_skinny(d, want_planes, accbuf, stream);
             return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
         }
     }
-    if (use_bitplane(o)) {
+    if (!want_planes && use_packed(d, o) && packed_fits(d)) {
+        e = tasq::packed_tile_ops(pick_packed_tile(d.M, d.N, d.K)).single(d, x_aligned(d), stream);
+        return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+    }
+    if (want_planes) {
         e = tasq::tile_ops(tasq::TILE_64x64_K128_W4_PF2).planes(
             d, (d.K % 16) == 0 && aligned16(d.X) && fits_buffers(d), stream);
     } else {
@@ -149,6 +221,7 @@ LayerDesc make_desc(const tasq_layer &L, const tasq_opts *o)
     d.X = L.X;
     d.W = L.W;
     d.P = L.W_planes ? L.W_planes : (o ? o->W_planes : nullptr);
+    d.Wp = L.W_packed ? L.W_packed : (o ? o->W_packed : nullptr);
     d.sw = L.sw;
     d.bias = L.bias;
     d.acc = L.acc;
@@ -181,6 +254,8 @@ int validate_layer(const tasq_layer &L, const tasq_opts *o)
     tasq_opts local = o ? *o : tasq_opts{};
     if (L.W_planes)
         local.W_planes = L.W_planes;
+    if (L.W_packed)
+        local.W_packed = L.W_packed;
     const bool needs_w = L.N > 0 && L.K > 0;
     if (int rc = check_variant(&local, needs_w ? L.W : reinterpret_cast<const int8_t *>(1)))
         return rc;
@@ -194,6 +269,10 @@ int validate_layer(const tasq_layer &L, const tasq_opts *o)
     }
     if (int rc = check_dims(L.M, L.N, L.K))
         return rc;
+    // Without the row-major copy the packed buffer must be addressable.
+    if (local.W_packed && !L.W && !use_bitplane(&local) &&
+        tasq::packed_weight_bytes_host(L.N, L.K) >= (1ULL << 31))
+        return TASQ_ERR_DIM;
     // Outputs are written through 32-bit buffer offsets (see gemm_core.h).
     if (((long long)L.M + 256) * (long long)L.N * 4 >= (1LL << 31))
         return TASQ_ERR_DIM;
@@ -218,7 +297,7 @@ const char *tasq_status_string(int status)
     case TASQ_ERR_WORKSPACE: return "workspace missing or too small";
     case TASQ_ERR_HIP: return "HIP runtime or launch failure";
     case TASQ_ERR_KIND: return "unknown layer kind or variant";
-    case TASQ_ERR_ALIGN: return "workspace not 256-byte aligned";
+    case TASQ_ERR_ALIGN: return "workspace not 256-byte aligned or packed weight not 16-byte aligned";
     default: return "unknown status";
     }
 }
@@ -319,6 +398,27 @@ int tasq_pack_planes(const int8_t *W, int N, int K, uint32_t *planes_out, void *
     return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
 }
 
+int tasq_pack_weights(const int8_t *W, int N, int K, int8_t *packed_out, void *stream)
+{
+    if (N < 0 || K < 0)
+        return TASQ_ERR_DIM;
+    if (K > TASQ_MAX_K)
+        return TASQ_ERR_OVERFLOW;
+    if (N == 0 || K == 0)
+        return TASQ_OK;
+    if (!W || !packed_out)
+        return TASQ_ERR_NULL;
+    if (!aligned16(packed_out))
+        return TASQ_ERR_ALIGN;
+    hipError_t e = tasq::launch_pack_weights(W, N, K, packed_out, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}
+
+size_t tasq_packed_weight_bytes(int N, int K)
+{
+    return (size_t)tasq::packed_weight_bytes_host(N, K);
+}
+
 size_t tasq_schedule_workspace_bytes(const tasq_layer *layers, int L)
 {
     (void)layers;
@@ -364,22 +464,34 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
 
     // Grouped path: one launch per step over every layer's tiles, with the
     // layer list and bit table resident in the caller's workspace.
+    // When every layer has a packed weight the launch reads those; otherwise
+    // every layer needs its aligned row-major weight.
     const size_t need = tasq_schedule_workspace_bytes(layers, L);
     bool grouped = opts && opts->workspace && opts->workspace_bytes >= need &&
                    !use_bitplane(opts);
+    bool all_packed = true;
+    for (int l = 0; l < L; ++l)
+        all_packed = all_packed && use_packed(descs[l], opts) && packed_fits(descs[l]);
     for (int l = 0; grouped && l < L; ++l) {
         const LayerDesc &d = descs[l];
-        const bool ok = d.kind == tasq::KIND_CONV3X3
-                            ? (d.C % 16 == 0 && aligned16(d.X) && aligned16(d.W))
-                            : (d.K % 16 == 0 && aligned16(d.X) && aligned16(d.W));
-        grouped = ok && fits_buffers(d);
+        grouped = x_aligned(d) && (all_packed || (d.W && aligned16(d.W)));
     }
     if (grouped) {
         bool any_conv = false;
         for (int l = 0; l < L; ++l)
             any_conv = any_conv || descs[l].kind == tasq::KIND_CONV3X3;
-        const tasq::TileOps &ops = tasq::tile_ops(pick_grouped_tile());
-        const tasq::TileShape ts = ops.shape;
+        tasq::TileShape ts;
+        hipError_t (*launch_step)(const LayerDesc *, int, int, const uint8_t *, int, int, bool,
+                                  hipStream_t);
+        if (all_packed) {
+            const tasq::PackedTileOps &ops = tasq::packed_tile_ops(pick_packed_grouped_tile());
+            ts = ops.shape;
+            launch_step = ops.grouped;
+        } else {
+            const tasq::TileOps &ops = tasq::tile_ops(pick_grouped_tile());
+            ts = ops.shape;
+            launch_step = ops.grouped;
+        }
         long long total = 0;
         for (int l = 0; l < L; ++l) {
             LayerDesc &d = descs[l];
@@ -408,7 +520,7 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
             return TASQ_ERR_HIP;
         for (int t = t_begin; t < t_end; ++t) {
             const int s = tasq_stage_of_step(t, S, T);
-            if (ops.grouped(d_descs, L, (int)total, d_table, S, s, any_conv, st) != hipSuccess)
+            if (launch_step(d_descs, L, (int)total, d_table, S, s, any_conv, st) != hipSuccess)
                 return TASQ_ERR_HIP;
         }
         return TASQ_OK;

@@ -15,6 +15,7 @@ struct LayerDesc {
     const int8_t *X;        // [M][K] (linear) or NHWC [H][Wd][C] (conv)
     const int8_t *W;        // [N][K]
     const uint32_t *P;      // bit planes [8][ceil(K/128)][N][4] or null
+    const int8_t *Wp;       // packed weights (MFMA operand order) or null
     const float *sw;        // [N]
     const float *bias;      // [N] or null
     int32_t *acc;           // [M][N] or null
@@ -67,6 +68,40 @@ enum TileId : int {
     TILE_COUNT = 6
 };
 const TileOps &tile_ops(int tile);
+
+// Launchers of one packed-weight tile configuration (gemm_packed.h).
+struct PackedTileOps {
+    TileShape shape;
+    hipError_t (*single)(const LayerDesc &d, bool aligned, hipStream_t stream);
+    hipError_t (*grouped)(const LayerDesc *d_descs, int L, int total_tiles,
+                          const uint8_t *d_table, int S, int stage, bool any_conv,
+                          hipStream_t stream);
+};
+
+enum PackedTileId : int {
+    PTILE_256x256_K128_W8 = 0,  // 256x256 tile, 8 waves (128x64 per wave), BK 128
+    PTILE_256x256_K64_W8 = 1,   // 256x256 tile, 8 waves, BK 64
+    PTILE_128x256_K128_W4 = 2,  // 128x256 tile, 4 waves (64x128 per wave), two workgroups per CU
+    PTILE_128x256_K64_W4 = 3,   // 128x256 tile, 4 waves, BK 64
+    PTILE_256x128_K64_W4 = 4,   // 256x128 tile, 4 waves (128x64 per wave), two workgroups per CU
+    PTILE_128x128_K64_W4 = 5,   // 128x128 tile, 4 waves (64x64 per wave)
+    PTILE_64x64_K128_W4 = 6,    // 64x64 tile, 4 waves (32x32 per wave), BK 128
+    PTILE_COUNT = 7
+};
+const PackedTileOps &packed_tile_ops(int tile);
+
+// Bytes of the packed weight buffer: 32 * ceil(N/32) * 128 * ceil(K/128).
+inline unsigned long long packed_weight_bytes_host(long long N, long long K)
+{
+    if (N <= 0 || K <= 0)
+        return 0;
+    return (unsigned long long)((N + 31) / 32) * 32ULL * (unsigned long long)((K + 127) / 128) *
+           128ULL;
+}
+
+// Packs an [N][K] int8 weight into the MFMA operand order (gemm_packed.h).
+hipError_t launch_pack_weights(const int8_t *W, int N, int K, int8_t *packed,
+                               hipStream_t stream);
 
 hipError_t launch_pack_planes(const int8_t *W, int N, int K, uint32_t *planes,
                               hipStream_t stream);

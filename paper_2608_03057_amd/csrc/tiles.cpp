@@ -26,4 +26,29 @@ const TileOps &tile_ops(int tile)
     return kTiles[tile]();
 }
 
+const PackedTileOps &ops_ptile_256x256_k128_w8();
+const PackedTileOps &ops_ptile_256x256_k64_w8();
+const PackedTileOps &ops_ptile_128x256_k128_w4();
+const PackedTileOps &ops_ptile_128x256_k64_w4();
+const PackedTileOps &ops_ptile_256x128_k64_w4();
+const PackedTileOps &ops_ptile_128x128_k64_w4();
+const PackedTileOps &ops_ptile_64x64_k128_w4();
+
+using PackedOpsFn = const PackedTileOps &(*)();
+static const PackedOpsFn kPackedTiles[PTILE_COUNT] = {
+    &ops_ptile_256x256_k128_w8,
+    &ops_ptile_256x256_k64_w8,
+    &ops_ptile_128x256_k128_w4,
+    &ops_ptile_128x256_k64_w4,
+    &ops_ptile_256x128_k64_w4,
+    &ops_ptile_128x128_k64_w4,
+    &ops_ptile_64x64_k128_w4};
+
+const PackedTileOps &packed_tile_ops(int tile)
+{
+    if (tile < 0 || tile >= PTILE_COUNT)
+        tile = PTILE_128x128_K64_W4;
+    return kPackedTiles[tile]();
+}
+
 }  // namespace tasq

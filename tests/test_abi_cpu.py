@@ -87,6 +87,10 @@ def opts(**kw):
     (dict(W=None, opts=opts(variant=_lib.VARIANT_MASKED_I8)), _lib.TASQ_ERR_NULL),
     (dict(opts=opts(workspace=FAKE + 8, workspace_bytes=1024)), _lib.TASQ_ERR_ALIGN),
     (dict(opts=opts(split_k=-2)), _lib.TASQ_ERR_RANGE),
+    (dict(opts=opts(variant=_lib.VARIANT_PACKED)), _lib.TASQ_ERR_LAYOUT),
+    (dict(opts=opts(W_packed=FAKE + 4)), _lib.TASQ_ERR_ALIGN),
+    (dict(W=None, opts=opts(variant=_lib.VARIANT_MASKED_I8, W_packed=FAKE)), _lib.TASQ_ERR_NULL),
+    (dict(W=None, b=0, opts=opts(W_packed=FAKE)), _lib.TASQ_ERR_BITS),
 ])
 def test_masked_linear_rejects(kw, code):
     assert lin(**kw) == code
@@ -101,6 +105,28 @@ def test_bitplane_variant_accepts_missing_w_only_with_planes():
     o = opts(variant=_lib.VARIANT_BITPLANE, W_planes=FAKE)
     assert lin(W=None, M=0, opts=o) == _lib.TASQ_OK
     assert lin(W=None, b=0, opts=o) == _lib.TASQ_ERR_BITS
+
+
+def test_packed_variant_accepts_missing_w_only_with_packed():
+    for v in (_lib.VARIANT_AUTO, _lib.VARIANT_PACKED):
+        assert lin(W=None, M=0, opts=opts(variant=v, W_packed=FAKE)) == _lib.TASQ_OK
+    assert lin(W=None, M=0, opts=opts(variant=_lib.VARIANT_PACKED)) == _lib.TASQ_ERR_LAYOUT
+
+
+def test_packed_weight_bytes():
+    assert L.tasq_packed_weight_bytes(1152, 1152) == 1152 * 1152
+    assert L.tasq_packed_weight_bytes(33, 129) == 64 * 256
+    assert L.tasq_packed_weight_bytes(1, 1) == 32 * 128
+    assert L.tasq_packed_weight_bytes(0, 5) == 0
+
+
+def test_pack_weights_rejects():
+    assert L.tasq_pack_weights(None, 4, 4, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert L.tasq_pack_weights(FAKE, 4, 4, None, None) == _lib.TASQ_ERR_NULL
+    assert L.tasq_pack_weights(FAKE, -1, 4, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert L.tasq_pack_weights(FAKE, 4, 131072, FAKE, None) == _lib.TASQ_ERR_OVERFLOW
+    assert L.tasq_pack_weights(FAKE, 4, 4, FAKE + 8, None) == _lib.TASQ_ERR_ALIGN
+    assert L.tasq_pack_weights(FAKE, 0, 4, FAKE, None) == _lib.TASQ_OK
 
 
 def test_conv_rejects():
@@ -164,6 +190,10 @@ def test_schedule_rejects_before_launching():
     assert sched([bad_conv, layer()], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_DIM
     assert sched(good, tbl, 4, 20, 0, 1, opts(workspace=FAKE + 16, workspace_bytes=1 << 20)) \
         == _lib.TASQ_ERR_ALIGN
+    # a layer without its row-major weight needs a packed copy
+    assert sched([layer(), layer(W=None)], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_NULL
+    assert sched([layer(), layer(W_packed=FAKE + 2)], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_ALIGN
+    assert sched([layer(W=None, W_packed=FAKE)] * 2, tbl, 4, 20, 0, 0) == _lib.TASQ_OK
     assert L.tasq_run_schedule(None, 2, None, 4, 20, 0, 1, None, None) == _lib.TASQ_ERR_NULL
     assert L.tasq_run_schedule(None, -1, None, 4, 20, 0, 1, None, None) == _lib.TASQ_ERR_RANGE
 

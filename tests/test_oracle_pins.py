@@ -300,6 +300,40 @@ def test_planes_round_trip(N, K):
     assert total == int(bits.sum())
 
 
+def unpack_weights(P, N, K):
+    """Inverse of the packed layout by reshaping: [NB][KS][half][row][16]."""
+    NB, KS = (N + 31) // 32, 4 * ((K + 127) // 128)
+    full = np.asarray(P).reshape(NB, KS, 2, 32, 16).transpose(0, 3, 1, 2, 4)
+    return full.reshape(NB * 32, KS * 32)
+
+
+def test_packed_weights_worked_positions():
+    """Byte positions derived by hand from the layout definition (unit
+    (n//32, k//32) of 1 KB, lane n%32 + 32*((k%32)//16), byte k%16)."""
+    N, K = 40, 200                       # KS = 8
+    W = np.zeros((N, K), np.int8)
+    cases = {(0, 0): 0, (31, 15): 31 * 16 + 15, (0, 16): 32 * 16, (0, 32): 1024,
+             (33, 50): ((1 * 8 + 1) * 64 + 33) * 16 + 2, (39, 199): ((8 + 6) * 64 + 7) * 16 + 7}
+    for i, (nk, pos) in enumerate(cases.items()):
+        W[nk] = i + 1
+    P = oracle.pack_weights(W)
+    assert P.size == 64 * 256
+    for i, (nk, pos) in enumerate(cases.items()):
+        assert P[pos] == i + 1, (nk, pos)
+    assert np.count_nonzero(P) == len(cases)
+
+
+@pytest.mark.parametrize("N,K", [(1, 1), (5, 31), (32, 128), (33, 129), (70, 300)])
+def test_packed_weights_round_trip(N, K):
+    rng = np.random.default_rng(N * 1000 + K)
+    W = rng.integers(-128, 128, (N, K), dtype=np.int64).astype(np.int8)
+    P = oracle.pack_weights(W)
+    assert P.size == 32 * ((N + 31) // 32) * 128 * ((K + 127) // 128)
+    full = unpack_weights(P, N, K)
+    assert np.array_equal(full[:N, :K], W)
+    assert not full[N:].any() and not full[:, K:].any()
+
+
 @pytest.mark.parametrize("b", range(1, 9))
 def test_bit_plane_identity(b):
     """X W_b^T = sum_{p >= 8-b} c_p 2^p X P_p^T, c_7 = -1 (App. G.2: read
