@@ -129,6 +129,50 @@ def time_launches(layers, table, wl, ws, reps):
     return float(np.mean([a.elapsed_time(b) for a, b in evs]))
 
 
+def skinny_schedule(wl, table, keep, device, M=16, reps=3):
+    """The same 112 layers at M tokens (weight-streaming regime): schedule
+    wall time per denoising step with the weights read as int8 rows, as the
+    packed buffer, or as the top b bit planes, at the TASQ table and at a
+    static b = 8.  Reuses the weights already on the GPU."""
+    layers = {"rows": [], "packed": [], "planes": []}
+    hold = []
+    for l, spec in enumerate(wl.layers):
+        W = keep[l][1]
+        if W.dim() == 1:           # packed-only run: no row-major copy to stream
+            return None
+        X = inputs.x_rows(wl, l, np.arange(M), device=device)
+        sw = keep[l][2]
+        y = torch.empty((M, spec.N), dtype=torch.float32, device=device)
+        P = T.pack_weights(W)
+        Q = T.pack_planes(W)
+        hold += [X, y, P, Q]
+        layers["rows"].append(T.make_layer(X, W, wl.sx, sw, None, None, y))
+        layers["packed"].append(T.make_layer(X, None, wl.sx, sw, None, None, y, packed=P))
+        layers["planes"].append(T.make_layer(X, None, wl.sx, sw, None, None, y, planes=Q))
+    torch.cuda.synchronize()
+    ws = torch.empty(T.schedule_workspace_bytes(layers["rows"]), dtype=torch.uint8, device=device)
+    t8 = torch.full_like(table, 8)
+    out = {}
+    for name, ls in layers.items():
+        variant = T.VARIANT_BITPLANE if name == "planes" else T.VARIANT_AUTO
+        for tname, tab in (("tasq", table), ("b8", t8)):
+            T.run_schedule(ls, tab, wl.S, wl.T, 0, wl.T, workspace=ws, variant=variant)
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                T.run_schedule(ls, tab, wl.S, wl.T, 0, wl.T, workspace=ws, variant=variant)
+            b.record()
+            torch.cuda.synchronize()
+            out[f"{name}_{tname}"] = round(a.elapsed_time(b) / reps / wl.T, 4)
+    wbytes = sum(float(s.N * s.K) for s in wl.layers)
+    mean_b = float(table.float().mean())
+    return {"M": M, "ms_per_denoising_step": out,
+            "weight_bytes_per_step": {"int8": wbytes, "planes_tasq": wbytes * mean_b / 8.0},
+            "planes_speedup_vs_b8": round(out["planes_b8"] / out["planes_tasq"], 3),
+            "planes_tasq_vs_rows_b8": round(out["rows_b8"] / out["planes_tasq"], 3)}
+
+
 def cpu_baseline(wl, table, budget_s=15.0):
     """The CPU oracle on a bounded sample: the first R rows of each of block
     0's four linears at its stage-0 b, R grown until the sample takes about
@@ -161,6 +205,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--tokens", type=int, default=None, help="override M (skinny sweeps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-skinny", action="store_true",
+                    help="skip the extra weight-streaming (M=16) schedule measurement")
     ap.add_argument("--per-layer", action="store_true",
                     help="launch each layer separately instead of one grouped launch per step")
     ap.add_argument("--weights", choices=("packed", "rowmajor"), default="rowmajor",
@@ -228,6 +274,11 @@ def main():
         roof["algorithmic_bytes"] = gemm_bytes(wl)
         roof["algorithmic_ops"] = ops_step
 
+    skinny = None
+    if not args.no_skinny and not args.per_layer:
+        log("timing the weight-streaming schedule at M=16")
+        skinny = skinny_schedule(wl, table, keep, dev)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle sample")
@@ -247,6 +298,7 @@ def main():
         "margin_vs_static_b8": round(1.0 - ms / ms8, 4),
         "mean_bits": round(float(table.float().mean()), 3),
         "roofline": roof,
+        "skinny_schedule": skinny,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

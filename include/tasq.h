@@ -79,18 +79,18 @@ enum {
 /*
  * Optional controls; pass NULL for defaults (AUTO variant, no workspace).
  *   variant         TASQ_VARIANT_*.
- *   split_k         0 = library choice, 1 = never split K, >1 = split K into
- *                   that many slices (needs a workspace).
+ *   split_k         reserved, must be >= 0: every output tile accumulates all
+ *                   of K in one workgroup.
  *   W_planes        bit-plane copy of W as written by tasq_pack_planes; needed
  *                   by the BITPLANE variant (W may then be NULL).
  *   W_packed        W in the MFMA operand order as written by
  *                   tasq_pack_weights; used by the PACKED variant and chosen
  *                   by AUTO when present (W may then be NULL).
  *   workspace       device scratch, 256-byte aligned, owned by the caller;
- *                   used for split-K partial sums and for the schedule's
- *                   device-side layer list.  Size from tasq_workspace_bytes /
- *                   tasq_schedule_workspace_bytes.  Contents need no
- *                   initialisation and are left unspecified.
+ *                   holds the schedule's device-side layer list and bit
+ *                   table.  Size from tasq_schedule_workspace_bytes.
+ *                   Contents need no initialisation and are left
+ *                   unspecified.
  *   workspace_bytes its size in bytes.
  */
 typedef struct tasq_opts {
@@ -221,15 +221,20 @@ typedef struct tasq_layer {
  *   b_table  host uint8 [L][S], entries in [1, 8] (read during the call only).
  *   1 <= S <= T, 0 <= t_begin <= t_end <= T.
  * With opts->workspace of at least tasq_schedule_workspace_bytes(layers, L)
- * bytes, each step is one grouped launch over every layer's tiles; without it
- * each layer is launched separately.  When every layer carries W_packed the
- * grouped launch reads the packed weights (W may then be NULL).  The whole table and every layer are
+ * bytes, each step is one grouped launch over every layer's work; without it
+ * each layer is launched separately.  The grouped launch streams the weights
+ * (one workgroup per 32 output channels) when every layer has M <= 64 and
+ * the same weight source (bit planes with the BITPLANE variant, packed
+ * buffers, or row-major W); otherwise it tiles every layer's GEMM, reading
+ * the packed weights when every layer carries W_packed (W may then be NULL)
+ * and the row-major W otherwise.  The whole table and every layer are
  * validated before anything is enqueued.
  */
 int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
                       int t_begin, int t_end, const tasq_opts *opts, void *stream);
 
-/* Workspace a single layer call may use (0 when it never needs one). */
+/* Workspace a single layer call may use: 0, no single-layer path needs one
+ * (kept so that callers can size a workspace without knowing the kernels). */
 size_t tasq_workspace_bytes(int M, int N, int K);
 
 /* Workspace for the grouped schedule over these layers (host array). */

@@ -1,26 +1,34 @@
 // Masked linear for skinny activations (M <= 64): weight-streaming kernels.
 //
-// With few activation rows the layer reads each weight once and does little
-// arithmetic per byte, so its time is the weight stream.  Two sources:
-//   * int8 rows, masked with one v_and_b32 per 4 weights: 1 byte per weight;
+// With few activation rows a layer reads each weight once and does little
+// arithmetic per byte, so its time is the weight stream.  Three sources of
+// the weight operand:
+//   * int8 rows [N][K], masked with one v_and_b32 per 4 weights;
+//   * the packed buffer (tasq_pack_weights): each 32 x 32 fragment is one
+//     contiguous 1 KB, so a wave's weight loads are fully coalesced;
 //   * bit planes, reading only the top b planes (App. G.2; the dropped
 //     planes are never fetched): b/8 byte per weight, rebuilt into the
 //     two's-complement bytes of W_b in registers (a rotate and an AND-OR
 //     place 4 bits of a plane in 4 bytes).
-// Each wave owns 32 output channels and a slice of K (no LDS, no barriers),
-// computes acc^T = W_b X^T with v_mfma_i32_32x32x32_i8 (A = 32 weight rows,
-// B = up to 32 activation rows per m-tile), and adds its int32 partial sums
-// into a zeroed int32 buffer with atomics, which is exact and independent of
-// the order.  A finishing kernel applies y = acc * sx * sw[n] + bias[n].
-#include <algorithm>
-
+// A workgroup owns 32 output channels; its 8 waves take interleaved
+// 128-byte K blocks and compute acc^T = W_b X^T with v_mfma_i32_32x32x32_i8
+// (A = 32 weight rows, B = up to 32 activation rows per m-tile).  The waves'
+// exact int32 partial sums are added through LDS in a fixed order and the
+// workgroup writes acc and y = acc * sx * sw[n] + bias[n] itself: one launch,
+// no atomics, no workspace.  The grouped form covers every layer of a
+// denoising step in one launch, its b taken from the (layer, stage) table.
 #include "gemm_core.h"
+#include "gemm_packed.h"
 
 namespace tasq {
 
 namespace {
 
-constexpr int SK_KBLK = 128;          // K bytes per plane block (one 16-byte word group)
+constexpr int SK_WAVES = 8;
+constexpr int SK_KBLK = 128;          // K bytes per block (four 32-wide MFMA steps)
+constexpr int SK_PAD = 65;            // LDS row pitch (ints) of the reduction buffer
+
+enum SkinnySource : int { SRC_ROWS = 0, SRC_PACKED = 1, SRC_PLANES = 2 };
 
 // The lane half's 16 weights of plane word w (groups 4h .. 4h+3) placed at
 // bit `up` of 16 bytes and OR-ed into 4 dwords.
@@ -32,34 +40,27 @@ __device__ __forceinline__ void plane_half(uint32_t w, int h, int up, v4i &acc)
     acc.w = (int)plane_group(w, 4 * h + 3, up, (uint32_t)acc.w);
 }
 
-// One wave: 32 output channels n0..n0+31, K blocks [kb0, kb1) of 128 bytes,
-// all m-tiles (MT <= 2 tiles of 32 rows).
-template <bool PLANES, int MT>
-__global__ void __launch_bounds__(256) k_skinny(LayerDesc d, int blocks_per_wave, int nkb,
-                                                int32_t *accbuf)
+// Output channels 32*nb .. 32*nb+31 of layer d at b bits.  red holds
+// SK_WAVES * MT * 16 rows of SK_PAD ints.
+template <int SRC, int MT>
+__device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, int *red)
 {
-    const int lane = threadIdx.x & 63;
-    const int gw = (blockIdx.x * 256 + threadIdx.x) >> 6;     // global wave id
-    const int ntiles = (d.N + 31) / 32;
-    const int nsl = (nkb + blocks_per_wave - 1) / blocks_per_wave;
-    if (gw >= ntiles * nsl)
-        return;
-    const int nt = gw % ntiles, sl = gw / ntiles;
-    const int n0 = nt * 32;
-    const int kb0 = sl * blocks_per_wave;
-    const int kb1 = min(nkb, kb0 + blocks_per_wave);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
     const int h = lane >> 5, r = lane & 31;
+    const int n0 = nb * 32;
     const int n = n0 + r;
+    const int nkb = (d.K + SK_KBLK - 1) / SK_KBLK;
 
     const rsrc_t rX = make_rsrc(d.X, (uint32_t)d.M * (uint32_t)d.K);
-    // activation row m = 32*mt + r, lane half h: bytes 16h.. of each 32-k step
     uint32_t offX[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         const int m = 32 * mt + r;
         offX[mt] = m < d.M ? (uint32_t)m * (uint32_t)d.K + 16 * h : kOOB;
     }
-    const int msk = (int)keep_mask_dword(d.bits);
+    const int msk = (int)keep_mask_dword(b);
 
     v16i acc[MT];
 #pragma unroll
@@ -68,36 +69,94 @@ __global__ void __launch_bounds__(256) k_skinny(LayerDesc d, int blocks_per_wave
 
     rsrc_t rW;
     uint32_t offW;
-    if constexpr (PLANES) {
-        // words planes[q][kb][n][0..3]; plane stride KB*N*16 bytes
-        rW = make_rsrc(d.P, (uint32_t)8 * (uint32_t)nkb * (uint32_t)d.N * 16u);
+    uint32_t plane_stride = 0;
+    if constexpr (SRC == SRC_PLANES) {
+        // words planes[q][kb][n][0..3]
+        plane_stride = (uint32_t)nkb * (uint32_t)d.N * 16u;
+        rW = make_rsrc(d.P, 8u * plane_stride);
         offW = n < d.N ? (uint32_t)n * 16u : kOOB;
+    } else if constexpr (SRC == SRC_PACKED) {
+        // unit (nb, 4*kb + s), this lane's 16 bytes
+        const int NB = (d.N + 31) / 32;
+        rW = make_rsrc(d.Wp, (uint32_t)packed_weight_bytes(d.N, d.K));
+        offW = nb < NB ? (uint32_t)nb * (uint32_t)(4 * nkb) * 1024u + (uint32_t)lane * 16u : kOOB;
     } else {
         rW = make_rsrc(d.W, (uint32_t)d.N * (uint32_t)d.K);
         offW = n < d.N ? (uint32_t)n * (uint32_t)d.K + 16 * h : kOOB;
     }
-    const uint32_t plane_stride = (uint32_t)nkb * (uint32_t)d.N * 16u;
-    const int b = d.bits;
 
-    for (int kb = kb0; kb < kb1; ++kb) {
+    // One K block's operands: every load of the block is issued before any
+    // is used.  Latency is covered by the other waves of the CU rather than
+    // by a second buffer, which would halve the waves that fit.  Planes: the
+    // two lanes of a weight row (halves h = 0, 1) need the same plane words,
+    // so lane half h loads planes h, h+2, .. (64 distinct 16-byte chunks per
+    // load) and v_permlane32_swap hands each half the other's words.
+    constexpr int NWORDS = 4;
+    struct Block {
+        v4i w[NWORDS];
+        v4i x[4][MT];
+    };
+    auto load = [&](int kb, Block &bl) {
         const uint32_t k0 = (uint32_t)kb * SK_KBLK;
-        // weight operand for the 4 sub-steps of this 128-byte K block
-        v4i wq[4];
-        if constexpr (PLANES) {
-            wq[0] = wq[1] = wq[2] = wq[3] = zero4();
+        if constexpr (SRC == SRC_PLANES) {
             const uint32_t base = offW + (uint32_t)kb * (uint32_t)d.N * 16u;
-            for (int q = 0; q < b; ++q) {
-                const v4i words = ld16(rW, base + (uint32_t)q * plane_stride);
-                const int up = 7 - q;
-                plane_half((uint32_t)words.x, h, up, wq[0]);
-                plane_half((uint32_t)words.y, h, up, wq[1]);
-                plane_half((uint32_t)words.z, h, up, wq[2]);
-                plane_half((uint32_t)words.w, h, up, wq[3]);
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+                const int q = 2 * qq + h;
+                bl.w[qq] = zero4();
+                if (2 * qq < b)
+                    bl.w[qq] = ld16(rW, q < b ? base + (uint32_t)q * plane_stride : kOOB);
             }
         } else {
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                v4i v = ld16(rW, offW + k0 + 32 * s);
+                if constexpr (SRC == SRC_PACKED)
+                    bl.w[s] = ld16(rW, offW + (uint32_t)(4 * kb + s) * 1024u);
+                else
+                    bl.w[s] = ld16(rW, offW + k0 + 32 * s);
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                bl.x[s][mt] = ld16(rX, offX[mt] + k0 + 32 * s);
+    };
+    auto compute = [&](int kb, const Block &bl) {
+        const uint32_t k0 = (uint32_t)kb * SK_KBLK;
+        v4i wq[4];
+        if constexpr (SRC == SRC_PLANES) {
+            wq[0] = wq[1] = wq[2] = wq[3] = zero4();
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+                if (2 * qq < b) {
+                    // even plane 2qq from the lower lanes, odd plane 2qq+1
+                    // (zero past b) from the upper lanes, on every lane
+                    const v4i mine = bl.w[qq];
+                    v4i ev, od;
+                    auto sx = __builtin_amdgcn_permlane32_swap(mine.x, mine.x, false, false);
+                    auto sy = __builtin_amdgcn_permlane32_swap(mine.y, mine.y, false, false);
+                    auto sz = __builtin_amdgcn_permlane32_swap(mine.z, mine.z, false, false);
+                    auto sw = __builtin_amdgcn_permlane32_swap(mine.w, mine.w, false, false);
+                    ev = v4i{(int)sx[0], (int)sy[0], (int)sz[0], (int)sw[0]};
+                    od = v4i{(int)sx[1], (int)sy[1], (int)sz[1], (int)sw[1]};
+                    const int up = 7 - 2 * qq;
+                    plane_half((uint32_t)ev.x, h, up, wq[0]);
+                    plane_half((uint32_t)ev.y, h, up, wq[1]);
+                    plane_half((uint32_t)ev.z, h, up, wq[2]);
+                    plane_half((uint32_t)ev.w, h, up, wq[3]);
+                    if (2 * qq + 1 < b) {
+                        plane_half((uint32_t)od.x, h, up - 1, wq[0]);
+                        plane_half((uint32_t)od.y, h, up - 1, wq[1]);
+                        plane_half((uint32_t)od.z, h, up - 1, wq[2]);
+                        plane_half((uint32_t)od.w, h, up - 1, wq[3]);
+                    }
+                }
+            }
+        } else {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                v4i v = bl.w[s];
                 v.x &= msk;
                 v.y &= msk;
                 v.z &= msk;
@@ -105,110 +164,149 @@ __global__ void __launch_bounds__(256) k_skinny(LayerDesc d, int blocks_per_wave
                 wq[s] = v;
             }
         }
-        // columns past K: zero the weights (the activations there may hold
-        // the next row)
-        if (k0 + SK_KBLK > (uint32_t)d.K) {
+        // Columns past K: zero the weights (row-major loads there may hold
+        // the next row; packed and plane layouts are zero already).
+        if (SRC == SRC_ROWS && k0 + SK_KBLK > (uint32_t)d.K) {
 #pragma unroll
             for (int s = 0; s < 4; ++s)
                 if (k0 + 32 * s + 16 * h >= (uint32_t)d.K)
                     wq[s] = zero4();
         }
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
+        for (int s = 0; s < 4; ++s)
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                const v4i xv = ld16(rX, offX[mt] + k0 + 32 * s);
-                acc[mt] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wq[s], xv, acc[mt], 0, 0, 0);
-            }
-        }
+            for (int mt = 0; mt < MT; ++mt)
+                acc[mt] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wq[s], bl.x[s][mt], acc[mt], 0, 0,
+                                                                0);
+    };
+
+    for (int kb = wave; kb < nkb; kb += SK_WAVES) {
+        Block bl;
+        load(kb, bl);
+        compute(kb, bl);
     }
-    // acc^T block: register v of lane l is weight row 8*(v/4) + 4*(l/32) + v%4
-    // (output channel), column l%32 (activation row)
+
+    // Each wave's partial block: register v of lane l is channel
+    // 8*(v/4) + 4*(l/32) + v%4, token l%32.
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int m = 32 * mt + (lane & 31);
-        if (m >= d.M)
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+            red[((wave * MT + mt) * 16 + v) * SK_PAD + lane] = acc[mt][v];
+    __syncthreads();
+
+    // Thread t writes channel n0 + t%32 of tokens t/32 + 16*i: 32 threads
+    // cover one 128-byte output row segment.
+    const int col = tid & 31;
+    const int nn = n0 + col;
+    const int vv = 4 * (col >> 3) + (col & 3);
+    const int lh = 32 * ((col & 7) >> 2);
+    float scale = 0.f, bias = 0.f;
+    if (nn < d.N && d.y) {
+        scale = d.sx * d.sw[nn];
+        if (d.bias)
+            bias = d.bias[nn];
+    }
+#pragma unroll
+    for (int i = 0; i < 2 * MT; ++i) {
+        const int row = (tid >> 5) + 16 * i;
+        if (row >= d.M || nn >= d.N)
             continue;
+        const int mt = row >> 5;
+        const int ln = (row & 31) + lh;
+        int sum = 0;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int nn = n0 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-            if (nn < d.N)
-                atomicAdd(accbuf + (size_t)m * d.N + nn, acc[mt][v]);
-        }
-    }
-}
-
-__global__ void k_fill_zero(int32_t *p, long long n)
-{
-    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (long long)gridDim.x * blockDim.x)
-        p[i] = 0;
-}
-
-// y = acc * (sx * sw[n]) + bias[n]; acc copied out when it lives in scratch.
-__global__ void k_skinny_finish(LayerDesc d, const int32_t *accbuf)
-{
-    const long long total = (long long)d.M * d.N;
-    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (long long)gridDim.x * blockDim.x) {
-        const int nn = (int)(i % d.N);
-        const int a = accbuf[i];
-        if (d.acc && d.acc != accbuf)
-            d.acc[i] = a;
+        for (int w = 0; w < SK_WAVES; ++w)
+            sum += red[((w * MT + mt) * 16 + vv) * SK_PAD + ln];
+        const size_t o = (size_t)row * (size_t)d.N + (size_t)nn;
+        if (d.acc)
+            d.acc[o] = sum;
         if (d.y)
-            d.y[i] = (float)a * (d.sx * d.sw[nn]) + (d.bias ? d.bias[nn] : 0.f);
+            d.y[o] = (float)sum * scale + bias;
     }
+}
+
+template <int SRC, int MT>
+__global__ void __launch_bounds__(SK_WAVES * 64) k_skinny(LayerDesc d)
+{
+    __shared__ int red[SK_WAVES * MT * 16 * SK_PAD];
+    skinny_block<SRC, MT>(d, d.bits, blockIdx.x, red);
+}
+
+// One launch per denoising step over every layer's 32-channel blocks;
+// d.tile_begin is the layer's first block.
+template <int SRC, int MT>
+__global__ void __launch_bounds__(SK_WAVES * 64)
+k_skinny_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *table, int S, int stage)
+{
+    __shared__ int red[SK_WAVES * MT * 16 * SK_PAD];
+    const int t = blockIdx.x;
+    int lo = 0, hi = L - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (descs[mid].tile_begin <= t)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    const LayerDesc d = descs[lo];
+    skinny_block<SRC, MT>(d, table[lo * S + stage], t - d.tile_begin, red);
+}
+
+template <int SRC>
+hipError_t launch_single_src(const LayerDesc &d, hipStream_t stream)
+{
+    const unsigned grid = (unsigned)((d.N + 31) / 32);
+    if (d.M > 32)
+        hipLaunchKernelGGL((k_skinny<SRC, 2>), dim3(grid), dim3(SK_WAVES * 64), 0, stream, d);
+    else
+        hipLaunchKernelGGL((k_skinny<SRC, 1>), dim3(grid), dim3(SK_WAVES * 64), 0, stream, d);
+    return hipGetLastError();
+}
+
+template <int SRC>
+hipError_t launch_grouped_src(const LayerDesc *d_descs, int L, int total, int max_m,
+                              const uint8_t *d_table, int S, int stage, hipStream_t stream)
+{
+    if (max_m > 32)
+        hipLaunchKernelGGL((k_skinny_grouped<SRC, 2>), dim3((unsigned)total), dim3(SK_WAVES * 64),
+                           0, stream, d_descs, L, d_table, S, stage);
+    else
+        hipLaunchKernelGGL((k_skinny_grouped<SRC, 1>), dim3((unsigned)total), dim3(SK_WAVES * 64),
+                           0, stream, d_descs, L, d_table, S, stage);
+    return hipGetLastError();
 }
 
 }  // namespace
 
-// K blocks per wave: enough waves (about 8 per SIMD) to cover HBM latency.
-static int skinny_blocks_per_wave(const LayerDesc &d)
+hipError_t launch_skinny(const LayerDesc &d, SkinnyWeights src, hipStream_t stream)
 {
-    const int nkb = (d.K + SK_KBLK - 1) / SK_KBLK;
-    const long long ntiles = (d.N + 31) / 32;
-    const long long target_waves = 256LL * 4 * 8;
-    long long slices = (target_waves + ntiles - 1) / ntiles;
-    if (slices > nkb)
-        slices = nkb;
-    if (slices < 1)
-        slices = 1;
-    return (int)((nkb + slices - 1) / slices);
+    if (d.M > kSkinnyMaxM || d.N <= 0 || d.M <= 0)
+        return hipErrorInvalidValue;
+    switch (src) {
+    case SKINNY_PLANES: return launch_single_src<SRC_PLANES>(d, stream);
+    case SKINNY_PACKED: return launch_single_src<SRC_PACKED>(d, stream);
+    default: return launch_single_src<SRC_ROWS>(d, stream);
+    }
 }
 
-hipError_t launch_skinny(const LayerDesc &d, bool planes, int32_t *accbuf, hipStream_t stream)
+hipError_t launch_skinny_grouped(const LayerDesc *d_descs, int L, int total_blocks, int max_m,
+                                 SkinnyWeights src, const uint8_t *d_table, int S, int stage,
+                                 hipStream_t stream)
 {
-    if (d.M > 64)
+    if (max_m > kSkinnyMaxM)
         return hipErrorInvalidValue;
-    const long long total = (long long)d.M * d.N;
-    const int fill_blocks = (int)std::min<long long>(1024, (total + 255) / 256);
-    hipLaunchKernelGGL(k_fill_zero, dim3(fill_blocks), dim3(256), 0, stream, accbuf, total);
-    const int nkb = (d.K + SK_KBLK - 1) / SK_KBLK;
-    const int bpw = skinny_blocks_per_wave(d);
-    const long long waves = (long long)((d.N + 31) / 32) * ((nkb + bpw - 1) / bpw);
-    const unsigned grid = (unsigned)((waves + 3) / 4);
-    if (nkb > 0) {
-        if (planes) {
-            if (d.M > 32)
-                hipLaunchKernelGGL((k_skinny<true, 2>), dim3(grid), dim3(256), 0, stream, d, bpw,
-                                   nkb, accbuf);
-            else
-                hipLaunchKernelGGL((k_skinny<true, 1>), dim3(grid), dim3(256), 0, stream, d, bpw,
-                                   nkb, accbuf);
-        } else {
-            if (d.M > 32)
-                hipLaunchKernelGGL((k_skinny<false, 2>), dim3(grid), dim3(256), 0, stream, d, bpw,
-                                   nkb, accbuf);
-            else
-                hipLaunchKernelGGL((k_skinny<false, 1>), dim3(grid), dim3(256), 0, stream, d, bpw,
-                                   nkb, accbuf);
-        }
+    switch (src) {
+    case SKINNY_PLANES:
+        return launch_grouped_src<SRC_PLANES>(d_descs, L, total_blocks, max_m, d_table, S, stage,
+                                              stream);
+    case SKINNY_PACKED:
+        return launch_grouped_src<SRC_PACKED>(d_descs, L, total_blocks, max_m, d_table, S, stage,
+                                              stream);
+    default:
+        return launch_grouped_src<SRC_ROWS>(d_descs, L, total_blocks, max_m, d_table, S, stage,
+                                            stream);
     }
-    if (d.y || (d.acc && d.acc != accbuf)) {
-        hipLaunchKernelGGL(k_skinny_finish, dim3(fill_blocks), dim3(256), 0, stream, d,
-                           (const int32_t *)accbuf);
-    }
-    return hipGetLastError();
 }
 
 }  // namespace tasq

@@ -153,33 +153,31 @@ bool packed_fits(const LayerDesc &d)
     return tasq::packed_weight_bytes_host(d.N, d.K) < (1ULL << 31);
 }
 
-// Weight-streaming path for skinny activations: needs an int32 [M][N]
-// buffer to accumulate into (acc_out, else the caller's workspace).
-int32_t *skinny_accbuf(const LayerDesc &d, const tasq_opts *o)
-{
-    if (d.acc)
-        return d.acc;
-    const size_t need = (size_t)d.M * (size_t)d.N * 4;
-    if (o && o->workspace && o->workspace_bytes >= need)
-        return static_cast<int32_t *>(o->workspace);
-    return nullptr;
-}
-
-bool skinny_ok(const LayerDesc &d, bool planes)
-{
-    if (d.kind != tasq::KIND_LINEAR || d.M > tasq::kSkinnyMaxM || d.K % 16 != 0 ||
-        !aligned16(d.X) || !fits_buffers(d))
-        return false;
-    if (planes)
-        return d.P && (long long)8 * ((d.K + 127) / 128) * d.N * 16 < (1LL << 31);
-    return d.W && aligned16(d.W);
-}
-
 // Activation operand on the 16-byte buffer fast path.
 bool x_aligned(const LayerDesc &d)
 {
     const int inner = d.kind == tasq::KIND_CONV3X3 ? d.C : d.K;
     return inner % 16 == 0 && aligned16(d.X) && fits_buffers(d);
+}
+
+// Weight-streaming path for skinny activations: linear layers with M <= 64
+// and 16-byte activation rows, reading the planes (BITPLANE), the packed
+// buffer (when the variant allows it) or the aligned int8 rows.  Returns
+// false when none applies.
+bool skinny_source(const LayerDesc &d, const tasq_opts *o, tasq::SkinnyWeights &src)
+{
+    if (d.kind != tasq::KIND_LINEAR || d.M > tasq::kSkinnyMaxM || !x_aligned(d))
+        return false;
+    if (use_bitplane(o)) {
+        src = tasq::SKINNY_PLANES;
+        return d.P && (long long)8 * ((d.K + 127) / 128) * d.N * 16 < (1LL << 31);
+    }
+    if (use_packed(d, o) && packed_fits(d)) {
+        src = tasq::SKINNY_PACKED;
+        return true;
+    }
+    src = tasq::SKINNY_ROWS;
+    return d.W && aligned16(d.W);
 }
 
 int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
@@ -188,12 +186,10 @@ int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
         return TASQ_OK;
     hipError_t e;
     const bool want_planes = use_bitplane(o);
-    const bool forced_packed = o && o->variant == TASQ_VARIANT_PACKED;
-    if (d.M <= tasq::kSkinnyMaxM && !forced_packed && skinny_ok(d, want_planes)) {
-        if (int32_t *accbuf = skinny_accbuf(d, o)) {
-            e = tasq::launch_skinny(d, want_planes, accbuf, stream);
-            return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
-        }
+    tasq::SkinnyWeights src;
+    if (skinny_source(d, o, src)) {
+        e = tasq::launch_skinny(d, src, stream);
+        return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
     }
     if (!want_planes && use_packed(d, o) && packed_fits(d)) {
         e = tasq::packed_tile_ops(pick_packed_tile(d.M, d.N, d.K)).single(d, x_aligned(d), stream);
@@ -318,10 +314,10 @@ size_t tasq_planes_bytes(int N, int K)
 
 size_t tasq_workspace_bytes(int M, int N, int K)
 {
+    (void)M;
+    (void)N;
     (void)K;
-    if (M <= 0 || N <= 0 || M > tasq::kSkinnyMaxM)
-        return 0;
-    return (size_t)M * (size_t)N * 4;   // int32 accumulators of the skinny path
+    return 0;   // no single-layer path uses a workspace
 }
 
 int tasq_masked_linear(const int8_t *X, const int8_t *W, float sx, const float *sw,
@@ -464,26 +460,43 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
 
     // Grouped path: one launch per step over every layer's tiles, with the
     // layer list and bit table resident in the caller's workspace.
-    // When every layer has a packed weight the launch reads those; otherwise
-    // every layer needs its aligned row-major weight.
+    // Grouped launches need the workspace for the device-side layer list.
+    // Three kinds, each over every layer's work units in one launch per step:
+    //  - weight streaming, when every layer is skinny (M <= 64) with the same
+    //    weight source: one unit per 32 output channels;
+    //  - packed-weight GEMM, when every layer has a packed weight;
+    //  - staged GEMM, when every layer has its aligned row-major weight.
+    // Otherwise each layer is launched on its own.
     const size_t need = tasq_schedule_workspace_bytes(layers, L);
-    bool grouped = opts && opts->workspace && opts->workspace_bytes >= need &&
-                   !use_bitplane(opts);
-    bool all_packed = true;
+    const bool have_ws = opts && opts->workspace && opts->workspace_bytes >= need;
+    tasq::SkinnyWeights src = tasq::SKINNY_ROWS;
+    bool all_skinny = have_ws;
+    int max_m = 0;
+    for (int l = 0; all_skinny && l < L; ++l) {
+        tasq::SkinnyWeights sl;
+        all_skinny = skinny_source(descs[l], opts, sl) && (l == 0 || sl == src);
+        src = sl;
+        max_m = descs[l].M > max_m ? descs[l].M : max_m;
+    }
+    bool all_packed = !use_bitplane(opts);
     for (int l = 0; l < L; ++l)
         all_packed = all_packed && use_packed(descs[l], opts) && packed_fits(descs[l]);
+    bool grouped = have_ws && !use_bitplane(opts);
     for (int l = 0; grouped && l < L; ++l) {
         const LayerDesc &d = descs[l];
         grouped = x_aligned(d) && (all_packed || (d.W && aligned16(d.W)));
     }
-    if (grouped) {
+    if (all_skinny || grouped) {
         bool any_conv = false;
         for (int l = 0; l < L; ++l)
             any_conv = any_conv || descs[l].kind == tasq::KIND_CONV3X3;
-        tasq::TileShape ts;
+        tasq::TileShape ts = {32, 32, 128};
         hipError_t (*launch_step)(const LayerDesc *, int, int, const uint8_t *, int, int, bool,
-                                  hipStream_t);
-        if (all_packed) {
+                                  hipStream_t) = nullptr;
+        if (all_skinny) {
+            // one unit per 32 output channels, all tokens
+            ts = {tasq::kSkinnyMaxM, 32, 128};
+        } else if (all_packed) {
             const tasq::PackedTileOps &ops = tasq::packed_tile_ops(pick_packed_grouped_tile());
             ts = ops.shape;
             launch_step = ops.grouped;
@@ -520,7 +533,11 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
             return TASQ_ERR_HIP;
         for (int t = t_begin; t < t_end; ++t) {
             const int s = tasq_stage_of_step(t, S, T);
-            if (launch_step(d_descs, L, (int)total, d_table, S, s, any_conv, st) != hipSuccess)
+            const hipError_t e =
+                all_skinny ? tasq::launch_skinny_grouped(d_descs, L, (int)total, max_m, src,
+                                                         d_table, S, s, st)
+                           : launch_step(d_descs, L, (int)total, d_table, S, s, any_conv, st);
+            if (e != hipSuccess)
                 return TASQ_ERR_HIP;
         }
         return TASQ_OK;

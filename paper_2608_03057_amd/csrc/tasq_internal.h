@@ -106,10 +106,15 @@ hipError_t launch_pack_weights(const int8_t *W, int N, int K, int8_t *packed,
 hipError_t launch_pack_planes(const int8_t *W, int N, int K, uint32_t *planes,
                               hipStream_t stream);
 
-// Weight-streaming kernels for M <= 64 (skinny.hip): int8 rows (masked) or
-// the top b bit planes; int32 partial sums are added into `accbuf`
-// (M x N, zeroed by the launcher), then dequantised into d.y.
+// Weight-streaming kernels for M <= 64 (skinny.hip): one workgroup per 32
+// output channels reads the weight once from one of three layouts and
+// writes acc / y directly.
 constexpr int kSkinnyMaxM = 64;
-hipError_t launch_skinny(const LayerDesc &d, bool planes, int32_t *accbuf, hipStream_t stream);
+enum SkinnyWeights : int { SKINNY_ROWS = 0, SKINNY_PACKED = 1, SKINNY_PLANES = 2 };
+hipError_t launch_skinny(const LayerDesc &d, SkinnyWeights src, hipStream_t stream);
+// Grouped step: d_descs[l].tile_begin is layer l's first 32-channel block.
+hipError_t launch_skinny_grouped(const LayerDesc *d_descs, int L, int total_blocks, int max_m,
+                                 SkinnyWeights src, const uint8_t *d_table, int S, int stage,
+                                 hipStream_t stream);
 
 }  // namespace tasq

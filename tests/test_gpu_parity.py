@@ -275,30 +275,74 @@ SKINNY = [(1, 37, 1152), (5, 300, 1040), (16, 1152, 144), (32, 33, 16), (33, 257
 
 
 @pytest.mark.parametrize("case", range(len(SKINNY)))
-@pytest.mark.parametrize("planes", [False, True])
-def test_skinny_weight_streaming(case, planes):
-    """M <= 64 runs the weight-streaming kernels (int8 rows or the top b bit
-    planes), with and without an int32 output."""
+@pytest.mark.parametrize("source", ["rows", "packed", "planes"])
+def test_skinny_weight_streaming(case, source):
+    """M <= 64 runs the weight-streaming kernels (int8 rows, the packed
+    buffer, or the top b bit planes), with and without an int32 output."""
     M, N, K = SKINNY[case]
     X, W, sw, bias = inputs.random_case(300 + case, M, N, K)
     X[0, 0] = -128
     W[0, 0] = -128
     Xd, Wd, swd, bd = X.to(DEV), W.to(DEV), sw.to(DEV), bias.to(DEV)
-    P = T.pack_planes(Wd) if planes else None
-    kw = dict(variant=T.VARIANT_BITPLANE, planes=P) if planes else {}
+    if source == "planes":
+        kw = dict(variant=T.VARIANT_BITPLANE, planes=T.pack_planes(Wd))
+    elif source == "packed":
+        kw = dict(packed=T.pack_weights(Wd))
+    else:
+        kw = {}
+    Wuse = Wd if source == "rows" else None
     sx = f32(0.02)
     for b in range(1, 9):
         use_bias = bd if b % 3 == 0 else None
         ra, ry = oracle.masked_linear(X, W, sx, sw, b, bias if b % 3 == 0 else None)
-        acc, y = T.masked_linear(Xd, None if planes else Wd, sx, swd, b, use_bias, **kw)
+        acc, y = T.masked_linear(Xd, Wuse, sx, swd, b, use_bias, **kw)
         torch.cuda.synchronize()
         check_outputs(acc, y, ra, ry, sx, sw, bias if b % 3 == 0 else None,
-                      f"skinny {M}x{N}x{K} planes={planes} b={b}")
-        _, y2 = T.masked_linear(Xd, None if planes else Wd, sx, swd, b, use_bias,
-                                want_acc=False, **kw)
+                      f"skinny {M}x{N}x{K} {source} b={b}")
+        _, y2 = T.masked_linear(Xd, Wuse, sx, swd, b, use_bias, want_acc=False, **kw)
         torch.cuda.synchronize()
         check_outputs(None, y2, ra, ry, sx, sw, bias if b % 3 == 0 else None,
-                      f"skinny y-only {M}x{N}x{K} planes={planes} b={b}")
+                      f"skinny y-only {M}x{N}x{K} {source} b={b}")
+
+
+@pytest.mark.parametrize("source", ["rows", "packed", "planes"])
+def test_skinny_schedule_grouped(source):
+    """A schedule of skinny layers (M <= 64) runs one weight-streaming launch
+    per step; every step range matches the oracle's literal step loop."""
+    shapes = [(16, 1152, 1152), (16, 3456, 1152), (64, 130, 528), (33, 257, 1152),
+              (1, 37, 1152)]
+    host, dev = [], []
+    for i, (M, N, K) in enumerate(shapes):
+        X, W, sw, bias = inputs.random_case(700 + i, M, N, K)
+        host.append(dict(X=X, W=W, sw=sw, bias=bias if i == 2 else None))
+        d = dict(X=X.to(DEV), W=W.to(DEV), sw=sw.to(DEV),
+                 bias=bias.to(DEV) if i == 2 else None)
+        d["acc"] = torch.full((M, N), 12345, dtype=torch.int32, device=DEV)
+        d["y"] = torch.full((M, N), -7.0, dtype=torch.float32, device=DEV)
+        dev.append(d)
+    S, Tn = 4, 20
+    rng = np.random.default_rng(17)
+    table = torch.as_tensor(rng.integers(1, 9, size=(len(host), S)), dtype=torch.uint8)
+    sx = f32(0.02)
+    variant = T.VARIANT_AUTO
+    layers = []
+    for d in dev:
+        W = d["W"] if source == "rows" else None
+        planes = T.pack_planes(d["W"]) if source == "planes" else None
+        packed = T.pack_weights(d["W"]) if source == "packed" else None
+        d["keep"] = (planes, packed)
+        layers.append(T.make_layer(d["X"], W, sx, d["sw"], d["bias"], d["acc"], d["y"],
+                                   planes=planes, packed=packed))
+    if source == "planes":
+        variant = T.VARIANT_BITPLANE
+    ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
+    for (t0, t1) in [(0, 20), (0, 1), (6, 7), (14, 20)]:
+        T.run_schedule(layers, table, S, Tn, t0, t1, workspace=ws, variant=variant)
+        torch.cuda.synchronize()
+        ref = oracle.run_schedule(host, table.numpy(), S, Tn, t0, t1, sx)
+        for h, d, (ra, ry, b) in zip(host, dev, ref):
+            check_outputs(d["acc"], d["y"], ra, ry, sx, h["sw"], h.get("bias"),
+                          f"skinny schedule {source} [{t0},{t1}) b={b}")
 
 
 # ------------------------------------------------------------------- schedule
