@@ -15,7 +15,6 @@ kernel's roofline fraction, and the CPU oracle timed on a bounded sample.
 from __future__ import annotations
 
 import argparse
-import glob
 import hashlib
 import json
 import os
@@ -44,12 +43,23 @@ def traffic_file(kernel: str) -> str:
     return os.path.join(ROOT, "profiles", f"{kernel}_pixart28_traffic.json")
 
 
-def kernel_source_sha256() -> str:
-    """Hash of the HIP sources; ties recorded counter readings to the code."""
+# Sources the grouped kernel of each weight layout is built from: recorded
+# counter readings stay valid while none of these files changes.
+KERNEL_SOURCES = {
+    "k_masked_gemm_grouped": ["gemm_core.h", "tasq_internal.h", "tile_256x256_k128_w8_pf1.hip",
+                              "tasq_api.cpp"],
+    "k_gemm_packed_grouped": ["gemm_core.h", "gemm_packed.h", "tasq_internal.h",
+                              "ptile_256x256_k128_w8.hip", "tasq_api.cpp"],
+}
+
+
+def kernel_source_sha256(kernel: str = "k_masked_gemm_grouped") -> str:
+    """Hash of the HIP sources of one grouped kernel; ties recorded counter
+    readings to the code."""
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2608_03057_amd", "csrc", "*"))):
-        with open(f, "rb") as fh:
-            h.update(os.path.basename(f).encode())
+    for name in sorted(KERNEL_SOURCES[kernel]):
+        with open(os.path.join(ROOT, "paper_2608_03057_amd", "csrc", name), "rb") as fh:
+            h.update(name.encode())
             h.update(fh.read())
     return h.hexdigest()
 
@@ -63,7 +73,7 @@ def recorded_traffic(kernel: str):
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("source_sha256") != kernel_source_sha256():
+    if rec.get("source_sha256") != kernel_source_sha256(kernel):
         return None
     return rec.get("fetch_bytes_per_launch", 0) + rec.get("write_bytes_per_launch", 0)
 
@@ -213,13 +223,15 @@ def main():
                     help="weight buffer layout: packed (operand order, no LDS staging of "
                          "weights) or row-major [N][K] (weights staged through LDS)")
     ap.add_argument("--print-source-hash", action="store_true",
-                    help="print the HIP source hash that recorded counter readings refer to")
+                    help="print the HIP source hash that recorded counter readings refer to "
+                         "(of the grouped kernel of --weights)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy a 1 GiB buffer (reference for the FETCH_SIZE/WRITE_SIZE "
                          "counters) and exit")
     args = ap.parse_args()
     if args.print_source_hash:
-        print(kernel_source_sha256())
+        print(kernel_source_sha256("k_gemm_packed_grouped" if args.weights == "packed"
+                                   else "k_masked_gemm_grouped"))
         return
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
