@@ -183,6 +183,49 @@ def skinny_schedule(wl, table, keep, device, M=16, reps=3):
             "planes_tasq_vs_rows_b8": round(out["rows_b8"] / out["planes_tasq"], 3)}
 
 
+def skinny_sweep(device, steps=64):
+    """Single weight-streaming layers: M in {1, 16, 64} on the (K, N) pairs
+    of the PixArt and SANA blocks, the weight read as int8 rows, as the packed
+    buffer or as the top b planes.  Each figure is one tasq_run_schedule call
+    over `steps` steps of the one layer (per-layer launches issued back to
+    back from the library), timed with HIP events; returns one dict per
+    (M, K, N) with microseconds per launch and weight bytes read per
+    microsecond."""
+    rows = []
+    for l_cfg in (1, 2):
+        wl = inputs.workload(l_cfg)
+        for l, spec in enumerate(wl.layers):
+            W = inputs.w_full(wl, l).to(device)
+            sw = inputs.sw_full(wl, l).to(device)
+            P, Q = T.pack_weights(W), T.pack_planes(W)
+            for M in (1, 16, 64):
+                X = inputs.x_rows(wl, l, np.arange(M), device=device)
+                y = torch.empty((M, spec.N), dtype=torch.float32, device=device)
+                srcs = {"rows": (T.make_layer(X, W, wl.sx, sw, None, None, y), T.VARIANT_AUTO),
+                        "packed": (T.make_layer(X, None, wl.sx, sw, None, None, y, packed=P),
+                                   T.VARIANT_AUTO),
+                        "planes": (T.make_layer(X, None, wl.sx, sw, None, None, y, planes=Q),
+                                   T.VARIANT_BITPLANE)}
+                row = {"workload": wl.name, "layer": spec.name, "M": M, "K": spec.K, "N": spec.N}
+                for name, (layer, variant) in srcs.items():
+                    for bits in ((2, 4, 6, 8) if name == "planes" else (8,)):
+                        tab = torch.full((1, 1), bits, dtype=torch.uint8)
+                        T.run_schedule([layer], tab, 1, steps, 0, steps, variant=variant)
+                        torch.cuda.synchronize()
+                        a = torch.cuda.Event(enable_timing=True)
+                        b_ = torch.cuda.Event(enable_timing=True)
+                        a.record()
+                        T.run_schedule([layer], tab, 1, steps, 0, steps, variant=variant)
+                        b_.record()
+                        torch.cuda.synchronize()
+                        us = a.elapsed_time(b_) / steps * 1e3
+                        wbytes = spec.N * spec.K * (bits / 8.0 if name == "planes" else 1.0)
+                        row[f"{name}_b{bits}_us"] = round(us, 2)
+                        row[f"{name}_b{bits}_GBps"] = round(wbytes / us / 1e3, 1)
+                rows.append(row)
+    return rows
+
+
 def cpu_baseline(wl, table, budget_s=15.0):
     """The CPU oracle on a bounded sample: the first R rows of each of block
     0's four linears at its stage-0 b, R grown until the sample takes about
@@ -215,6 +258,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--tokens", type=int, default=None, help="override M (skinny sweeps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--skinny-sweep", action="store_true",
+                    help="only time single weight-streaming layers (M = 1, 16, 64) and print one "
+                         "JSON line per layer shape")
     ap.add_argument("--no-skinny", action="store_true",
                     help="skip the extra weight-streaming (M=16) schedule measurement")
     ap.add_argument("--per-layer", action="store_true",
@@ -240,6 +286,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": src.numel(), "reps": 3}), flush=True)
+        return
+    if args.skinny_sweep:
+        for row in skinny_sweep("cuda"):
+            print(json.dumps(row), flush=True)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the path shards by "

@@ -122,62 +122,43 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
             for (int mt = 0; mt < MT; ++mt)
                 bl.x[s][mt] = ld16(rX, offX[mt] + k0 + 32 * s);
     };
+    // Sub-step s of a block: weight fragment rebuilt (planes) or masked
+    // (int8) and consumed at once, so only one fragment is live.
     auto compute = [&](int kb, const Block &bl) {
         const uint32_t k0 = (uint32_t)kb * SK_KBLK;
-        v4i wq[4];
-        if constexpr (SRC == SRC_PLANES) {
-            wq[0] = wq[1] = wq[2] = wq[3] = zero4();
 #pragma unroll
-            for (int qq = 0; qq < 4; ++qq) {
-                if (2 * qq < b) {
-                    // even plane 2qq from the lower lanes, odd plane 2qq+1
-                    // (zero past b) from the upper lanes, on every lane
-                    const v4i mine = bl.w[qq];
-                    v4i ev, od;
-                    auto sx = __builtin_amdgcn_permlane32_swap(mine.x, mine.x, false, false);
-                    auto sy = __builtin_amdgcn_permlane32_swap(mine.y, mine.y, false, false);
-                    auto sz = __builtin_amdgcn_permlane32_swap(mine.z, mine.z, false, false);
-                    auto sw = __builtin_amdgcn_permlane32_swap(mine.w, mine.w, false, false);
-                    ev = v4i{(int)sx[0], (int)sy[0], (int)sz[0], (int)sw[0]};
-                    od = v4i{(int)sx[1], (int)sy[1], (int)sz[1], (int)sw[1]};
-                    const int up = 7 - 2 * qq;
-                    plane_half((uint32_t)ev.x, h, up, wq[0]);
-                    plane_half((uint32_t)ev.y, h, up, wq[1]);
-                    plane_half((uint32_t)ev.z, h, up, wq[2]);
-                    plane_half((uint32_t)ev.w, h, up, wq[3]);
-                    if (2 * qq + 1 < b) {
-                        plane_half((uint32_t)od.x, h, up - 1, wq[0]);
-                        plane_half((uint32_t)od.y, h, up - 1, wq[1]);
-                        plane_half((uint32_t)od.z, h, up - 1, wq[2]);
-                        plane_half((uint32_t)od.w, h, up - 1, wq[3]);
+        for (int s = 0; s < 4; ++s) {
+            v4i wq = zero4();
+            if constexpr (SRC == SRC_PLANES) {
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) {
+                    if (2 * qq < b) {
+                        // even plane 2qq from the lower lanes, odd plane
+                        // 2qq+1 (zero past b) from the upper lanes
+                        const v4i wv = bl.w[qq];
+                        const int words[4] = {wv.x, wv.y, wv.z, wv.w};
+                        const int mine = words[s];
+                        const auto sw2 = __builtin_amdgcn_permlane32_swap(mine, mine, false, false);
+                        plane_half((uint32_t)sw2[0], h, 7 - 2 * qq, wq);
+                        if (2 * qq + 1 < b)
+                            plane_half((uint32_t)sw2[1], h, 6 - 2 * qq, wq);
                     }
                 }
+            } else {
+                wq = bl.w[s];
+                wq.x &= msk;
+                wq.y &= msk;
+                wq.z &= msk;
+                wq.w &= msk;
+                // Columns past K: zero the weights (row-major loads there may
+                // hold the next row; packed and plane layouts are zero).
+                if (SRC == SRC_ROWS && k0 + 32 * s + 16 * h >= (uint32_t)d.K)
+                    wq = zero4();
             }
-        } else {
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                v4i v = bl.w[s];
-                v.x &= msk;
-                v.y &= msk;
-                v.z &= msk;
-                v.w &= msk;
-                wq[s] = v;
-            }
-        }
-        // Columns past K: zero the weights (row-major loads there may hold
-        // the next row; packed and plane layouts are zero already).
-        if (SRC == SRC_ROWS && k0 + SK_KBLK > (uint32_t)d.K) {
-#pragma unroll
-            for (int s = 0; s < 4; ++s)
-                if (k0 + 32 * s + 16 * h >= (uint32_t)d.K)
-                    wq[s] = zero4();
-        }
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
-                acc[mt] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wq[s], bl.x[s][mt], acc[mt], 0, 0,
-                                                                0);
+                acc[mt] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wq, bl.x[s][mt], acc[mt], 0, 0, 0);
+        }
     };
 
     for (int kb = wave; kb < nkb; kb += SK_WAVES) {
