@@ -230,7 +230,6 @@ LayerDesc make_desc(const tasq_layer &L, const tasq_opts *o)
     d.H = L.H;
     d.Wd = L.Wd;
     d.C = L.C;
-    d.ksplit = 1;
     return d;
 }
 

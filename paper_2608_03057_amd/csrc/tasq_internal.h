@@ -27,9 +27,6 @@ struct LayerDesc {
     int32_t bits;           // effective precision b (single calls)
     int32_t tiles_m, tiles_n;
     int32_t tile_begin;     // first tile of this layer in a grouped launch
-    int32_t ksplit;         // number of K slices (1 = no split)
-    int32_t kslice;         // bytes of K per slice (multiple of the K tile)
-    int32_t ws_tile_offset; // first partial-sum tile slot in the workspace
 };
 
 // Per-byte keep mask for b effective bits, replicated over the 4 bytes of a

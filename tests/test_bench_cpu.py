@@ -1,0 +1,41 @@
+"""Host-side pieces of bench.py that need no GPU: the algorithmic op and byte
+counts that the roofline object is computed from, and the CLI contract."""
+import subprocess
+import sys
+
+import pytest
+
+from conftest import ROOT
+from paper_2608_03057_amd import inputs
+
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_schedule_ops_and_bytes_closed_form():
+    """Config 4 per denoising step: 28 blocks of QKV 1152->3456, out
+    1152->1152, MLP 1152->4608 and 4608->1152 at M = 8192."""
+    wl = inputs.workload(4)
+    M = 8192
+    shapes = [(1152, 3456), (1152, 1152), (1152, 4608), (4608, 1152)]
+    ops = 28 * sum(2 * M * N * K for K, N in shapes)
+    nbytes = 28 * sum(M * K + N * K + 4 * M * N for K, N in shapes)
+    assert bench.gemm_ops(wl) == ops == 7305739370496
+    assert bench.gemm_bytes(wl) == nbytes == 11808276480
+    # both rooflines of a step at the datasheet peaks (ms)
+    assert abs(ops / 5.0e15 * 1e3 - 1.4611) < 1e-3
+    assert abs(nbytes / 8.0e12 * 1e3 - 1.4760) < 1e-3
+
+
+def test_multi_gpu_request_exits_with_message():
+    r = subprocess.run([sys.executable, "bench.py", "--gpus", "2"], cwd=ROOT,
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+def test_kernel_source_hash_is_stable_and_per_kernel():
+    a = bench.kernel_source_sha256("k_masked_gemm_grouped")
+    b = bench.kernel_source_sha256("k_gemm_packed_grouped")
+    assert a == bench.kernel_source_sha256("k_masked_gemm_grouped")
+    assert len(a) == 64 and a != b
