@@ -31,7 +31,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared",
-                               "-Wall", "-Werror", _SRC, "-o", tmp])
+                               "-Wall", "-Werror", _SRC, "-o", tmp, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -60,6 +60,12 @@ def lib():
                                              ctypes.c_int, p, p, i64, p, p]
         L.oracle_pack_planes.argtypes = [p, i64, i64, p]
         L.oracle_pack_weights.argtypes = [p, i64, i64, p]
+        L.oracle_act_quant.argtypes = [p, i64, p, p, p]
+        L.oracle_weight_colsums.argtypes = [p, i64, i64, p]
+        L.oracle_masked_linear_asym.argtypes = [p, p, ctypes.c_double, ctypes.c_double, p, p,
+                                                i64, i64, i64, ctypes.c_int, p, p]
+        L.oracle_masked_linear_asym_entries.argtypes = [p, p, ctypes.c_double, ctypes.c_double,
+                                                        p, p, i64, ctypes.c_int, p, p, i64, p, p]
         _lib = L
     return _lib
 
@@ -216,6 +222,75 @@ def pack_weights(W) -> np.ndarray:
     out = np.empty(32 * ((N + 31) // 32) * 128 * ((K + 127) // 128), np.int8)
     lib().oracle_pack_weights(_ptr(W), N, K, _ptr(out))
     return out
+
+
+def act_quant(x):
+    """(alpha, z, Q uint8 of x's shape): the per-tensor asymmetric 8-bit
+    activation quantizer of App. A.1.2, decided in IEEE single precision."""
+    x = _np(x, np.float32)
+    q = np.empty(x.shape, np.uint8)
+    a = np.empty(1, np.float32)
+    z = np.empty(1, np.float32)
+    rc = lib().oracle_act_quant(_ptr(x), x.size, _ptr(a), _ptr(z), _ptr(q))
+    if rc != OK:
+        raise ValueError(f"oracle_act_quant rc={rc}")
+    return float(a[0]), float(z[0]), q
+
+
+def weight_colsums(W) -> np.ndarray:
+    """int32 [8 x N]: row b-1 holds sum_k W_b[n][k] for every output channel."""
+    W = _np(W, np.int8)
+    N = W.shape[0]
+    K = W.size // N if N else 0
+    out = np.empty((8, N), np.int32)
+    rc = lib().oracle_weight_colsums(_ptr(W), N, K, _ptr(out))
+    if rc != OK:
+        raise ValueError(f"oracle_weight_colsums rc={rc}")
+    return out
+
+
+def masked_linear_asym(Q, W, alpha: float, z: float, sw, b: int, bias=None):
+    """(acc int32 [M x N] of the signed codes Q - 128, y fp64 [M x N] of
+    sum_k alpha (Q - z) sw W_b) for asymmetric activation codes Q."""
+    Q = _np(Q, np.uint8)
+    W = _np(W, np.int8)
+    sw = _np(sw, np.float32)
+    bias = None if bias is None else _np(bias, np.float32)
+    M, K = Q.shape
+    N, K2 = W.shape
+    assert K == K2 and sw.shape == (N,)
+    acc = np.empty((M, N), np.int32)
+    y = np.empty((M, N), np.float64)
+    rc = lib().oracle_masked_linear_asym(_ptr(Q), _ptr(W), float(alpha), float(z), _ptr(sw),
+                                         _ptr(bias), M, N, K, b, _ptr(acc), _ptr(y))
+    if rc == EOVERFLOW:
+        raise OverflowError("accumulator outside int32")
+    if rc != OK:
+        raise ValueError(f"oracle_masked_linear_asym rc={rc}")
+    return acc, y
+
+
+def masked_linear_asym_entries(Q, W, alpha, z, sw, b, rows, cols, bias=None):
+    """The (rows[i], cols[i]) outputs of masked_linear_asym, one dot product
+    each (rows index Q, cols index W, sw and bias)."""
+    Q = _np(Q, np.uint8)
+    W = _np(W, np.int8)
+    sw = _np(sw, np.float32)
+    bias = None if bias is None else _np(bias, np.float32)
+    rows = _np(rows, np.int64)
+    cols = _np(cols, np.int64)
+    K = Q.shape[1]
+    assert W.shape[1] == K and rows.shape == cols.shape
+    acc = np.empty(rows.size, np.int32)
+    y = np.empty(rows.size, np.float64)
+    rc = lib().oracle_masked_linear_asym_entries(_ptr(Q), _ptr(W), float(alpha), float(z),
+                                                 _ptr(sw), _ptr(bias), K, b, _ptr(rows),
+                                                 _ptr(cols), rows.size, _ptr(acc), _ptr(y))
+    if rc == EOVERFLOW:
+        raise OverflowError("accumulator outside int32")
+    if rc != OK:
+        raise ValueError(f"oracle_masked_linear_asym_entries rc={rc}")
+    return acc, y
 
 
 def run_schedule(layers, table, S: int, T: int, t_begin: int, t_end: int, sx: float):

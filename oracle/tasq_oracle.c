@@ -34,6 +34,7 @@
  */
 #include <stdint.h>
 #include <stddef.h>
+#include <math.h>
 #include <stdlib.h>
 #ifdef _OPENMP
 #include <omp.h>
@@ -293,4 +294,143 @@ int oracle_pack_weights(const int8_t *W, int64_t N, int64_t K, int8_t *packed)
             packed[((nb * KS + ks) * 64 + l) * 16 + k % 16] = W[n * K + k];
         }
     return ORACLE_OK;
+}
+
+/*
+ * Activation quantizer of App. A.1.2 (Eqs. act_quant, act_scale), n = 8,
+ * per tensor:
+ *   alpha = (max(x) - min(x)) / (2^n - 1),   z = -min(x) / alpha,
+ *   Q = clamp(round_to_nearest(x / alpha + z), 0, 2^n - 1).
+ * z is kept real, as printed.  Each operation is one IEEE single-precision
+ * operation in this order (the subtraction, the divisions, then the
+ * addition), rounding ties to even: the precision the kernel decides the
+ * codes in.  When max == min the scale is undefined; alpha = 1 and z = -min
+ * are taken, so every code is 0 and dequantises to min exactly.
+ * x must be finite.
+ */
+int oracle_act_quant(const float *x, int64_t n, float *alpha_out, float *z_out, uint8_t *q)
+{
+    if (n <= 0)
+        return ORACLE_EDIM;
+    float mn = x[0], mx = x[0];
+    for (int64_t i = 1; i < n; ++i) {
+        if (x[i] < mn)
+            mn = x[i];
+        if (x[i] > mx)
+            mx = x[i];
+    }
+    float alpha, z;
+    if (mx == mn) {
+        alpha = 1.0f;
+        z = -mn;
+    } else {
+        float range = mx - mn;
+        alpha = range / 255.0f;
+        z = -mn / alpha;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        float t = x[i] / alpha;
+        t = t + z;
+        float r = rintf(t);
+        if (r < 0.0f)
+            r = 0.0f;
+        if (r > 255.0f)
+            r = 255.0f;
+        q[i] = (uint8_t)r;
+    }
+    *alpha_out = alpha;
+    *z_out = z;
+    return ORACLE_OK;
+}
+
+/*
+ * Per-output-channel sums of the masked weight at every precision, for the
+ * zero-point term of an asymmetric activation:
+ *   colsum[b-1][n] = sum_k 2^(8-b) floor(W[n][k] / 2^(8-b)),  b = 1..8.
+ */
+int oracle_weight_colsums(const int8_t *W, int64_t N, int64_t K, int32_t *colsum)
+{
+    if (N < 0 || K < 0)
+        return ORACLE_EDIM;
+    for (int b = 1; b <= 8; ++b)
+        for (int64_t n = 0; n < N; ++n) {
+            int64_t s = 0;
+            for (int64_t k = 0; k < K; ++k)
+                s += masked_value(W[n * K + k], b);
+            colsum[(b - 1) * N + n] = (int32_t)s;
+        }
+    return ORACLE_OK;
+}
+
+/*
+ * The layer on asymmetric activation codes Q (App. A.1.2: x_hat =
+ * alpha (Q - z)) and the masked weight (per-channel scale sw):
+ *   y[m][n]   = sum_k alpha (Q[m][k] - z) * sw[n] W_b[n][k]  (+ bias[n])   fp64,
+ *               the definition, summed in ascending k;
+ *   acc[m][n] = sum_k (Q[m][k] - 128) W_b[n][k]                          int32,
+ *               the integer product of the signed codes Q - 128 that the
+ *               int8 matrix instruction consumes.
+ * Q uint8 [M][K]; other arguments as oracle_masked_linear.
+ */
+int oracle_masked_linear_asym(const uint8_t *Q, const int8_t *W, double alpha, double z,
+                              const float *sw, const float *bias, int64_t M, int64_t N,
+                              int64_t K, int b, int32_t *acc, double *y)
+{
+    if (b < 1 || b > 8)
+        return ORACLE_EBITS;
+    if (M < 0 || N < 0 || K < 0)
+        return ORACLE_EDIM;
+    int overflow = 0;
+#pragma omp parallel for schedule(static) reduction(| : overflow)
+    for (int64_t m = 0; m < M; ++m) {
+        for (int64_t n = 0; n < N; ++n) {
+            int64_t s = 0;
+            double v = 0.0;
+            for (int64_t k = 0; k < K; ++k) {
+                int64_t w = masked_value(W[n * K + k], b);
+                s += ((int64_t)Q[m * K + k] - 128) * w;
+                v += alpha * ((double)Q[m * K + k] - z) * (double)sw[n] * (double)w;
+            }
+            if (s >= ((int64_t)1 << 31) || s < -((int64_t)1 << 31))
+                overflow = 1;
+            if (acc)
+                acc[m * N + n] = (int32_t)s;
+            if (y) {
+                if (bias)
+                    v += (double)bias[n];
+                y[m * N + n] = v;
+            }
+        }
+    }
+    return overflow ? ORACLE_EOVERFLOW : ORACLE_OK;
+}
+
+/* Entries (rows[i], cols[i]) of oracle_masked_linear_asym, one dot product
+ * each (rows index Q, cols index W, sw and bias). */
+int oracle_masked_linear_asym_entries(const uint8_t *Q, const int8_t *W, double alpha, double z,
+                                      const float *sw, const float *bias, int64_t K, int b,
+                                      const int64_t *rows, const int64_t *cols, int64_t count,
+                                      int32_t *acc, double *y)
+{
+    if (b < 1 || b > 8)
+        return ORACLE_EBITS;
+    int overflow = 0;
+#pragma omp parallel for schedule(static) reduction(| : overflow)
+    for (int64_t i = 0; i < count; ++i) {
+        const int64_t m = rows[i], n = cols[i];
+        int64_t s = 0;
+        double v = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+            int64_t w = masked_value(W[n * K + k], b);
+            s += ((int64_t)Q[m * K + k] - 128) * w;
+            v += alpha * ((double)Q[m * K + k] - z) * (double)sw[n] * (double)w;
+        }
+        if (s >= ((int64_t)1 << 31) || s < -((int64_t)1 << 31))
+            overflow = 1;
+        acc[i] = (int32_t)s;
+        if (bias)
+            v += (double)bias[n];
+        y[i] = v;
+    }
+    return overflow ? ORACLE_EOVERFLOW : ORACLE_OK;
 }

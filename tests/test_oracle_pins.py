@@ -427,3 +427,113 @@ def test_generator_published_value_and_ranges():
     # counter-based: sampled rows equal the same rows of the full tensor
     rows = [0, 17, 255]
     np.testing.assert_array_equal(inputs.x_rows(wl, 0, rows).numpy(), X[rows].numpy())
+
+
+# ------------------------------------------- activation quantizer (App. A.1.2)
+
+def test_act_quant_exact_grid_and_ties():
+    """Ranges whose scale is exactly 1 or 2: codes are x - min (scaled), and
+    halves round to even (round to nearest, ties to even)."""
+    a, z, q = oracle.act_quant(np.array([0.0, 2.5, 3.5, 100.0, 255.0], np.float32))
+    assert (a, z) == (1.0, 0.0)
+    assert q.tolist() == [0, 2, 4, 100, 255]
+    a, z, q = oracle.act_quant(np.array([-128.0, -0.5, 0.5, 1.5, 127.0], np.float32))
+    assert (a, z) == (1.0, 128.0)
+    assert q.tolist() == [0, 128, 128, 130, 255]
+    a, z, q = oracle.act_quant(np.array([0.0, 1.0, 3.0, 5.0, 510.0], np.float32))
+    assert (a, z) == (2.0, 0.0)
+    assert q.tolist() == [0, 0, 2, 2, 255]
+
+
+def test_act_quant_constant_tensor():
+    a, z, q = oracle.act_quant(np.full(7, -3.25, np.float32))
+    assert a == 1.0 and z == 3.25 and not q.any()
+    assert a * (0 - z) == -3.25          # dequantises to the constant exactly
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_act_quant_properties(seed):
+    """min -> 0, max -> 255, codes monotone in x, and the dequantised value
+    alpha (Q - z) within alpha/2 of x (plus single-precision slack, which
+    matters when the range is narrow against its offset and z is large)."""
+    rng = np.random.default_rng(seed)
+    x = (rng.standard_normal(5000) * (10.0 ** rng.uniform(-3, 3)) + rng.uniform(-5, 5))
+    x = x.astype(np.float32)
+    a, z, q = oracle.act_quant(x)
+    assert q[np.argmin(x)] == 0 and q[np.argmax(x)] == 255
+    order = np.argsort(x, kind="stable")
+    assert np.all(np.diff(q[order].astype(np.int64)) >= 0)
+    span = float(x.max()) - float(x.min())
+    assert abs(a - span / 255) <= 1e-6 * span / 255
+    xhat = a * (q.astype(np.float64) - z)
+    # single-precision slack of x/alpha + z (and of alpha, z themselves), in
+    # units of alpha: a few ulps of the largest magnitude involved
+    slack = 8 * 2.0 ** -24 * (np.abs(x.astype(np.float64)) / a + abs(z) + 255)
+    assert np.all(np.abs(xhat - x.astype(np.float64)) <= a * (0.5 + slack))
+
+
+def test_weight_colsums():
+    """b = 8 equals the plain row sum; lower b equals the row sum of the
+    two's-complement AND mask (a different route from the oracle's floor);
+    and the dropped-bit identity colsum_8 - colsum_b = sum of the low bits."""
+    rng = np.random.default_rng(3)
+    W = rng.integers(-128, 128, (37, 300)).astype(np.int8)
+    cs = oracle.weight_colsums(W)
+    w64 = W.astype(np.int64)
+    assert np.array_equal(cs[7], w64.sum(axis=1))
+    for b in range(1, 9):
+        k = 8 - b
+        anded = w64 & ~((1 << k) - 1)
+        assert np.array_equal(cs[b - 1], anded.sum(axis=1)), b
+        low = (W.view(np.uint8).astype(np.int64) & ((1 << k) - 1)).sum(axis=1)
+        assert np.array_equal(cs[7] - cs[b - 1], low), b
+
+
+@pytest.mark.parametrize("b", [8, 5, 2])
+def test_asym_linear_factored_form_and_signed_codes(b):
+    """sum_k alpha (Q - z) sw W_b (the oracle's definition) equals the
+    factored zero-point form alpha sw (Q W_b^T - z colsum_b) computed with
+    numpy int64 matmul, and acc is the int64 product of the signed codes."""
+    rng = np.random.default_rng(b)
+    Q = rng.integers(0, 256, (9, 200)).astype(np.uint8)
+    W = rng.integers(-128, 128, (11, 200)).astype(np.int8)
+    sw = rng.uniform(1e-3, 1e-2, 11).astype(np.float32)
+    bias = rng.uniform(-1, 1, 11).astype(np.float32)
+    alpha, z = 0.0173, 121.37
+    acc, y = oracle.masked_linear_asym(Q, W, alpha, z, sw, b, bias)
+    k = 8 - b
+    Wb = W.astype(np.int64) & ~((1 << k) - 1)
+    colsum = Wb.sum(axis=1)
+    accQ = Q.astype(np.int64) @ Wb.T
+    assert np.array_equal(acc, (Q.astype(np.int64) - 128) @ Wb.T)
+    assert np.array_equal(accQ, acc + 128 * colsum)
+    ref = alpha * sw.astype(np.float64) * (accQ - z * colsum) + bias
+    assert np.allclose(y, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_asym_linear_reduces_to_symmetric():
+    """With z = 128 and alpha = sx the asymmetric layer is the symmetric one
+    on the codes Q - 128."""
+    rng = np.random.default_rng(11)
+    Q = rng.integers(0, 256, (6, 96)).astype(np.uint8)
+    W = rng.integers(-128, 128, (5, 96)).astype(np.int8)
+    sw = rng.uniform(1e-3, 1e-2, 5).astype(np.float32)
+    for b in (8, 3):
+        acc_a, y_a = oracle.masked_linear_asym(Q, W, 0.02, 128.0, sw, b)
+        acc_s, y_s = oracle.masked_linear((Q.astype(np.int16) - 128).astype(np.int8), W, 0.02,
+                                          sw, b)
+        assert np.array_equal(acc_a, acc_s)
+        assert np.allclose(y_a, y_s, rtol=1e-12, atol=1e-15)
+
+
+def test_asym_entries_match_full():
+    rng = np.random.default_rng(12)
+    Q = rng.integers(0, 256, (13, 150)).astype(np.uint8)
+    W = rng.integers(-128, 128, (17, 150)).astype(np.int8)
+    sw = rng.uniform(1e-3, 1e-2, 17).astype(np.float32)
+    acc, y = oracle.masked_linear_asym(Q, W, 0.05, 100.25, sw, 4)
+    rows = rng.integers(0, 13, 40)
+    cols = rng.integers(0, 17, 40)
+    ae, ye = oracle.masked_linear_asym_entries(Q, W, 0.05, 100.25, sw, 4, rows, cols)
+    assert np.array_equal(ae, acc[rows, cols])
+    assert np.allclose(ye, y[rows, cols], rtol=1e-13, atol=0)
