@@ -226,6 +226,69 @@ def skinny_sweep(device, steps=64):
     return rows
 
 
+def act_schedule(wl, table, keep, ws, device, reps=2):
+    """The asymmetric-activation form of the same schedule: each layer's input
+    arrives as fp32 (seeded normal draws with a few large channels), is
+    quantized per tensor on the GPU, and the grouped launch dequantises with
+    the zero-point term.  Per denoising step: the 112 quantizer calls, then
+    one grouped launch.  Returns milliseconds per denoising step for the
+    quantizer, the grouped launch and both, and the quantizer's HBM roofline
+    (algorithmic bytes: 4 read + 1 written per element)."""
+    xs, codes, layers, hold = [], [], [], []
+    params = torch.empty((len(wl.layers), T.TASQ_ACT_PARAMS_FLOATS), dtype=torch.float32,
+                         device=device)
+    gen = torch.Generator(device=device)
+    for l, spec in enumerate(wl.layers):
+        X, W, sw, y = keep[l]
+        if W.dim() == 1:           # packed-only run: no row-major copy for the channel sums
+            return None
+        gen.manual_seed(wl.seed * 1000 + l)
+        x = torch.randn((spec.M, spec.K), generator=gen, device=device, dtype=torch.float32)
+        x[:, ::61] *= 24.0
+        q = torch.empty((spec.M, spec.K), dtype=torch.int8, device=device)
+        cs = T.weight_colsums(W)
+        xs.append(x)
+        codes.append(q)
+        hold.append(cs)
+        layers.append(T.make_layer(q, W, 0.0, sw, None, None, y, act=params[l], colsums=cs))
+    torch.cuda.synchronize()
+
+    def quantize_all():
+        for l in range(len(xs)):
+            T.quantize_activations(xs[l], out=codes[l], params=params[l])
+
+    quantize_all()
+    T.run_schedule(layers, table, wl.S, wl.T, 0, 1, workspace=ws)
+    torch.cuda.synchronize()
+    ev = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
+    q_ms, g_ms = [], []
+    a0, a1 = ev(), ev()
+    a0.record()
+    for _ in range(reps):
+        for t in range(wl.T):
+            e0, e1, e2 = ev(), ev(), ev()
+            e0.record()
+            quantize_all()
+            e1.record()
+            T.run_schedule(layers, table, wl.S, wl.T, t, t + 1, workspace=ws)
+            e2.record()
+            q_ms.append((e0, e1))
+            g_ms.append((e1, e2))
+    a1.record()
+    torch.cuda.synchronize()
+    qm = float(np.mean([a.elapsed_time(b) for a, b in q_ms]))
+    gm = float(np.mean([a.elapsed_time(b) for a, b in g_ms]))
+    elems = sum(float(s.M * s.K) for s in wl.layers)
+    ach = 5.0 * elems / (qm * 1e-3) / 1e9
+    return {"ms_per_denoising_step": round(a0.elapsed_time(a1) / reps / wl.T, 4),
+            "quantize_ms": round(qm, 4), "grouped_launch_ms": round(gm, 4),
+            "quantizer_roofline": {"bound": "hbm", "achieved": round(ach, 1),
+                                   "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                   "frac": round(ach / PEAK_HBM_GBS, 4),
+                                   "algorithmic_bytes": 5.0 * elems,
+                                   "kernels": "k_act_range, k_act_quantize per layer"}}
+
+
 def cpu_baseline(wl, table, budget_s=15.0):
     """The CPU oracle on a bounded sample: the first R rows of each of block
     0's four linears at its stage-0 b, R grown until the sample takes about
@@ -263,6 +326,8 @@ def main():
                          "JSON line per layer shape")
     ap.add_argument("--no-skinny", action="store_true",
                     help="skip the extra weight-streaming (M=16) schedule measurement")
+    ap.add_argument("--no-act", action="store_true",
+                    help="skip the extra asymmetric-activation (fp32 input) measurement")
     ap.add_argument("--per-layer", action="store_true",
                     help="launch each layer separately instead of one grouped launch per step")
     ap.add_argument("--weights", choices=("packed", "rowmajor"), default="rowmajor",
@@ -341,6 +406,11 @@ def main():
         log("timing the weight-streaming schedule at M=16")
         skinny = skinny_schedule(wl, table, keep, dev)
 
+    act = None
+    if not args.no_act and not args.per_layer:
+        log("timing the asymmetric-activation schedule")
+        act = act_schedule(wl, table, keep, ws, dev)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle sample")
@@ -361,6 +431,7 @@ def main():
         "mean_bits": round(float(table.float().mean()), 3),
         "roofline": roof,
         "skinny_schedule": skinny,
+        "asymmetric_activations": act,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

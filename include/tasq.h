@@ -61,6 +61,10 @@ enum {
 /* |X| <= 128 and |W_b| <= 128, so |acc| <= 16384 * K < 2^31 iff K <= 131071. */
 #define TASQ_MAX_K 131071
 
+/* Length in floats of the parameter buffer of an asymmetric activation
+ * tensor (tasq_quantize_activations): [0] alpha, [1] z, the rest scratch. */
+#define TASQ_ACT_PARAMS_FLOATS 1028
+
 /* Kernel variants (tasq_opts.variant). */
 enum {
     TASQ_VARIANT_AUTO = 0,      /* library picks per shape                         */
@@ -92,6 +96,19 @@ enum {
  *                   Contents need no initialisation and are left
  *                   unspecified.
  *   workspace_bytes its size in bytes.
+ *   act_params      device float[TASQ_ACT_PARAMS_FLOATS] written by
+ *                   tasq_quantize_activations, or NULL.  When given, X holds
+ *                   asymmetric activation codes (stored as Q - 128), sx is
+ *                   ignored, and (only [0] and [1] are read)
+ *                   y = act_params[0] * sw[n] *
+ *                       (acc + (128 - act_params[1]) * colsums[b-1][n]) + bias[n]
+ *                   (App. A.1.2 dequantisation x_hat = alpha (Q - z)).
+ *   colsums         device int32 [8][N] from tasq_weight_colsums; required
+ *                   with act_params.  act_params and colsums must be 4-byte
+ *                   aligned (TASQ_ERR_ALIGN).  Linear layers only: a conv's
+ *                   zero padding is not the code of a real zero, so
+ *                   act_params on a TASQ_KIND_CONV3X3 layer or in
+ *                   tasq_masked_conv3x3 is TASQ_ERR_LAYOUT.
  */
 typedef struct tasq_opts {
     int32_t variant;
@@ -100,6 +117,8 @@ typedef struct tasq_opts {
     void *workspace;
     size_t workspace_bytes;
     const int8_t *W_packed;
+    const float *act_params;
+    const int32_t *colsums;
 } tasq_opts;
 
 /*
@@ -184,6 +203,36 @@ int tasq_pack_weights(const int8_t *W, int N, int K, int8_t *packed_out, void *s
 size_t tasq_packed_weight_bytes(int N, int K);
 
 /*
+ * Asymmetric 8-bit activation quantizer, per tensor (App. A.1.2, Eqs.
+ * act_quant and act_scale), the step before the masked GEMM:
+ *   alpha = (max(x) - min(x)) / 255,  z = -min(x) / alpha  (z kept real),
+ *   Q = clamp(round_to_nearest(x / alpha + z), 0, 255),  X_out = Q - 128.
+ * The codes are decided in IEEE single precision: correctly rounded
+ * division, then addition, rounding ties to even.  When max == min,
+ * alpha = 1 and z = -min (every code 0, dequantising to min exactly).
+ *   x           fp32 [M][K] device, finite values, 4-byte aligned (16-byte
+ *               alignment, with X_out 4-byte aligned, takes vector loads).
+ *   X_out       int8 [M][K] device: the signed codes Q - 128, ready as the X
+ *               of tasq_masked_linear with opts->act_params.
+ *   act_params  device float[TASQ_ACT_PARAMS_FLOATS]: [0] = alpha, [1] = z
+ *               on completion (stream-ordered); [2..] scratch.  Nothing needs
+ *               clearing beforehand; two calls that share one buffer must be
+ *               ordered on one stream.
+ * M*K == 0 enqueues nothing.  Errors: TASQ_ERR_NULL, _DIM, _ALIGN (x or
+ * act_params not 4-byte aligned), _HIP.
+ */
+int tasq_quantize_activations(const float *x, int M, int K, int8_t *X_out, float *act_params,
+                              void *stream);
+
+/*
+ * Channel sums of the masked weight at every precision, for the zero-point
+ * term of asymmetric activations: colsums_out[b-1][n] = sum_k W_b[n][k],
+ * b = 1..8 (int32 [8][N] device).  A one-time pass over the stored buffer,
+ * like the packers.  Errors: TASQ_ERR_NULL, _DIM, _OVERFLOW, _HIP.
+ */
+int tasq_weight_colsums(const int8_t *W, int N, int K, int32_t *colsums_out, void *stream);
+
+/*
  * Stage of denoising step t (Sec. 3.2: contiguous stages sharing one mask;
  * Sec. 4.1: 20 steps in four stages, or one stage per step when S = T;
  * App. D.1: stage 0 is the noisiest, first part of the trajectory):
@@ -209,6 +258,8 @@ typedef struct tasq_layer {
     int32_t *acc;
     float *y;
     const int8_t *W_packed;     /* packed copy of W or NULL (tasq_pack_weights) */
+    const float *act_params;    /* asymmetric activations (see tasq_opts) or NULL */
+    const int32_t *colsums;     /* [8][N] channel sums, required with act_params */
 } tasq_layer;
 
 /*

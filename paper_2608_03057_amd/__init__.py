@@ -8,10 +8,10 @@ from __future__ import annotations
 
 from .api import (  # noqa: F401
     masked_linear, masked_conv3x3, pack_planes, planes_bytes, pack_weights, packed_weight_bytes,
-    stage_of_step, run_schedule, schedule_workspace_bytes, workspace_bytes, make_layer,
-    status_string,
+    quantize_activations, weight_colsums, stage_of_step, run_schedule, schedule_workspace_bytes,
+    workspace_bytes, make_layer, status_string,
 )
 from ._lib import (  # noqa: F401
     TasqError, VARIANT_AUTO, VARIANT_MASKED_I8, VARIANT_BITPLANE, VARIANT_PACKED, KIND_LINEAR,
-    KIND_CONV3X3,
+    KIND_CONV3X3, TASQ_ACT_PARAMS_FLOATS,
 )

@@ -25,6 +25,7 @@ TASQ_ERR_HIP = -8
 TASQ_ERR_KIND = -9
 TASQ_ERR_ALIGN = -10
 TASQ_MAX_K = 131071
+TASQ_ACT_PARAMS_FLOATS = 1028
 
 VARIANT_AUTO = 0
 VARIANT_MASKED_I8 = 1
@@ -37,7 +38,8 @@ KIND_CONV3X3 = 1
 # Every exported symbol the header declares.
 EXPORTS = (
     "tasq_masked_linear", "tasq_masked_conv3x3", "tasq_pack_planes", "tasq_planes_bytes",
-    "tasq_pack_weights", "tasq_packed_weight_bytes", "tasq_stage_of_step", "tasq_run_schedule",
+    "tasq_pack_weights", "tasq_packed_weight_bytes", "tasq_quantize_activations",
+    "tasq_weight_colsums", "tasq_stage_of_step", "tasq_run_schedule",
     "tasq_workspace_bytes", "tasq_schedule_workspace_bytes", "tasq_status_string",
 )
 
@@ -45,7 +47,8 @@ EXPORTS = (
 class Opts(ctypes.Structure):
     _fields_ = [("variant", ctypes.c_int32), ("split_k", ctypes.c_int32),
                 ("W_planes", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
-                ("workspace_bytes", ctypes.c_size_t), ("W_packed", ctypes.c_void_p)]
+                ("workspace_bytes", ctypes.c_size_t), ("W_packed", ctypes.c_void_p),
+                ("act_params", ctypes.c_void_p), ("colsums", ctypes.c_void_p)]
 
 
 class Layer(ctypes.Structure):
@@ -54,7 +57,8 @@ class Layer(ctypes.Structure):
                 ("C", ctypes.c_int32), ("sx", ctypes.c_float),
                 ("X", ctypes.c_void_p), ("W", ctypes.c_void_p), ("W_planes", ctypes.c_void_p),
                 ("sw", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("acc", ctypes.c_void_p),
-                ("y", ctypes.c_void_p), ("W_packed", ctypes.c_void_p)]
+                ("y", ctypes.c_void_p), ("W_packed", ctypes.c_void_p),
+                ("act_params", ctypes.c_void_p), ("colsums", ctypes.c_void_p)]
 
 
 class TasqError(RuntimeError):
@@ -87,6 +91,10 @@ def lib() -> ctypes.CDLL:
         L.tasq_pack_weights.restype = i32
         L.tasq_packed_weight_bytes.argtypes = [i32, i32]
         L.tasq_packed_weight_bytes.restype = ctypes.c_size_t
+        L.tasq_quantize_activations.argtypes = [vp, i32, i32, vp, vp, vp]
+        L.tasq_quantize_activations.restype = i32
+        L.tasq_weight_colsums.argtypes = [vp, i32, i32, vp, vp]
+        L.tasq_weight_colsums.restype = i32
         L.tasq_stage_of_step.argtypes = [i32, i32, i32]
         L.tasq_stage_of_step.restype = i32
         L.tasq_run_schedule.argtypes = [ctypes.POINTER(Layer), i32, vp, i32, i32, i32, i32,

@@ -37,7 +37,7 @@ def _need(t: Optional[torch.Tensor], dtype, shape, name):
         raise ValueError(f"{name} must be contiguous")
 
 
-def _opts(variant, planes, workspace, split_k, packed=None) -> Opts:
+def _opts(variant, planes, workspace, split_k, packed=None, act=None, colsums=None) -> Opts:
     o = Opts()
     o.variant = variant
     o.split_k = split_k
@@ -45,6 +45,8 @@ def _opts(variant, planes, workspace, split_k, packed=None) -> Opts:
     o.workspace = _ptr(workspace)
     o.workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     o.W_packed = _ptr(packed)
+    o.act_params = _ptr(act)
+    o.colsums = _ptr(colsums)
     return o
 
 
@@ -98,13 +100,47 @@ def pack_weights(W: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.T
     return out
 
 
+def quantize_activations(x: torch.Tensor, out: Optional[torch.Tensor] = None,
+                         params: Optional[torch.Tensor] = None):
+    """(int8 codes Q - 128 of x's shape, fp32 [TASQ_ACT_PARAMS_FLOATS] params
+    with alpha at 0 and z at 1) of fp32 activations x, per tensor (App. A.1.2)."""
+    M = x.shape[0] if x.dim() else 1
+    K = x.numel() // M if M else 0
+    _need(x, torch.float32, tuple(x.shape), "x")
+    if out is None:
+        out = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+    if params is None:
+        params = torch.empty(_lib.TASQ_ACT_PARAMS_FLOATS, dtype=torch.float32, device=x.device)
+    _need(out, torch.int8, tuple(x.shape), "out")
+    _need(params, torch.float32, (_lib.TASQ_ACT_PARAMS_FLOATS,), "params")
+    check(_lib.lib().tasq_quantize_activations(_ptr(x), M, K, _ptr(out), _ptr(params), _stream()),
+          "tasq_quantize_activations")
+    return out, params
+
+
+def weight_colsums(W: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """int32 [8, N]: row b-1 holds sum_k W_b[n][k] of int8 W [N, ...]."""
+    N = W.shape[0]
+    K = W.numel() // N if N else 0
+    _need(W, torch.int8, tuple(W.shape), "W")
+    if out is None:
+        out = torch.empty((8, N), dtype=torch.int32, device=W.device)
+    _need(out, torch.int32, (8, N), "colsums")
+    check(_lib.lib().tasq_weight_colsums(_ptr(W), N, K, _ptr(out), _stream()),
+          "tasq_weight_colsums")
+    return out
+
+
 def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: torch.Tensor,
                   b: int, bias: Optional[torch.Tensor] = None, *, want_acc: bool = True,
                   want_y: bool = True, acc: Optional[torch.Tensor] = None,
                   y: Optional[torch.Tensor] = None, variant: int = _lib.VARIANT_AUTO,
                   planes: Optional[torch.Tensor] = None, packed: Optional[torch.Tensor] = None,
-                  workspace: Optional[torch.Tensor] = None, split_k: int = 0):
-    """(acc int32 [M, N] or None, y fp32 [M, N] or None) of the masked layer."""
+                  workspace: Optional[torch.Tensor] = None, split_k: int = 0,
+                  act: Optional[torch.Tensor] = None, colsums: Optional[torch.Tensor] = None):
+    """(acc int32 [M, N] or None, y fp32 [M, N] or None) of the masked layer.
+    With ``act`` (params of quantize_activations) and ``colsums`` X holds
+    asymmetric activation codes and sx is ignored."""
     M, K = X.shape
     N = sw.shape[0]
     _need(X, torch.int8, (M, K), "X")
@@ -122,7 +158,8 @@ def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: tor
         wb = workspace_bytes(M, N, K)
         if wb:
             workspace = torch.empty(wb, dtype=torch.uint8, device=X.device)
-    o = _opts(variant, planes, workspace, split_k, packed)
+    _need(colsums, torch.int32, (8, N), "colsums")
+    o = _opts(variant, planes, workspace, split_k, packed, act, colsums)
     rc = _lib.lib().tasq_masked_linear(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias), M, N,
                                        K, int(b), _ptr(acc), _ptr(y), ctypes.byref(o), _stream())
     check(rc, "tasq_masked_linear")
@@ -156,7 +193,7 @@ def masked_conv3x3(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: to
 
 
 def make_layer(X, W, sx, sw, bias=None, acc=None, y=None, planes=None, kind=None,
-               packed=None) -> Layer:
+               packed=None, act=None, colsums=None) -> Layer:
     """A tasq_layer for run_schedule; tensors must stay alive while in use."""
     L = Layer()
     if kind is None:
@@ -173,6 +210,8 @@ def make_layer(X, W, sx, sw, bias=None, acc=None, y=None, planes=None, kind=None
     L.X, L.W, L.W_planes = _ptr(X), _ptr(W), _ptr(planes)
     L.sw, L.bias, L.acc, L.y = _ptr(sw), _ptr(bias), _ptr(acc), _ptr(y)
     L.W_packed = _ptr(packed)
+    L.act_params = _ptr(act)
+    L.colsums = _ptr(colsums)
     return L
 
 

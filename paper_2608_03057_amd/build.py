@@ -29,6 +29,7 @@ SOURCES = [
     "ptile_64x64_k128_w4.hip",
     "pack_planes.hip",
     "pack_weights.hip",
+    "act_quant.hip",
     "skinny.hip",
     "tiles.cpp",
     "tasq_api.cpp",

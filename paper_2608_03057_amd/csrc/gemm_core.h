@@ -442,13 +442,15 @@ __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int
 }
 
 // Writes a finished tile: int32 accumulators and/or the fp32 dequantised
-// value y = float(acc) * (sx * sw[n]) + bias[n].  Register v of a 32x32
+// value y = float(acc) * (sx * sw[n]) + bias[n].  With asymmetric
+// activations (d.act) the zero point enters through the channel sum of W_b:
+// y = (float(acc) + (128 - z) * colsum_b[n]) * (alpha * sw[n]) + bias[n].  Register v of a 32x32
 // accumulator in lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32, so
 // each store instruction covers two 128-byte row segments.  Rows past M
 // fall past the buffer end and are dropped; columns past N carry kOOB.
 template <class C>
 __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
-                                         const v16i (&acc)[C::FM][C::FN])
+                                         const v16i (&acc)[C::FM][C::FN], int bits)
 {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -463,9 +465,14 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
     for (int j = 0; j < C::FN; ++j) {
         const int n = n0 + wn * C::WTN + j * 32 + (lane & 31);
         const bool nok = n < d.N;
-        float scale = 0.f, bias = 0.f;
+        float scale = 0.f, bias = 0.f, corr = 0.f;
         if (nok) {
-            scale = d.sx * d.sw[n];
+            if (d.act) {
+                scale = d.act[0] * d.sw[n];
+                corr = (128.0f - d.act[1]) * (float)d.colsums[(bits - 1) * d.N + n];
+            } else {
+                scale = d.sx * d.sw[n];
+            }
             if (d.bias)
                 bias = d.bias[n];
         }
@@ -484,7 +491,8 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
 #pragma unroll
                 for (int v = 0; v < 16; ++v)
                     st32(ry, base + (uint32_t)(i * 32 + 8 * (v >> 2) + (v & 3)) * rowb,
-                         __builtin_bit_cast(uint32_t, (float)acc[i][j][v] * scale + bias));
+                         __builtin_bit_cast(uint32_t,
+                                            ((float)acc[i][j][v] + corr) * scale + bias));
         }
     }
 }
@@ -531,7 +539,7 @@ __global__ void __launch_bounds__(C::NT, C::OCC) k_masked_gemm(LayerDesc d)
     v16i acc[C::FM][C::FN];
     mainloop<C, ALIGNED, KIND, PLANES>(d, keep_mask_dword(d.bits), m0, n0, 0, d.K, acc, smA,
                                        smB);
-    epilogue<C>(d, m0, n0, acc);
+    epilogue<C>(d, m0, n0, acc, d.bits);
 }
 
 // Grouped launch over every layer of one denoising step: workgroup t finds
@@ -556,7 +564,8 @@ k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
             hi = mid - 1;
     }
     const LayerDesc d = descs[lo];
-    const uint32_t wmask = keep_mask_dword(table[lo * S + stage]);
+    const int bits = table[lo * S + stage];
+    const uint32_t wmask = keep_mask_dword(bits);
     int tm, tn;
     tile_coords(t - d.tile_begin, d.tiles_m, d.tiles_n, tm, tn);
     const int m0 = tm * C::BM, n0 = tn * C::BN;
@@ -565,7 +574,7 @@ k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
         mainloop<C, true, KIND_CONV3X3>(d, wmask, m0, n0, 0, d.K, acc, smA, smB);
     else
         mainloop<C, true, KIND_LINEAR>(d, wmask, m0, n0, 0, d.K, acc, smA, smB);
-    epilogue<C>(d, m0, n0, acc);
+    epilogue<C>(d, m0, n0, acc, bits);
 }
 
 // ---------------------------------------------------------------- launchers

@@ -193,7 +193,7 @@ __global__ void __launch_bounds__(C::NT, C::OCC) k_gemm_packed(LayerDesc d)
     const int m0 = tm * C::BM, n0 = tn * C::BN;
     v16i acc[C::FM][C::FN];
     mainloop_packed<C, ALIGNED, KIND>(d, keep_mask_dword(d.bits), m0, n0, acc, sm);
-    epilogue<C>(d, m0, n0, acc);
+    epilogue<C>(d, m0, n0, acc, d.bits);
 }
 
 // Grouped step over every layer (see k_masked_gemm_grouped); every layer
@@ -214,7 +214,8 @@ k_gemm_packed_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
             hi = mid - 1;
     }
     const LayerDesc d = descs[lo];
-    const uint32_t wmask = keep_mask_dword(table[lo * S + stage]);
+    const int bits = table[lo * S + stage];
+    const uint32_t wmask = keep_mask_dword(bits);
     int tm, tn;
     tile_coords(t - d.tile_begin, d.tiles_m, d.tiles_n, tm, tn);
     const int m0 = tm * C::BM, n0 = tn * C::BN;
@@ -223,7 +224,7 @@ k_gemm_packed_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
         mainloop_packed<C, true, KIND_CONV3X3>(d, wmask, m0, n0, acc, sm);
     else
         mainloop_packed<C, true, KIND_LINEAR>(d, wmask, m0, n0, acc, sm);
-    epilogue<C>(d, m0, n0, acc);
+    epilogue<C>(d, m0, n0, acc, bits);
 }
 
 template <class C>

@@ -182,9 +182,14 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
     const int nn = n0 + col;
     const int vv = 4 * (col >> 3) + (col & 3);
     const int lh = 32 * ((col & 7) >> 2);
-    float scale = 0.f, bias = 0.f;
+    float scale = 0.f, bias = 0.f, corr = 0.f;
     if (nn < d.N && d.y) {
-        scale = d.sx * d.sw[nn];
+        if (d.act) {
+            scale = d.act[0] * d.sw[nn];
+            corr = (128.0f - d.act[1]) * (float)d.colsums[(b - 1) * d.N + nn];
+        } else {
+            scale = d.sx * d.sw[nn];
+        }
         if (d.bias)
             bias = d.bias[nn];
     }
@@ -203,7 +208,7 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
         if (d.acc)
             d.acc[o] = sum;
         if (d.y)
-            d.y[o] = (float)sum * scale + bias;
+            d.y[o] = ((float)sum + corr) * scale + bias;
     }
 }
 

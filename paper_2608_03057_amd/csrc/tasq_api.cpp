@@ -218,6 +218,8 @@ LayerDesc make_desc(const tasq_layer &L, const tasq_opts *o)
     d.W = L.W;
     d.P = L.W_planes ? L.W_planes : (o ? o->W_planes : nullptr);
     d.Wp = L.W_packed ? L.W_packed : (o ? o->W_packed : nullptr);
+    d.act = L.act_params ? L.act_params : (o ? o->act_params : nullptr);
+    d.colsums = L.colsums ? L.colsums : (o ? o->colsums : nullptr);
     d.sw = L.sw;
     d.bias = L.bias;
     d.acc = L.acc;
@@ -251,6 +253,16 @@ int validate_layer(const tasq_layer &L, const tasq_opts *o)
         local.W_planes = L.W_planes;
     if (L.W_packed)
         local.W_packed = L.W_packed;
+    if (L.act_params)
+        local.act_params = L.act_params;
+    if (L.colsums)
+        local.colsums = L.colsums;
+    // Asymmetric activations need the channel sums for the zero point.
+    if (has_out && L.y && local.act_params && !local.colsums)
+        return TASQ_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(local.act_params) & 3) ||
+        (reinterpret_cast<uintptr_t>(local.colsums) & 3))
+        return TASQ_ERR_ALIGN;
     const bool needs_w = L.N > 0 && L.K > 0;
     if (int rc = check_variant(&local, needs_w ? L.W : reinterpret_cast<const int8_t *>(1)))
         return rc;
@@ -261,6 +273,10 @@ int validate_layer(const tasq_layer &L, const tasq_opts *o)
             return TASQ_ERR_DIM;
         if (use_bitplane(&local))
             return TASQ_ERR_LAYOUT;     // the bit-plane kernel covers linear layers
+        // A padded tap holds code 0, which dequantises to alpha (128 - z), not
+        // to zero: asymmetric codes would need a per-pixel zero-point term.
+        if (local.act_params)
+            return TASQ_ERR_LAYOUT;
     }
     if (int rc = check_dims(L.M, L.N, L.K))
         return rc;
@@ -406,6 +422,38 @@ int tasq_pack_weights(const int8_t *W, int N, int K, int8_t *packed_out, void *s
     if (!aligned16(packed_out))
         return TASQ_ERR_ALIGN;
     hipError_t e = tasq::launch_pack_weights(W, N, K, packed_out, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}
+
+int tasq_quantize_activations(const float *x, int M, int K, int8_t *X_out, float *act_params,
+                              void *stream)
+{
+    if (M < 0 || K < 0)
+        return TASQ_ERR_DIM;
+    const long long n = (long long)M * K;
+    if (n == 0)
+        return TASQ_OK;
+    if (!x || !X_out || !act_params)
+        return TASQ_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(x) & 3) || (reinterpret_cast<uintptr_t>(act_params) & 3))
+        return TASQ_ERR_ALIGN;
+    hipError_t e = tasq::launch_quantize_activations(x, n, X_out, act_params,
+                                                     static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}
+
+int tasq_weight_colsums(const int8_t *W, int N, int K, int32_t *colsums_out, void *stream)
+{
+    if (N < 0 || K < 0)
+        return TASQ_ERR_DIM;
+    if (K > TASQ_MAX_K)
+        return TASQ_ERR_OVERFLOW;
+    if (N == 0)
+        return TASQ_OK;
+    if (!colsums_out || (K > 0 && !W))
+        return TASQ_ERR_NULL;
+    hipError_t e = tasq::launch_weight_colsums(W, N, K, colsums_out,
+                                               static_cast<hipStream_t>(stream));
     return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
 }
 

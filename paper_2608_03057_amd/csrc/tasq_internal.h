@@ -18,6 +18,8 @@ struct LayerDesc {
     const int8_t *Wp;       // packed weights (MFMA operand order) or null
     const float *sw;        // [N]
     const float *bias;      // [N] or null
+    const float *act;       // asymmetric activation params [4] (alpha at 2, z at 3) or null
+    const int32_t *colsums; // [8][N] channel sums of W_b (with act)
     int32_t *acc;           // [M][N] or null
     float *y;               // [M][N] or null
     float sx;
@@ -95,6 +97,16 @@ inline unsigned long long packed_weight_bytes_host(long long N, long long K)
     return (unsigned long long)((N + 31) / 32) * 32ULL * (unsigned long long)((K + 127) / 128) *
            128ULL;
 }
+
+// Asymmetric 8-bit activation quantizer and the channel sums of the masked
+// weight (act_quant.hip).  params: device float[kActHeader + 2 * kActPartials],
+// [0] alpha, [1] z on completion, [kActHeader..] partial ranges.
+constexpr int kActHeader = 4;
+constexpr int kActPartials = 512;
+hipError_t launch_quantize_activations(const float *x, long long n, int8_t *q, float *params,
+                                       hipStream_t stream);
+hipError_t launch_weight_colsums(const int8_t *W, int N, int K, int32_t *colsums,
+                                 hipStream_t stream);
 
 // Packs an [N][K] int8 weight into the MFMA operand order (gemm_packed.h).
 hipError_t launch_pack_weights(const int8_t *W, int N, int K, int8_t *packed,

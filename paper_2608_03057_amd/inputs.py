@@ -82,6 +82,15 @@ def normal_int8(seed, tid, idx, sigma=32.0):
     return torch.clamp(torch.round(sigma * z), -127, 127).to(torch.int8)
 
 
+def normal_f32(seed, tid, idx):
+    """fp32 N(0, 1) draws by Box-Muller in fp64 on the CPU (as normal_int8)."""
+    idx = idx.to(torch.int64).cpu()
+    u1 = _lsr(raw(seed, tid, 2 * idx), 11).to(torch.float64) * (2.0 ** -53)
+    u2 = _lsr(raw(seed, tid, 2 * idx + 1), 11).to(torch.float64) * (2.0 ** -53)
+    z = torch.sqrt(-2.0 * torch.log1p(-u1)) * torch.cos(2.0 * math.pi * u2)
+    return z.to(torch.float32)
+
+
 def _grid(rows: Sequence[int] | torch.Tensor, ncols: int, device) -> torch.Tensor:
     r = torch.as_tensor(rows, dtype=torch.int64, device=device).reshape(-1, 1)
     c = torch.arange(ncols, dtype=torch.int64, device=device).reshape(1, -1)
@@ -243,6 +252,25 @@ def b_table(wl: Workload) -> torch.Tensor:
     idx = torch.arange(L * wl.S, dtype=torch.int64)
     return uniform_int(wl.seed, TID_TABLE, idx, wl.b_lo, wl.b_hi,
                        dtype=torch.uint8).reshape(L, wl.S)
+
+
+def activations_f32(seed: int, rows, K: int, shape: str = "outlier") -> torch.Tensor:
+    """Rows of a real-valued activation matrix, fp32 [len(rows) x K] on the
+    CPU, for the activation quantizer.
+
+    "outlier": N(0, 1) with every 61st channel scaled by 24 (the few large
+    channels of transformer activations).  "skewed": 0.5 z^2 - 0.17 with
+    z ~ N(0, 1), a one-sided tail above a small negative floor, like the
+    input of an MLP's second projection, the case an asymmetric range fits
+    better than a symmetric one."""
+    z = _draw_rows(rows, K, "cpu", torch.float32, lambda idx: normal_f32(seed, 5, idx))
+    if shape == "outlier":
+        gain = torch.ones(K, dtype=torch.float32)
+        gain[::61] = 24.0
+        return z * gain
+    if shape == "skewed":
+        return 0.5 * z * z - 0.17
+    raise ValueError(shape)
 
 
 def random_case(seed: int, M: int, N: int, K: int, device="cpu"):

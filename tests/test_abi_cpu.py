@@ -91,6 +91,9 @@ def opts(**kw):
     (dict(opts=opts(W_packed=FAKE + 4)), _lib.TASQ_ERR_ALIGN),
     (dict(W=None, opts=opts(variant=_lib.VARIANT_MASKED_I8, W_packed=FAKE)), _lib.TASQ_ERR_NULL),
     (dict(W=None, b=0, opts=opts(W_packed=FAKE)), _lib.TASQ_ERR_BITS),
+    (dict(opts=opts(act_params=FAKE)), _lib.TASQ_ERR_NULL),
+    (dict(opts=opts(act_params=FAKE + 2, colsums=FAKE)), _lib.TASQ_ERR_ALIGN),
+    (dict(opts=opts(act_params=FAKE, colsums=FAKE + 1)), _lib.TASQ_ERR_ALIGN),
 ])
 def test_masked_linear_rejects(kw, code):
     assert lin(**kw) == code
@@ -127,6 +130,38 @@ def test_pack_weights_rejects():
     assert L.tasq_pack_weights(FAKE, 4, 131072, FAKE, None) == _lib.TASQ_ERR_OVERFLOW
     assert L.tasq_pack_weights(FAKE, 4, 4, FAKE + 8, None) == _lib.TASQ_ERR_ALIGN
     assert L.tasq_pack_weights(FAKE, 0, 4, FAKE, None) == _lib.TASQ_OK
+
+
+def test_quantize_activations_rejects():
+    q = L.tasq_quantize_activations
+    assert q(None, 4, 4, FAKE, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert q(FAKE, 4, 4, None, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert q(FAKE, 4, 4, FAKE, None, None) == _lib.TASQ_ERR_NULL
+    assert q(FAKE, -1, 4, FAKE, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert q(FAKE, 4, -2, FAKE, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert q(FAKE + 2, 4, 4, FAKE, FAKE, None) == _lib.TASQ_ERR_ALIGN
+    assert q(FAKE, 4, 4, FAKE, FAKE + 1, None) == _lib.TASQ_ERR_ALIGN
+    assert q(None, 0, 4, None, None, None) == _lib.TASQ_OK          # empty: nothing enqueued
+
+
+def test_weight_colsums_rejects():
+    c = L.tasq_weight_colsums
+    assert c(None, 4, 4, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert c(FAKE, 4, 4, None, None) == _lib.TASQ_ERR_NULL
+    assert c(FAKE, -1, 4, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert c(FAKE, 4, 131072, FAKE, None) == _lib.TASQ_ERR_OVERFLOW
+    assert c(FAKE, 0, 4, None, None) == _lib.TASQ_OK
+
+
+def test_schedule_asymmetric_layer_needs_colsums():
+    tbl = [8, 7, 6, 5, 4, 3, 2, 1]
+    conv = layer(kind=_lib.KIND_CONV3X3, H=2, Wd=2, C=16, M=4, K=144, act_params=FAKE,
+                 colsums=FAKE)
+    assert sched([layer(), conv], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_LAYOUT
+    assert sched([layer(), layer(act_params=FAKE)], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_NULL
+    assert sched([layer(act_params=FAKE, colsums=FAKE + 2), layer()], tbl, 4, 20, 0, 1) \
+        == _lib.TASQ_ERR_ALIGN
+    assert sched([layer(act_params=FAKE, colsums=FAKE)] * 2, tbl, 4, 20, 0, 0) == _lib.TASQ_OK
 
 
 def test_conv_rejects():
