@@ -8,8 +8,9 @@ it; the two meet only in the seeded inputs the tests hand to both.
 The arithmetic lives in ``tasq_oracle.c`` (plain C, int64 accumulation, fp64
 dequantisation).  This module loads it with ctypes and adds the schedule
 (Sec. 3.2 contiguous stages, Sec. 4.1 step/stage counts), which only loops
-over the C definition.  ``brute.py`` is a second, pure-Python route for tiny
-shapes.
+over the C definition, and the 16-bit low-rank branch in numpy fp64 (its
+products of bfloat16 values are exact in fp64).  ``brute.py`` is a second,
+pure-Python route for tiny shapes.
 """
 from __future__ import annotations
 
@@ -291,6 +292,58 @@ def masked_linear_asym_entries(Q, W, alpha, z, sw, b, rows, cols, bias=None):
     if rc != OK:
         raise ValueError(f"oracle_masked_linear_asym_entries rc={rc}")
     return acc, y
+
+
+# --------------------------------------------------- 16-bit low-rank branch
+#
+# The SVDQuant-initialised models carry a frozen 16-bit low-rank branch beside
+# the quantized layer (Sec. 4.1 setup: rank 16 at the 6-bit setting, rank 32
+# at 4 bits; App. training details).  Its output is added to the dequantised
+# GEMM:  y = dequant(X W_b^T) + (x~ D^T) U^T,  with D [r x K] the down and
+# U [N x r] the up projection held in bfloat16, and x~ the activation rounded
+# to bfloat16 (the branch runs in 16 bits).  The oracle evaluates the branch
+# in fp64 from those 16-bit values; every product of two bfloat16 values is
+# exact in fp64.
+
+
+def bf16_value(bits) -> np.ndarray:
+    """fp64 values of bfloat16 bit patterns (the upper half of an IEEE
+    single with the same bits)."""
+    bits = np.asarray(bits).astype(np.uint16).astype(np.uint32)
+    return (bits << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def bf16_round(x) -> np.ndarray:
+    """bfloat16 bit patterns of fp32 values, rounded to nearest with ties to
+    even: the nearest multiple of the bfloat16 spacing at x's binade (2^(e-8)
+    for x = m 2^e, 1/2 <= |m| < 1, and 2^-133 below the normal range)."""
+    x = np.asarray(x, dtype=np.float32).astype(np.float64)
+    _, e = np.frexp(x)
+    spacing = np.ldexp(1.0, np.maximum(e - 8, -133))
+    v = np.rint(x / spacing) * spacing                      # exact in fp64
+    return (v.astype(np.float32).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def lowrank(x, down, up):
+    """(T fp64 [M x r], lr fp64 [M x N]) of the low-rank branch:
+    T = x~ D^T, lr = T U^T, with x~ = bf16_round(x) and D, U given as
+    bfloat16 bit patterns ([r x K] and [N x r])."""
+    xt = bf16_value(bf16_round(x))
+    D = bf16_value(down)
+    U = bf16_value(up)
+    assert xt.shape[1] == D.shape[1] and U.shape[1] == D.shape[0]
+    T = xt @ D.T
+    return T, T @ U.T
+
+
+def lowrank_entries(x_rows, down, up, rows, cols) -> np.ndarray:
+    """lr[rows[i], cols[i]] where ``rows`` index x_rows (the branch of a few
+    activation rows, e.g. sampled from a full-size layer)."""
+    T, _ = lowrank(x_rows, down, up[:1])
+    U = bf16_value(up)
+    rows = np.asarray(rows, np.int64)
+    cols = np.asarray(cols, np.int64)
+    return np.einsum("ij,ij->i", T[rows], U[cols])
 
 
 def run_schedule(layers, table, S: int, T: int, t_begin: int, t_end: int, sx: float):

@@ -273,6 +273,20 @@ def activations_f32(seed: int, rows, K: int, shape: str = "outlier") -> torch.Te
     raise ValueError(shape)
 
 
+def bf16_bits(seed: int, tid: int, shape, emin: int = -9, emax: int = -3) -> torch.Tensor:
+    """int16 [shape] bit patterns of random bfloat16 values: a uniform sign,
+    a uniform exponent in [emin, emax] and a uniform 7-bit mantissa, i.e.
+    +-(1 + m/128) 2^e (the weights of a low-rank branch).  Drawn as integer
+    fields, so no rounding is involved."""
+    n = math.prod(shape)
+    idx = torch.arange(n, dtype=torch.int64)
+    sign = uniform_int(seed, tid, 3 * idx, 0, 1, dtype=torch.int32)
+    expo = uniform_int(seed, tid, 3 * idx + 1, emin + 127, emax + 127, dtype=torch.int32)
+    mant = uniform_int(seed, tid, 3 * idx + 2, 0, 127, dtype=torch.int32)
+    bits = (sign << 15) | (expo << 7) | mant
+    return torch.where(bits >= 32768, bits - 65536, bits).to(torch.int16).reshape(shape)
+
+
 def random_case(seed: int, M: int, N: int, K: int, device="cpu"):
     """Free-form fuzz case: X, W uniform over the whole int8 range [-128, 127]
     (so both operands reach -128), sw uniform on [1e-3, 1e-2)."""

@@ -537,3 +537,104 @@ def test_asym_entries_match_full():
     ae, ye = oracle.masked_linear_asym_entries(Q, W, 0.05, 100.25, sw, 4, rows, cols)
     assert np.array_equal(ae, acc[rows, cols])
     assert np.allclose(ye, y[rows, cols], rtol=1e-13, atol=0)
+
+
+# ---------------------------------------------------- 16-bit low-rank branch
+
+BF16_WORKED = [
+    (1.0, 0x3F80),                      # exact
+    (1 + 2 ** -8, 0x3F80),              # halfway between 1 and 1 + 2^-7: even mantissa
+    (1 + 3 * 2 ** -8, 0x3F82),          # halfway between 1 + 2^-7 and 1 + 2^-6: even
+    (1 + 2 ** -8 + 2 ** -20, 0x3F81),   # just above halfway
+    (-2.5, 0xC020),
+    (0.0, 0x0000),
+    (-0.0, 0x8000),
+    (3.140625, 0x4049),                 # 1.5703125 * 2, mantissa 73/128
+    (65504.0, 0x4780),                  # largest fp16 value rounds up to 2^16
+    (2.0 ** -133, 0x0001),              # smallest bfloat16 subnormal
+    (1.5 * 2.0 ** -133, 0x0002),        # subnormal tie: even
+]
+
+
+@pytest.mark.parametrize("x,bits", BF16_WORKED)
+def test_bf16_round_worked_values(x, bits):
+    assert int(oracle.bf16_round(np.array([x], np.float32))[0]) == bits
+
+
+def test_bf16_value_decodes():
+    got = oracle.bf16_value([0x3F80, 0xC020, 0x0001, 0x4049, 0x3F82, 0x8000])
+    assert got.tolist() == [1.0, -2.5, 2.0 ** -133, 3.140625, 1 + 2 ** -6, 0.0]
+
+
+def test_bf16_round_matches_torch_rne():
+    """The frexp/rint route against torch's float32 -> bfloat16 conversion
+    (round to nearest even), on random values, exact ties and subnormals."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(7)
+    base = rng.standard_normal(4000).astype(np.float32) * np.float32(37.0)
+    finite = rng.integers(0, 0x7F00, 2000) | (rng.integers(0, 2, 2000) << 15)
+    ties = (oracle.bf16_value(finite).astype(np.float32).view(np.uint32)
+            | np.uint32(0x8000)).view(np.float32)
+    tiny = (rng.integers(1, 1 << 23, 500).astype(np.uint32)).view(np.float32)
+    x = np.concatenate([base, ties, tiny, -tiny])
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().astype(np.uint16)
+    assert np.array_equal(oracle.bf16_round(x), ref)
+
+
+def _lowrank_case(seed, M, K, r, N):
+    x = inputs.activations_f32(seed, np.arange(M), K, "outlier").numpy()
+    D = inputs.bf16_bits(seed, 1, (r, K)).numpy()
+    U = inputs.bf16_bits(seed, 2, (N, r)).numpy()
+    return x, D, U
+
+
+def test_lowrank_exact_rational_tiny():
+    """T and lr against exact rational arithmetic on the bfloat16 values."""
+    x, D, U = _lowrank_case(31, 3, 7, 2, 4)
+    T, lr = oracle.lowrank(x, D, U)
+    xt = [[Fraction(float(v)) for v in row] for row in oracle.bf16_value(oracle.bf16_round(x))]
+    Df = [[Fraction(float(v)) for v in row] for row in oracle.bf16_value(D)]
+    Uf = [[Fraction(float(v)) for v in row] for row in oracle.bf16_value(U)]
+    for m in range(3):
+        Tm = [sum(xt[m][k] * Df[j][k] for k in range(7)) for j in range(2)]
+        for j in range(2):
+            assert abs(Fraction(T[m, j]) - Tm[j]) <= abs(Tm[j]) * Fraction(1, 2 ** 50)
+        for n in range(4):
+            e = sum(Tm[j] * Uf[n][j] for j in range(2))
+            mag = sum(abs(Tm[j] * Uf[n][j]) for j in range(2))
+            assert abs(Fraction(lr[m, n]) - e) <= mag * Fraction(1, 2 ** 48)
+
+
+def test_lowrank_merged_weight():
+    """(x~ D^T) U^T equals x~ (U D)^T: the branch is one rank-r linear map."""
+    x, D, U = _lowrank_case(32, 9, 300, 16, 40)
+    _, lr = oracle.lowrank(x, D, U)
+    xt = oracle.bf16_value(oracle.bf16_round(x))
+    merged = xt @ (oracle.bf16_value(U) @ oracle.bf16_value(D)).T
+    mag = np.abs(xt) @ (np.abs(oracle.bf16_value(U)) @ np.abs(oracle.bf16_value(D))).T
+    assert np.all(np.abs(lr - merged) <= 1e-13 * mag)
+
+
+def test_lowrank_one_hot():
+    """D = e_j e_k^T, U = 2 e_n e_j^T: the branch copies 2 * bf16(x[:, k]) to
+    column n and zero elsewhere."""
+    x, _, _ = _lowrank_case(33, 5, 12, 4, 6)
+    D = np.zeros((4, 12), np.uint16)
+    U = np.zeros((6, 4), np.uint16)
+    D[2, 7] = 0x3F80                     # 1.0
+    U[3, 2] = 0x4000                     # 2.0
+    T, lr = oracle.lowrank(x, D, U)
+    xt = oracle.bf16_value(oracle.bf16_round(x))
+    expect = np.zeros((5, 6))
+    expect[:, 3] = 2.0 * xt[:, 7]
+    assert np.array_equal(lr, expect)
+    assert np.array_equal(T[:, 2], xt[:, 7]) and not T[:, [0, 1, 3]].any()
+
+
+def test_lowrank_entries_match_full():
+    x, D, U = _lowrank_case(34, 11, 130, 32, 21)
+    _, lr = oracle.lowrank(x, D, U)
+    rng = np.random.default_rng(3)
+    rows, cols = rng.integers(0, 11, 50), rng.integers(0, 21, 50)
+    e = oracle.lowrank_entries(x, D, U, rows, cols)
+    assert np.allclose(e, lr[rows, cols], rtol=1e-13, atol=0)
