@@ -226,15 +226,19 @@ def skinny_sweep(device, steps=64):
     return rows
 
 
-def act_schedule(wl, table, keep, ws, device, reps=2):
+def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
     """The asymmetric-activation form of the same schedule: each layer's input
     arrives as fp32 (seeded normal draws with a few large channels), is
     quantized per tensor on the GPU, and the grouped launch dequantises with
     the zero-point term.  Per denoising step: the 112 quantizer calls, then
-    one grouped launch.  Returns milliseconds per denoising step for the
+    one grouped launch.  Timed twice: without and with a rank-`rank` 16-bit
+    low-rank branch on every layer (SVDQuant-initialised models), where the
+    quantizer also writes the down projection and the grouped launch adds the
+    up projection.  Returns milliseconds per denoising step for the
     quantizer, the grouped launch and both, and the quantizer's HBM roofline
-    (algorithmic bytes: 4 read + 1 written per element)."""
-    xs, codes, layers, hold = [], [], [], []
+    (algorithmic bytes: 4 read + 1 written per element, plus 4 per element of
+    the projection with the branch)."""
+    xs, codes, Ts, plain, lowrank, hold = [], [], [], [], [], []
     params = torch.empty((len(wl.layers), T.TASQ_ACT_PARAMS_FLOATS), dtype=torch.float32,
                          device=device)
     gen = torch.Generator(device=device)
@@ -245,48 +249,64 @@ def act_schedule(wl, table, keep, ws, device, reps=2):
         gen.manual_seed(wl.seed * 1000 + l)
         x = torch.randn((spec.M, spec.K), generator=gen, device=device, dtype=torch.float32)
         x[:, ::61] *= 24.0
+        down = (0.05 * torch.randn((rank, spec.K), generator=gen, device=device)).to(
+            torch.bfloat16)
+        up = (0.05 * torch.randn((spec.N, rank), generator=gen, device=device)).to(
+            torch.bfloat16)
         q = torch.empty((spec.M, spec.K), dtype=torch.int8, device=device)
+        Tl = torch.empty((spec.M, rank), dtype=torch.float32, device=device)
         cs = T.weight_colsums(W)
-        xs.append(x)
+        xs.append((x, down))
         codes.append(q)
-        hold.append(cs)
-        layers.append(T.make_layer(q, W, 0.0, sw, None, None, y, act=params[l], colsums=cs))
+        Ts.append(Tl)
+        hold += [cs, up]
+        plain.append(T.make_layer(q, W, 0.0, sw, None, None, y, act=params[l], colsums=cs))
+        lowrank.append(T.make_layer(q, W, 0.0, sw, None, None, y, act=params[l], colsums=cs,
+                                    lowrank=(Tl, up)))
     torch.cuda.synchronize()
 
-    def quantize_all():
-        for l in range(len(xs)):
-            T.quantize_activations(xs[l], out=codes[l], params=params[l])
+    def quantize_all(with_lr):
+        for l, (x, down) in enumerate(xs):
+            if with_lr:
+                T.quantize_activations_lowrank(x, down, out=codes[l], params=params[l], T=Ts[l])
+            else:
+                T.quantize_activations(x, out=codes[l], params=params[l])
 
-    quantize_all()
-    T.run_schedule(layers, table, wl.S, wl.T, 0, 1, workspace=ws)
-    torch.cuda.synchronize()
     ev = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
-    q_ms, g_ms = [], []
-    a0, a1 = ev(), ev()
-    a0.record()
-    for _ in range(reps):
-        for t in range(wl.T):
-            e0, e1, e2 = ev(), ev(), ev()
-            e0.record()
-            quantize_all()
-            e1.record()
-            T.run_schedule(layers, table, wl.S, wl.T, t, t + 1, workspace=ws)
-            e2.record()
-            q_ms.append((e0, e1))
-            g_ms.append((e1, e2))
-    a1.record()
-    torch.cuda.synchronize()
-    qm = float(np.mean([a.elapsed_time(b) for a, b in q_ms]))
-    gm = float(np.mean([a.elapsed_time(b) for a, b in g_ms]))
     elems = sum(float(s.M * s.K) for s in wl.layers)
-    ach = 5.0 * elems / (qm * 1e-3) / 1e9
-    return {"ms_per_denoising_step": round(a0.elapsed_time(a1) / reps / wl.T, 4),
+    out = {}
+    for name, layers, with_lr in (("plain", plain, False), (f"lowrank_r{rank}", lowrank, True)):
+        quantize_all(with_lr)
+        T.run_schedule(layers, table, wl.S, wl.T, 0, 1, workspace=ws)
+        torch.cuda.synchronize()
+        q_ms, g_ms = [], []
+        a0, a1 = ev(), ev()
+        a0.record()
+        for _ in range(reps):
+            for t in range(wl.T):
+                e0, e1, e2 = ev(), ev(), ev()
+                e0.record()
+                quantize_all(with_lr)
+                e1.record()
+                T.run_schedule(layers, table, wl.S, wl.T, t, t + 1, workspace=ws)
+                e2.record()
+                q_ms.append((e0, e1))
+                g_ms.append((e1, e2))
+        a1.record()
+        torch.cuda.synchronize()
+        qm = float(np.mean([a.elapsed_time(b) for a, b in q_ms]))
+        gm = float(np.mean([a.elapsed_time(b) for a, b in g_ms]))
+        alg = 5.0 * elems + (4.0 * rank * sum(float(s.M) for s in wl.layers) if with_lr else 0)
+        ach = alg / (qm * 1e-3) / 1e9
+        out[name] = {
+            "ms_per_denoising_step": round(a0.elapsed_time(a1) / reps / wl.T, 4),
             "quantize_ms": round(qm, 4), "grouped_launch_ms": round(gm, 4),
-            "quantizer_roofline": {"bound": "hbm", "achieved": round(ach, 1),
-                                   "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                                   "frac": round(ach / PEAK_HBM_GBS, 4),
-                                   "algorithmic_bytes": 5.0 * elems,
-                                   "kernels": "k_act_range, k_act_quantize per layer"}}
+            "quantizer_roofline": {
+                "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 4), "algorithmic_bytes": alg,
+                "kernels": ("k_lowrank_down<true>, k_act_quantize per layer" if with_lr
+                            else "k_act_range, k_act_quantize per layer")}}
+    return out
 
 
 def cpu_baseline(wl, table, budget_s=15.0):

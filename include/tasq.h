@@ -109,6 +109,16 @@ enum {
  *                   zero padding is not the code of a real zero, so
  *                   act_params on a TASQ_KIND_CONV3X3 layer or in
  *                   tasq_masked_conv3x3 is TASQ_ERR_LAYOUT.
+ *   lowrank_T       device fp32 [M][lowrank_rank] from tasq_lowrank_down (or
+ *                   tasq_quantize_activations_lowrank), or NULL: the 16-bit
+ *                   low-rank branch of an SVDQuant-initialised layer (Sec.
+ *                   4.1 setup, training-details appendix).  When given, y
+ *                   gains (lowrank_T lowrank_up^T)[m][n]; acc is unchanged.
+ *   lowrank_up      device bfloat16 [N][lowrank_rank], the branch's up
+ *                   projection (bit patterns); required with lowrank_T.
+ *   lowrank_rank    16 or 32 (TASQ_ERR_DIM otherwise).  lowrank_T and
+ *                   lowrank_up must be 16-byte aligned (TASQ_ERR_ALIGN);
+ *                   linear layers only (TASQ_ERR_LAYOUT on a conv).
  */
 typedef struct tasq_opts {
     int32_t variant;
@@ -119,6 +129,9 @@ typedef struct tasq_opts {
     const int8_t *W_packed;
     const float *act_params;
     const int32_t *colsums;
+    const float *lowrank_T;
+    const uint16_t *lowrank_up;
+    int32_t lowrank_rank;
 } tasq_opts;
 
 /*
@@ -233,6 +246,30 @@ int tasq_quantize_activations(const float *x, int M, int K, int8_t *X_out, float
 int tasq_weight_colsums(const int8_t *W, int N, int K, int32_t *colsums_out, void *stream);
 
 /*
+ * Down projection of the 16-bit low-rank branch (Sec. 4.1 setup: a frozen
+ * rank-16 or rank-32 branch beside the quantized weight):
+ *   T[m][j] = sum_k bf16(x[m][k]) * down[j][k],
+ * bf16() rounding to nearest bfloat16, ties to even; fp32 accumulation.
+ *   x        fp32 [M][K] device, finite values, 4-byte aligned.
+ *   down     bfloat16 [r][K] device (bit patterns), 2-byte aligned.
+ *   r        16 or 32.
+ *   T_out    fp32 [M][r] device, the lowrank_T of tasq_opts / tasq_layer.
+ * M == 0 enqueues nothing; K == 0 writes zeros.  Errors: TASQ_ERR_NULL,
+ * _DIM (negative sizes, r not 16 or 32, M*r*4 >= 2^31), _ALIGN, _HIP.
+ */
+int tasq_lowrank_down(const float *x, int M, int K, const uint16_t *down, int r, float *T_out,
+                      void *stream);
+
+/*
+ * tasq_quantize_activations and tasq_lowrank_down of the same x in one read
+ * of x: the down projection's pass also folds the range of x.  Arguments and
+ * errors as in the two calls.
+ */
+int tasq_quantize_activations_lowrank(const float *x, int M, int K, int8_t *X_out,
+                                      float *act_params, const uint16_t *down, int r,
+                                      float *T_out, void *stream);
+
+/*
  * Stage of denoising step t (Sec. 3.2: contiguous stages sharing one mask;
  * Sec. 4.1: 20 steps in four stages, or one stage per step when S = T;
  * App. D.1: stage 0 is the noisiest, first part of the trajectory):
@@ -260,6 +297,9 @@ typedef struct tasq_layer {
     const int8_t *W_packed;     /* packed copy of W or NULL (tasq_pack_weights) */
     const float *act_params;    /* asymmetric activations (see tasq_opts) or NULL */
     const int32_t *colsums;     /* [8][N] channel sums, required with act_params */
+    const float *lowrank_T;     /* low-rank branch (see tasq_opts) or NULL */
+    const uint16_t *lowrank_up;
+    int32_t lowrank_rank;
 } tasq_layer;
 
 /*

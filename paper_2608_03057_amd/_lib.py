@@ -39,7 +39,8 @@ KIND_CONV3X3 = 1
 EXPORTS = (
     "tasq_masked_linear", "tasq_masked_conv3x3", "tasq_pack_planes", "tasq_planes_bytes",
     "tasq_pack_weights", "tasq_packed_weight_bytes", "tasq_quantize_activations",
-    "tasq_weight_colsums", "tasq_stage_of_step", "tasq_run_schedule",
+    "tasq_weight_colsums", "tasq_lowrank_down", "tasq_quantize_activations_lowrank",
+    "tasq_stage_of_step", "tasq_run_schedule",
     "tasq_workspace_bytes", "tasq_schedule_workspace_bytes", "tasq_status_string",
 )
 
@@ -48,7 +49,9 @@ class Opts(ctypes.Structure):
     _fields_ = [("variant", ctypes.c_int32), ("split_k", ctypes.c_int32),
                 ("W_planes", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
                 ("workspace_bytes", ctypes.c_size_t), ("W_packed", ctypes.c_void_p),
-                ("act_params", ctypes.c_void_p), ("colsums", ctypes.c_void_p)]
+                ("act_params", ctypes.c_void_p), ("colsums", ctypes.c_void_p),
+                ("lowrank_T", ctypes.c_void_p), ("lowrank_up", ctypes.c_void_p),
+                ("lowrank_rank", ctypes.c_int32)]
 
 
 class Layer(ctypes.Structure):
@@ -58,7 +61,9 @@ class Layer(ctypes.Structure):
                 ("X", ctypes.c_void_p), ("W", ctypes.c_void_p), ("W_planes", ctypes.c_void_p),
                 ("sw", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("acc", ctypes.c_void_p),
                 ("y", ctypes.c_void_p), ("W_packed", ctypes.c_void_p),
-                ("act_params", ctypes.c_void_p), ("colsums", ctypes.c_void_p)]
+                ("act_params", ctypes.c_void_p), ("colsums", ctypes.c_void_p),
+                ("lowrank_T", ctypes.c_void_p), ("lowrank_up", ctypes.c_void_p),
+                ("lowrank_rank", ctypes.c_int32)]
 
 
 class TasqError(RuntimeError):
@@ -95,6 +100,10 @@ def lib() -> ctypes.CDLL:
         L.tasq_quantize_activations.restype = i32
         L.tasq_weight_colsums.argtypes = [vp, i32, i32, vp, vp]
         L.tasq_weight_colsums.restype = i32
+        L.tasq_lowrank_down.argtypes = [vp, i32, i32, vp, i32, vp, vp]
+        L.tasq_lowrank_down.restype = i32
+        L.tasq_quantize_activations_lowrank.argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp]
+        L.tasq_quantize_activations_lowrank.restype = i32
         L.tasq_stage_of_step.argtypes = [i32, i32, i32]
         L.tasq_stage_of_step.restype = i32
         L.tasq_run_schedule.argtypes = [ctypes.POINTER(Layer), i32, vp, i32, i32, i32, i32,

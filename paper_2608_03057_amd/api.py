@@ -37,7 +37,8 @@ def _need(t: Optional[torch.Tensor], dtype, shape, name):
         raise ValueError(f"{name} must be contiguous")
 
 
-def _opts(variant, planes, workspace, split_k, packed=None, act=None, colsums=None) -> Opts:
+def _opts(variant, planes, workspace, split_k, packed=None, act=None, colsums=None,
+          lowrank=None) -> Opts:
     o = Opts()
     o.variant = variant
     o.split_k = split_k
@@ -47,7 +48,18 @@ def _opts(variant, planes, workspace, split_k, packed=None, act=None, colsums=No
     o.W_packed = _ptr(packed)
     o.act_params = _ptr(act)
     o.colsums = _ptr(colsums)
+    if lowrank is not None:
+        o.lowrank_T, o.lowrank_up, o.lowrank_rank = _lowrank_fields(lowrank)
     return o
+
+
+def _lowrank_fields(lowrank):
+    """(T, up) of a low-rank branch -> the three struct fields."""
+    T, up = lowrank
+    if up.dtype not in (torch.bfloat16, torch.int16):
+        raise ValueError("lowrank up projection must be bfloat16 (or its int16 bit patterns)")
+    _need(T, torch.float32, (T.shape[0], up.shape[1]), "lowrank T")
+    return _ptr(T), _ptr(up), int(up.shape[1])
 
 
 def status_string(status: int) -> str:
@@ -118,6 +130,48 @@ def quantize_activations(x: torch.Tensor, out: Optional[torch.Tensor] = None,
     return out, params
 
 
+def lowrank_down(x: torch.Tensor, down: torch.Tensor, out: Optional[torch.Tensor] = None):
+    """T = bf16(x) down^T, fp32 [M, r], of fp32 x [M, K] and a bfloat16 (or
+    int16 bit-pattern) down projection [r, K]."""
+    M, K = x.shape
+    r = down.shape[0]
+    _need(x, torch.float32, (M, K), "x")
+    if down.dtype not in (torch.bfloat16, torch.int16) or tuple(down.shape) != (r, K):
+        raise ValueError("down must be bfloat16 [r, K]")
+    if out is None:
+        out = torch.empty((M, r), dtype=torch.float32, device=x.device)
+    _need(out, torch.float32, (M, r), "out")
+    check(_lib.lib().tasq_lowrank_down(_ptr(x), M, K, _ptr(down), r, _ptr(out), _stream()),
+          "tasq_lowrank_down")
+    return out
+
+
+def quantize_activations_lowrank(x: torch.Tensor, down: torch.Tensor,
+                                 out: Optional[torch.Tensor] = None,
+                                 params: Optional[torch.Tensor] = None,
+                                 T: Optional[torch.Tensor] = None):
+    """(codes, params, T): quantize_activations and lowrank_down of x in one
+    read of x."""
+    M, K = x.shape
+    r = down.shape[0]
+    _need(x, torch.float32, (M, K), "x")
+    if down.dtype not in (torch.bfloat16, torch.int16) or tuple(down.shape) != (r, K):
+        raise ValueError("down must be bfloat16 [r, K]")
+    if out is None:
+        out = torch.empty((M, K), dtype=torch.int8, device=x.device)
+    if params is None:
+        params = torch.empty(_lib.TASQ_ACT_PARAMS_FLOATS, dtype=torch.float32, device=x.device)
+    if T is None:
+        T = torch.empty((M, r), dtype=torch.float32, device=x.device)
+    _need(out, torch.int8, (M, K), "out")
+    _need(params, torch.float32, (_lib.TASQ_ACT_PARAMS_FLOATS,), "params")
+    _need(T, torch.float32, (M, r), "T")
+    check(_lib.lib().tasq_quantize_activations_lowrank(_ptr(x), M, K, _ptr(out), _ptr(params),
+                                                       _ptr(down), r, _ptr(T), _stream()),
+          "tasq_quantize_activations_lowrank")
+    return out, params, T
+
+
 def weight_colsums(W: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """int32 [8, N]: row b-1 holds sum_k W_b[n][k] of int8 W [N, ...]."""
     N = W.shape[0]
@@ -137,10 +191,13 @@ def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: tor
                   y: Optional[torch.Tensor] = None, variant: int = _lib.VARIANT_AUTO,
                   planes: Optional[torch.Tensor] = None, packed: Optional[torch.Tensor] = None,
                   workspace: Optional[torch.Tensor] = None, split_k: int = 0,
-                  act: Optional[torch.Tensor] = None, colsums: Optional[torch.Tensor] = None):
+                  act: Optional[torch.Tensor] = None, colsums: Optional[torch.Tensor] = None,
+                  lowrank=None):
     """(acc int32 [M, N] or None, y fp32 [M, N] or None) of the masked layer.
     With ``act`` (params of quantize_activations) and ``colsums`` X holds
-    asymmetric activation codes and sx is ignored."""
+    asymmetric activation codes and sx is ignored.  ``lowrank`` = (T, up)
+    adds the low-rank branch T up^T to y (T from lowrank_down, up bfloat16
+    [N, r])."""
     M, K = X.shape
     N = sw.shape[0]
     _need(X, torch.int8, (M, K), "X")
@@ -159,7 +216,7 @@ def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: tor
         if wb:
             workspace = torch.empty(wb, dtype=torch.uint8, device=X.device)
     _need(colsums, torch.int32, (8, N), "colsums")
-    o = _opts(variant, planes, workspace, split_k, packed, act, colsums)
+    o = _opts(variant, planes, workspace, split_k, packed, act, colsums, lowrank)
     rc = _lib.lib().tasq_masked_linear(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias), M, N,
                                        K, int(b), _ptr(acc), _ptr(y), ctypes.byref(o), _stream())
     check(rc, "tasq_masked_linear")
@@ -193,7 +250,7 @@ def masked_conv3x3(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: to
 
 
 def make_layer(X, W, sx, sw, bias=None, acc=None, y=None, planes=None, kind=None,
-               packed=None, act=None, colsums=None) -> Layer:
+               packed=None, act=None, colsums=None, lowrank=None) -> Layer:
     """A tasq_layer for run_schedule; tensors must stay alive while in use."""
     L = Layer()
     if kind is None:
@@ -212,6 +269,8 @@ def make_layer(X, W, sx, sw, bias=None, acc=None, y=None, planes=None, kind=None
     L.W_packed = _ptr(packed)
     L.act_params = _ptr(act)
     L.colsums = _ptr(colsums)
+    if lowrank is not None:
+        L.lowrank_T, L.lowrank_up, L.lowrank_rank = _lowrank_fields(lowrank)
     return L
 
 

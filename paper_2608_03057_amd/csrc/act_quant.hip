@@ -158,6 +158,138 @@ __global__ void __launch_bounds__(256) k_act_quantize(const float *__restrict__ 
         q[i] = code_of(x[i], alpha, z);
 }
 
+// ------------------------------------------------- low-rank down projection
+//
+// T = x~ D^T for the 16-bit low-rank branch: x~ is x rounded to bfloat16
+// (nearest, ties to even), D [r x K] bfloat16, T fp32 [M x r], r <= 32.
+// One workgroup per 32-row block (grid-stride over blocks); its 8 waves take
+// interleaved 16-wide K steps, each a v_mfma_f32_32x32x16_bf16 with lane l
+// feeding row l%32 of x and column l%32 of D^T (columns past r are zero).
+// The waves' partial blocks are summed through LDS in a fixed order, so T
+// does not depend on timing.  The same pass can fold the range of x (one
+// partial per workgroup, as k_act_range), so that quantizing the codes and
+// projecting share one read of x.
+
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+
+constexpr int kDownWaves = 8;
+
+__device__ __forceinline__ uint32_t bf16_rne(float f)
+{
+    const uint32_t u = __float_as_uint(f);
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <bool RANGE>
+__global__ void __launch_bounds__(64 * kDownWaves)
+k_lowrank_down(const float *__restrict__ x, int M, int K, const uint16_t *__restrict__ D, int r,
+               float *__restrict__ T, uint32_t *__restrict__ part, bool fast)
+{
+    __shared__ float red[kDownWaves][16][64];
+    __shared__ uint32_t smin[kDownWaves], smax[kDownWaves];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int half = lane >> 5;
+    const int j = lane & 31;                         // column of D^T this lane feeds
+    const int nsteps = (K + 15) / 16;
+    const int nblocks = (M + 31) / 32;
+    float mn = __builtin_huge_valf(), mx = -__builtin_huge_valf();
+
+    for (int rb = blockIdx.x; rb < nblocks; rb += gridDim.x) {
+        const int row = rb * 32 + j;
+        const bool rok = row < M;
+        const float *xr = x + (size_t)(rok ? row : 0) * (size_t)K;
+        const uint16_t *dr = D + (size_t)(j < r ? j : 0) * (size_t)K;
+        v16f acc = {};
+        for (int s = wave; s < nsteps; s += kDownWaves) {
+            const int k = 16 * s + 8 * half;
+            float xv[8];
+            v4u bw;
+            if (fast) {
+                // K % 8 == 0 and 16-byte aligned rows: k < K covers all 8.
+                const bool ok = rok && k < K;
+                float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
+                if (ok) {
+                    const float4 *p = reinterpret_cast<const float4 *>(xr + k);
+                    lo = p[0];
+                    hi = p[1];
+                }
+                xv[0] = lo.x; xv[1] = lo.y; xv[2] = lo.z; xv[3] = lo.w;
+                xv[4] = hi.x; xv[5] = hi.y; xv[6] = hi.z; xv[7] = hi.w;
+                if (ok) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        mn = fminf(mn, xv[e]);
+                        mx = fmaxf(mx, xv[e]);
+                    }
+                }
+                bw = v4u{0, 0, 0, 0};
+                if (j < r && k < K)
+                    bw = *reinterpret_cast<const v4u *>(dr + k);
+            } else {
+                uint32_t dv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const bool ok = k + e < K;
+                    xv[e] = (rok && ok) ? xr[k + e] : 0.f;
+                    if (rok && ok) {
+                        mn = fminf(mn, xv[e]);
+                        mx = fmaxf(mx, xv[e]);
+                    }
+                    dv[e] = (j < r && ok) ? (uint32_t)dr[k + e] : 0u;
+                }
+                bw = v4u{dv[0] | (dv[1] << 16), dv[2] | (dv[3] << 16), dv[4] | (dv[5] << 16),
+                         dv[6] | (dv[7] << 16)};
+            }
+            const v4u aw = v4u{bf16_rne(xv[0]) | (bf16_rne(xv[1]) << 16),
+                               bf16_rne(xv[2]) | (bf16_rne(xv[3]) << 16),
+                               bf16_rne(xv[4]) | (bf16_rne(xv[5]) << 16),
+                               bf16_rne(xv[6]) | (bf16_rne(xv[7]) << 16)};
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, aw),
+                                                          __builtin_bit_cast(v8bf, bw), acc, 0, 0,
+                                                          0);
+        }
+        // Register v of lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32.
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+            red[wave][v][lane] = acc[v];
+        __syncthreads();
+        for (int e = threadIdx.x; e < 32 * 32; e += 64 * kDownWaves) {
+            const int v = e >> 6, l = e & 63;
+            const int orow = rb * 32 + 8 * (v >> 2) + 4 * (l >> 5) + (v & 3);
+            const int ocol = l & 31;
+            float sum = red[0][v][l];
+#pragma unroll
+            for (int w = 1; w < kDownWaves; ++w)
+                sum += red[w][v][l];
+            if (orow < M && ocol < r)
+                T[(size_t)orow * (size_t)r + ocol] = sum;
+        }
+        __syncthreads();
+    }
+    if (RANGE) {
+        uint32_t kmn = order_key(mn), kmx = order_key(mx);
+        for (int off = 32; off > 0; off >>= 1) {
+            kmn = min(kmn, (uint32_t)__shfl_xor((int)kmn, off));
+            kmx = max(kmx, (uint32_t)__shfl_xor((int)kmx, off));
+        }
+        if (lane == 0) {
+            smin[wave] = kmn;
+            smax[wave] = kmx;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            for (int w = 1; w < kDownWaves; ++w) {
+                kmn = min(kmn, smin[w]);
+                kmx = max(kmx, smax[w]);
+            }
+            part[2 * blockIdx.x] = kmn;
+            part[2 * blockIdx.x + 1] = kmx;
+        }
+    }
+}
+
 // One wave per output channel: the eight sums sum_k W_b[n][k], b = 1..8.
 __global__ void __launch_bounds__(256) k_weight_colsums(const int8_t *__restrict__ W, int N, int K,
                                                         int32_t *__restrict__ colsums)
@@ -206,6 +338,42 @@ hipError_t launch_quantize_activations(const float *x, long long n, int8_t *q, f
     const int G = grid_for(items, 256 * 4, kActPartials);
     uint32_t *part = reinterpret_cast<uint32_t *>(params + kActHeader);
     hipLaunchKernelGGL(k_act_range, dim3(G), dim3(256), 0, stream, x, n, n4, part);
+    hipLaunchKernelGGL(k_act_quantize, dim3(grid_for(items, 256, 1024)), dim3(256), 0, stream, x,
+                       n, n4, q, params, G);
+    return hipGetLastError();
+}
+
+hipError_t launch_lowrank_down(const float *x, int M, int K, const uint16_t *D, int r, float *T,
+                               uint32_t *part, int *groups, hipStream_t stream)
+{
+    const bool fast = (K % 8) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
+                      (reinterpret_cast<uintptr_t>(D) & 15) == 0;
+    const int G = grid_for(M, 32, kActPartials);
+    if (groups)
+        *groups = G;
+    if (part)
+        hipLaunchKernelGGL(k_lowrank_down<true>, dim3(G), dim3(64 * kDownWaves), 0, stream, x, M,
+                           K, D, r, T, part, fast);
+    else
+        hipLaunchKernelGGL(k_lowrank_down<false>, dim3(G), dim3(64 * kDownWaves), 0, stream, x, M,
+                           K, D, r, T, part, fast);
+    return hipGetLastError();
+}
+
+hipError_t launch_quantize_activations_lowrank(const float *x, int M, int K, int8_t *q,
+                                               float *params, const uint16_t *D, int r, float *T,
+                                               hipStream_t stream)
+{
+    int G = 0;
+    uint32_t *part = reinterpret_cast<uint32_t *>(params + kActHeader);
+    hipError_t e = launch_lowrank_down(x, M, K, D, r, T, part, &G, stream);
+    if (e != hipSuccess)
+        return e;
+    const long long n = (long long)M * K;
+    const bool vec = (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
+                     (reinterpret_cast<uintptr_t>(q) & 3) == 0;
+    const long long n4 = vec ? n >> 2 : 0;
+    const long long items = vec ? (n + 3) / 4 : n;
     hipLaunchKernelGGL(k_act_quantize, dim3(grid_for(items, 256, 1024)), dim3(256), 0, stream, x,
                        n, n4, q, params, G);
     return hipGetLastError();

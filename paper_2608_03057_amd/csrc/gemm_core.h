@@ -29,6 +29,13 @@ namespace tasq {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+// LDS row pitch of the low-rank branch's staged operands: a rank-32 row of
+// bfloat16 plus 16 bytes, so that the 16-byte fragment reads of 8
+// consecutive rows fall in distinct banks.
+constexpr int kLrPitch = 2 * kLowrankMaxRank + 16;
 
 template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int PF_ = 2, int OCC_ = 2>
 struct Cfg {
@@ -43,6 +50,11 @@ struct Cfg {
     static constexpr int CPR = BK / 16;                 // 16-byte chunks per row
     static constexpr int A_LOADS = BM * CPR / NT;
     static constexpr int B_LOADS = BN * CPR / NT;
+    // LDS of the A operand, also holding the low-rank operands in the
+    // epilogue: T rows as bfloat16 hi and lo parts, then rows of U.
+    static constexpr int LR_BYTES = (2 * BM + BN) * kLrPitch;
+    static constexpr int SMA = NSTAGE * BM * CPR > (LR_BYTES + 15) / 16 ? NSTAGE * BM * CPR
+                                                                       : (LR_BYTES + 15) / 16;
     static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must hold 32x32 blocks");
     static_assert(BK % 32 == 0 && (CPR == 4 || CPR == 8), "BK must be 64 or 128");
     static_assert((BM * CPR) % NT == 0 && (BN * CPR) % NT == 0, "loads must divide");
@@ -441,21 +453,101 @@ __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int
     }
 }
 
+// ------------------------------------------------------ low-rank branch
+
+// fp32 t as hi + lo bfloat16 bit patterns: hi keeps the top 16 bits (an
+// exact truncation), lo is the remainder t - hi (exact in fp32) rounded to
+// nearest even, so hi + lo = t within 2^-16 |t|.
+__device__ __forceinline__ void split_bf16(float t, uint32_t &hi, uint32_t &lo)
+{
+    const uint32_t u = __float_as_uint(t);
+    hi = u >> 16;
+    const uint32_t rem = __float_as_uint(t - __uint_as_float(u & 0xffff0000u));
+    lo = (rem + 0x7fffu + ((rem >> 16) & 1u)) >> 16;
+}
+
+// Stages the tile's low-rank operands in LDS: T rows m0.. (fp32 [M][r],
+// split into bfloat16 hi and lo parts) and U rows n0.. (bfloat16 [N][r]).
+// Rows past M or N read zero through the buffer bounds.
+template <class C>
+__device__ __forceinline__ void stage_lowrank(const LayerDesc &d, int m0, int n0, char *lds)
+{
+    const int r = d.lr_r;
+    const rsrc_t rU = make_rsrc(d.lr_U, (uint32_t)d.N * (uint32_t)r * 2u);
+    char *Thi = lds, *Tlo = lds + C::BM * kLrPitch, *Us = lds + 2 * C::BM * kLrPitch;
+    const int tpr = r / 4;
+    for (int e = threadIdx.x; e < C::BM * tpr; e += C::NT) {
+        const int row = e / tpr, c = e % tpr;
+        // A plain float4 load: the components of a 16-byte buffer load taken
+        // apart one by one here compiled to one dword load used four times.
+        float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (m0 + row < d.M)
+            t = *reinterpret_cast<const float4 *>(d.lr_T + (size_t)(m0 + row) * r + 4 * c);
+        uint32_t h[4], l[4];
+        split_bf16(t.x, h[0], l[0]);
+        split_bf16(t.y, h[1], l[1]);
+        split_bf16(t.z, h[2], l[2]);
+        split_bf16(t.w, h[3], l[3]);
+        *reinterpret_cast<uint2 *>(Thi + row * kLrPitch + 8 * c) =
+            make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+        *reinterpret_cast<uint2 *>(Tlo + row * kLrPitch + 8 * c) =
+            make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
+    }
+    const int upr = r / 8;
+    for (int e = threadIdx.x; e < C::BN * upr; e += C::NT) {
+        const int row = e / upr, c = e % upr;
+        *reinterpret_cast<v4i *>(Us + row * kLrPitch + 16 * c) =
+            ld16(rU, ((uint32_t)(n0 + row) * (uint32_t)r + 8u * c) * 2u);
+    }
+}
+
+// The 32x32 block (rows rl.., columns cl.. of the tile) of T U^T from the
+// staged operands: per 16-wide step of the rank, one bfloat16 MFMA on the hi
+// and one on the lo part of T, accumulated in fp32.  Same register layout
+// as the integer accumulators.
+template <class C>
+__device__ __forceinline__ v16f lowrank_block(const char *lds, int r, int rl, int cl, int lane)
+{
+    const char *Thi = lds, *Tlo = lds + C::BM * kLrPitch, *Us = lds + 2 * C::BM * kLrPitch;
+    const int ao = (rl + (lane & 31)) * kLrPitch + 16 * (lane >> 5);
+    const int bo = (cl + (lane & 31)) * kLrPitch + 16 * (lane >> 5);
+    v16f out = {};
+#pragma unroll
+    for (int s = 0; s < kLowrankMaxRank / 16; ++s) {
+        if (16 * s < r) {
+            const v8bf b = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4i *>(Us + bo + 32 * s));
+            const v8bf ah = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4i *>(Thi + ao + 32 * s));
+            const v8bf al = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4i *>(Tlo + ao + 32 * s));
+            out = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b, out, 0, 0, 0);
+            out = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b, out, 0, 0, 0);
+        }
+    }
+    return out;
+}
+
 // Writes a finished tile: int32 accumulators and/or the fp32 dequantised
 // value y = float(acc) * (sx * sw[n]) + bias[n].  With asymmetric
 // activations (d.act) the zero point enters through the channel sum of W_b:
-// y = (float(acc) + (128 - z) * colsum_b[n]) * (alpha * sw[n]) + bias[n].  Register v of a 32x32
+// y = (float(acc) + (128 - z) * colsum_b[n]) * (alpha * sw[n]) + bias[n].
+// With a low-rank branch (d.lr_T) y also gains (T U^T)[m][n], computed here
+// from operands staged in the (then idle) LDS.  Register v of a 32x32
 // accumulator in lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32, so
 // each store instruction covers two 128-byte row segments.  Rows past M
 // fall past the buffer end and are dropped; columns past N carry kOOB.
 template <class C>
 __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
-                                         const v16i (&acc)[C::FM][C::FN], int bits)
+                                         const v16i (&acc)[C::FM][C::FN], int bits, char *lds)
 {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+    const bool lowrank = d.lr_T != nullptr && d.y != nullptr;
+    if (lowrank) {
+        __syncthreads();            // every wave is done with the main loop's LDS
+        stage_lowrank<C>(d, m0, n0, lds);
+        __syncthreads();
+    }
     const uint32_t outb = (uint32_t)d.M * (uint32_t)d.N * 4u;
     const rsrc_t ry = make_rsrc(d.y, d.y ? outb : 0u);
     const rsrc_t ra = make_rsrc(d.acc, d.acc ? outb : 0u);
@@ -487,12 +579,23 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
         }
         if (d.y) {
 #pragma unroll
-            for (int i = 0; i < C::FM; ++i)
+            for (int i = 0; i < C::FM; ++i) {
+                if (lowrank) {
+                    const v16f lr = lowrank_block<C>(lds, d.lr_r, wm * C::WTM + i * 32,
+                                                     wn * C::WTN + j * 32, lane);
 #pragma unroll
-                for (int v = 0; v < 16; ++v)
-                    st32(ry, base + (uint32_t)(i * 32 + 8 * (v >> 2) + (v & 3)) * rowb,
-                         __builtin_bit_cast(uint32_t,
-                                            ((float)acc[i][j][v] + corr) * scale + bias));
+                    for (int v = 0; v < 16; ++v)
+                        st32(ry, base + (uint32_t)(i * 32 + 8 * (v >> 2) + (v & 3)) * rowb,
+                             __builtin_bit_cast(uint32_t, ((float)acc[i][j][v] + corr) * scale +
+                                                              bias + lr[v]));
+                } else {
+#pragma unroll
+                    for (int v = 0; v < 16; ++v)
+                        st32(ry, base + (uint32_t)(i * 32 + 8 * (v >> 2) + (v & 3)) * rowb,
+                             __builtin_bit_cast(uint32_t,
+                                                ((float)acc[i][j][v] + corr) * scale + bias));
+                }
+            }
         }
     }
 }
@@ -531,7 +634,7 @@ __device__ __forceinline__ void tile_coords(int t, int tiles_m, int tiles_n, int
 template <class C, bool ALIGNED, int KIND, bool PLANES>
 __global__ void __launch_bounds__(C::NT, C::OCC) k_masked_gemm(LayerDesc d)
 {
-    __shared__ v4i smA[C::NSTAGE * C::BM * C::CPR];
+    __shared__ v4i smA[C::SMA];
     __shared__ v4i smB[C::NSTAGE * C::BN * C::CPR];
     int tm, tn;
     tile_coords(xcd_remap(blockIdx.x, gridDim.x), d.tiles_m, d.tiles_n, tm, tn);
@@ -539,7 +642,7 @@ __global__ void __launch_bounds__(C::NT, C::OCC) k_masked_gemm(LayerDesc d)
     v16i acc[C::FM][C::FN];
     mainloop<C, ALIGNED, KIND, PLANES>(d, keep_mask_dword(d.bits), m0, n0, 0, d.K, acc, smA,
                                        smB);
-    epilogue<C>(d, m0, n0, acc, d.bits);
+    epilogue<C>(d, m0, n0, acc, d.bits, reinterpret_cast<char *>(smA));
 }
 
 // Grouped launch over every layer of one denoising step: workgroup t finds
@@ -552,7 +655,7 @@ __global__ void __launch_bounds__(C::NT, C::OCC)
 k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *table, int S,
                       int stage)
 {
-    __shared__ v4i smA[C::NSTAGE * C::BM * C::CPR];
+    __shared__ v4i smA[C::SMA];
     __shared__ v4i smB[C::NSTAGE * C::BN * C::CPR];
     const int t = xcd_remap(blockIdx.x, gridDim.x);
     int lo = 0, hi = L - 1;
@@ -574,7 +677,7 @@ k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
         mainloop<C, true, KIND_CONV3X3>(d, wmask, m0, n0, 0, d.K, acc, smA, smB);
     else
         mainloop<C, true, KIND_LINEAR>(d, wmask, m0, n0, 0, d.K, acc, smA, smB);
-    epilogue<C>(d, m0, n0, acc, bits);
+    epilogue<C>(d, m0, n0, acc, bits, reinterpret_cast<char *>(smA));
 }
 
 // ---------------------------------------------------------------- launchers

@@ -36,6 +36,9 @@ struct CfgP {
     static constexpr int FM = WTM / 32, FN = WTN / 32;
     static constexpr int CPR = BK / 16, KK = BK / 32;
     static constexpr int SA = BM * CPR;                 // v4i per LDS stage
+    // LDS of the kernel: two stages, or the epilogue's low-rank operands.
+    static constexpr int LR_BYTES = (2 * BM + BN) * kLrPitch;
+    static constexpr int SM = 2 * SA > (LR_BYTES + 15) / 16 ? 2 * SA : (LR_BYTES + 15) / 16;
     static constexpr int A_LOADS = BM * CPR / NT;
     static constexpr int B_LOADS = 0;                   // weights bypass LDS
     static constexpr int PF = PF_;                      // activation K tiles in the ring
@@ -187,13 +190,13 @@ __device__ __forceinline__ void mainloop_packed(const LayerDesc &d, uint32_t wma
 template <class C, bool ALIGNED, int KIND>
 __global__ void __launch_bounds__(C::NT, C::OCC) k_gemm_packed(LayerDesc d)
 {
-    __shared__ v4i sm[2 * C::SA];
+    __shared__ v4i sm[C::SM];
     int tm, tn;
     tile_coords(xcd_remap(blockIdx.x, gridDim.x), d.tiles_m, d.tiles_n, tm, tn);
     const int m0 = tm * C::BM, n0 = tn * C::BN;
     v16i acc[C::FM][C::FN];
     mainloop_packed<C, ALIGNED, KIND>(d, keep_mask_dword(d.bits), m0, n0, acc, sm);
-    epilogue<C>(d, m0, n0, acc, d.bits);
+    epilogue<C>(d, m0, n0, acc, d.bits, reinterpret_cast<char *>(sm));
 }
 
 // Grouped step over every layer (see k_masked_gemm_grouped); every layer
@@ -203,7 +206,7 @@ __global__ void __launch_bounds__(C::NT, C::OCC)
 k_gemm_packed_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *table, int S,
                       int stage)
 {
-    __shared__ v4i sm[2 * C::SA];
+    __shared__ v4i sm[C::SM];
     const int t = xcd_remap(blockIdx.x, gridDim.x);
     int lo = 0, hi = L - 1;
     while (lo < hi) {
@@ -224,7 +227,7 @@ k_gemm_packed_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
         mainloop_packed<C, true, KIND_CONV3X3>(d, wmask, m0, n0, acc, sm);
     else
         mainloop_packed<C, true, KIND_LINEAR>(d, wmask, m0, n0, acc, sm);
-    epilogue<C>(d, m0, n0, acc, bits);
+    epilogue<C>(d, m0, n0, acc, bits, reinterpret_cast<char *>(sm));
 }
 
 template <class C>

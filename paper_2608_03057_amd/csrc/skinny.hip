@@ -207,8 +207,18 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
         const size_t o = (size_t)row * (size_t)d.N + (size_t)nn;
         if (d.acc)
             d.acc[o] = sum;
-        if (d.y)
-            d.y[o] = ((float)sum + corr) * scale + bias;
+        if (d.y) {
+            // Low-rank branch (T U^T)[row][nn]: a rank <= 32 dot product in
+            // fp32 (U in bfloat16).
+            float lr = 0.f;
+            if (d.lr_T) {
+                const float *t = d.lr_T + (size_t)row * (size_t)d.lr_r;
+                const uint16_t *u = d.lr_U + (size_t)nn * (size_t)d.lr_r;
+                for (int q = 0; q < d.lr_r; ++q)
+                    lr = fmaf(t[q], __uint_as_float((uint32_t)u[q] << 16), lr);
+            }
+            d.y[o] = ((float)sum + corr) * scale + bias + lr;
+        }
     }
 }
 

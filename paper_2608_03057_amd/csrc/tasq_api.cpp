@@ -220,6 +220,15 @@ LayerDesc make_desc(const tasq_layer &L, const tasq_opts *o)
     d.Wp = L.W_packed ? L.W_packed : (o ? o->W_packed : nullptr);
     d.act = L.act_params ? L.act_params : (o ? o->act_params : nullptr);
     d.colsums = L.colsums ? L.colsums : (o ? o->colsums : nullptr);
+    if (L.lowrank_T) {
+        d.lr_T = L.lowrank_T;
+        d.lr_U = L.lowrank_up;
+        d.lr_r = L.lowrank_rank;
+    } else if (o && o->lowrank_T) {
+        d.lr_T = o->lowrank_T;
+        d.lr_U = o->lowrank_up;
+        d.lr_r = o->lowrank_rank;
+    }
     d.sw = L.sw;
     d.bias = L.bias;
     d.acc = L.acc;
@@ -263,6 +272,27 @@ int validate_layer(const tasq_layer &L, const tasq_opts *o)
     if ((reinterpret_cast<uintptr_t>(local.act_params) & 3) ||
         (reinterpret_cast<uintptr_t>(local.colsums) & 3))
         return TASQ_ERR_ALIGN;
+    // Low-rank branch: the layer's own fields, else the call's.
+    if (L.lowrank_T) {
+        local.lowrank_T = L.lowrank_T;
+        local.lowrank_up = L.lowrank_up;
+        local.lowrank_rank = L.lowrank_rank;
+    }
+    if (has_out && L.y && local.lowrank_T) {
+        if (!local.lowrank_up)
+            return TASQ_ERR_NULL;
+        if (local.lowrank_rank != 16 && local.lowrank_rank != 32)
+            return TASQ_ERR_DIM;
+        if ((reinterpret_cast<uintptr_t>(local.lowrank_T) & 15) ||
+            (reinterpret_cast<uintptr_t>(local.lowrank_up) & 15))
+            return TASQ_ERR_ALIGN;
+        if (L.kind == TASQ_KIND_CONV3X3)
+            return TASQ_ERR_LAYOUT;
+        // Staged through 32-bit buffer offsets, with a tile's rows past M.
+        if (((long long)L.M + 256) * local.lowrank_rank * 4 >= (1LL << 31) ||
+            ((long long)L.N + 256) * local.lowrank_rank * 2 >= (1LL << 31))
+            return TASQ_ERR_DIM;
+    }
     const bool needs_w = L.N > 0 && L.K > 0;
     if (int rc = check_variant(&local, needs_w ? L.W : reinterpret_cast<const int8_t *>(1)))
         return rc;
@@ -439,6 +469,57 @@ int tasq_quantize_activations(const float *x, int M, int K, int8_t *X_out, float
         return TASQ_ERR_ALIGN;
     hipError_t e = tasq::launch_quantize_activations(x, n, X_out, act_params,
                                                      static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}
+
+static int check_lowrank_down(const float *x, int M, int K, const uint16_t *down, int r,
+                              const float *T_out)
+{
+    if (M < 0 || K < 0 || (r != 16 && r != 32))
+        return TASQ_ERR_DIM;
+    if ((long long)M * r * 4 >= (1LL << 31) || K > (1 << 30) / 32)
+        return TASQ_ERR_DIM;
+    if (M == 0)
+        return TASQ_OK;
+    if (!T_out || (K > 0 && (!x || !down)))
+        return TASQ_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(x) & 3) || (reinterpret_cast<uintptr_t>(down) & 1) ||
+        (reinterpret_cast<uintptr_t>(T_out) & 3))
+        return TASQ_ERR_ALIGN;
+    return TASQ_OK;
+}
+
+int tasq_lowrank_down(const float *x, int M, int K, const uint16_t *down, int r, float *T_out,
+                      void *stream)
+{
+    if (int rc = check_lowrank_down(x, M, K, down, r, T_out))
+        return rc;
+    if (M == 0)
+        return TASQ_OK;
+    hipError_t e = tasq::launch_lowrank_down(x, M, K, down, r, T_out, nullptr, nullptr,
+                                             static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}
+
+int tasq_quantize_activations_lowrank(const float *x, int M, int K, int8_t *X_out,
+                                      float *act_params, const uint16_t *down, int r,
+                                      float *T_out, void *stream)
+{
+    if (int rc = check_lowrank_down(x, M, K, down, r, T_out))
+        return rc;
+    if (M == 0)
+        return TASQ_OK;
+    if (K == 0) {       // no codes to write; the projection is zero
+        hipError_t e = tasq::launch_lowrank_down(x, M, K, down, r, T_out, nullptr, nullptr,
+                                                 static_cast<hipStream_t>(stream));
+        return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+    }
+    if (!X_out || !act_params)
+        return TASQ_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(act_params) & 3)
+        return TASQ_ERR_ALIGN;
+    hipError_t e = tasq::launch_quantize_activations_lowrank(
+        x, M, K, X_out, act_params, down, r, T_out, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
 }
 

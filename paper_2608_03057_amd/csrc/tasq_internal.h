@@ -18,8 +18,10 @@ struct LayerDesc {
     const int8_t *Wp;       // packed weights (MFMA operand order) or null
     const float *sw;        // [N]
     const float *bias;      // [N] or null
-    const float *act;       // asymmetric activation params [4] (alpha at 2, z at 3) or null
+    const float *act;       // asymmetric activation params (alpha at 0, z at 1) or null
     const int32_t *colsums; // [8][N] channel sums of W_b (with act)
+    const float *lr_T;      // low-rank branch x~ D^T, fp32 [M][lr_r], or null
+    const uint16_t *lr_U;   // its up projection, bfloat16 [N][lr_r]
     int32_t *acc;           // [M][N] or null
     float *y;               // [M][N] or null
     float sx;
@@ -27,6 +29,7 @@ struct LayerDesc {
     int32_t kind;
     int32_t H, Wd, C;
     int32_t bits;           // effective precision b (single calls)
+    int32_t lr_r;           // rank of the low-rank branch (16 or 32) when lr_T is set
     int32_t tiles_m, tiles_n;
     int32_t tile_begin;     // first tile of this layer in a grouped launch
 };
@@ -103,6 +106,17 @@ inline unsigned long long packed_weight_bytes_host(long long N, long long K)
 // [0] alpha, [1] z on completion, [kActHeader..] partial ranges.
 constexpr int kActHeader = 4;
 constexpr int kActPartials = 512;
+
+// Largest rank of the 16-bit low-rank branch the epilogues take.
+constexpr int kLowrankMaxRank = 32;
+// Down projection T = x~ D^T (act_quant.hip); with part set it also writes
+// the per-workgroup ranges of x that launch_quantize_activations folds.
+// Returns the number of workgroups (partial ranges) through *groups.
+hipError_t launch_lowrank_down(const float *x, int M, int K, const uint16_t *D, int r, float *T,
+                               uint32_t *part, int *groups, hipStream_t stream);
+hipError_t launch_quantize_activations_lowrank(const float *x, int M, int K, int8_t *q,
+                                               float *params, const uint16_t *D, int r, float *T,
+                                               hipStream_t stream);
 hipError_t launch_quantize_activations(const float *x, long long n, int8_t *q, float *params,
                                        hipStream_t stream);
 hipError_t launch_weight_colsums(const int8_t *W, int N, int K, int32_t *colsums,

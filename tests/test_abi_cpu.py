@@ -94,6 +94,11 @@ def opts(**kw):
     (dict(opts=opts(act_params=FAKE)), _lib.TASQ_ERR_NULL),
     (dict(opts=opts(act_params=FAKE + 2, colsums=FAKE)), _lib.TASQ_ERR_ALIGN),
     (dict(opts=opts(act_params=FAKE, colsums=FAKE + 1)), _lib.TASQ_ERR_ALIGN),
+    (dict(opts=opts(lowrank_T=FAKE, lowrank_rank=16)), _lib.TASQ_ERR_NULL),
+    (dict(opts=opts(lowrank_T=FAKE, lowrank_up=FAKE, lowrank_rank=24)), _lib.TASQ_ERR_DIM),
+    (dict(opts=opts(lowrank_T=FAKE, lowrank_up=FAKE, lowrank_rank=0)), _lib.TASQ_ERR_DIM),
+    (dict(opts=opts(lowrank_T=FAKE + 4, lowrank_up=FAKE, lowrank_rank=16)), _lib.TASQ_ERR_ALIGN),
+    (dict(opts=opts(lowrank_T=FAKE, lowrank_up=FAKE + 8, lowrank_rank=32)), _lib.TASQ_ERR_ALIGN),
 ])
 def test_masked_linear_rejects(kw, code):
     assert lin(**kw) == code
@@ -144,6 +149,26 @@ def test_quantize_activations_rejects():
     assert q(None, 0, 4, None, None, None) == _lib.TASQ_OK          # empty: nothing enqueued
 
 
+def test_lowrank_down_rejects():
+    f = L.tasq_lowrank_down
+    assert f(FAKE, 4, 4, FAKE, 24, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert f(FAKE, 4, 4, FAKE, 64, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert f(FAKE, -1, 4, FAKE, 16, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert f(None, 4, 4, FAKE, 16, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert f(FAKE, 4, 4, None, 16, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert f(FAKE, 4, 4, FAKE, 16, None, None) == _lib.TASQ_ERR_NULL
+    assert f(FAKE + 2, 4, 4, FAKE, 16, FAKE, None) == _lib.TASQ_ERR_ALIGN
+    assert f(FAKE, 4, 4, FAKE + 1, 16, FAKE, None) == _lib.TASQ_ERR_ALIGN
+    assert f(FAKE, 1 << 24, 4, FAKE, 32, FAKE, None) == _lib.TASQ_ERR_DIM   # M*r*4 >= 2^31
+    assert f(None, 0, 4, None, 16, None, None) == _lib.TASQ_OK
+    g = L.tasq_quantize_activations_lowrank
+    assert g(FAKE, 4, 4, None, FAKE, FAKE, 16, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert g(FAKE, 4, 4, FAKE, None, FAKE, 16, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert g(FAKE, 4, 4, FAKE, FAKE + 2, FAKE, 16, FAKE, None) == _lib.TASQ_ERR_ALIGN
+    assert g(FAKE, 4, 4, FAKE, FAKE, FAKE, 48, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert g(None, 0, 4, None, None, None, 32, None, None) == _lib.TASQ_OK
+
+
 def test_weight_colsums_rejects():
     c = L.tasq_weight_colsums
     assert c(None, 4, 4, FAKE, None) == _lib.TASQ_ERR_NULL
@@ -158,6 +183,11 @@ def test_schedule_asymmetric_layer_needs_colsums():
     conv = layer(kind=_lib.KIND_CONV3X3, H=2, Wd=2, C=16, M=4, K=144, act_params=FAKE,
                  colsums=FAKE)
     assert sched([layer(), conv], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_LAYOUT
+    conv_lr = layer(kind=_lib.KIND_CONV3X3, H=2, Wd=2, C=16, M=4, K=144, lowrank_T=FAKE,
+                    lowrank_up=FAKE, lowrank_rank=16)
+    assert sched([layer(), conv_lr], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_LAYOUT
+    assert sched([layer(lowrank_T=FAKE, lowrank_up=FAKE, lowrank_rank=32)] * 2, tbl, 4, 20,
+                 0, 0) == _lib.TASQ_OK
     assert sched([layer(), layer(act_params=FAKE)], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_NULL
     assert sched([layer(act_params=FAKE, colsums=FAKE + 2), layer()], tbl, 4, 20, 0, 1) \
         == _lib.TASQ_ERR_ALIGN
