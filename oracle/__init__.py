@@ -67,6 +67,12 @@ def lib():
                                                 i64, i64, i64, ctypes.c_int, p, p]
         L.oracle_masked_linear_asym_entries.argtypes = [p, p, ctypes.c_double, ctypes.c_double,
                                                         p, p, i64, ctypes.c_int, p, p, i64, p, p]
+        L.oracle_weight_quant.argtypes = [p, i64, i64, ctypes.c_int, p, p, p, p]
+        d = ctypes.c_double
+        L.oracle_layer_dequant.argtypes = [p, ctypes.c_int, d, d, d, p, p, p, p, i64, i64, i64,
+                                           ctypes.c_int, p, p]
+        L.oracle_layer_dequant_entries.argtypes = [p, ctypes.c_int, d, d, d, p, p, p, p, i64,
+                                                   ctypes.c_int, p, p, i64, p, p]
         _lib = L
     return _lib
 
@@ -291,6 +297,84 @@ def masked_linear_asym_entries(Q, W, alpha, z, sw, b, rows, cols, bias=None):
         raise OverflowError("accumulator outside int32")
     if rc != OK:
         raise ValueError(f"oracle_masked_linear_asym_entries rc={rc}")
+    return acc, y
+
+
+# ------------------------------------------------------ weight quantizer
+
+
+def weight_quant(W, nbits: int = 8):
+    """(Q uint8 [N x K], alpha [N], z [N], sw [N]) of fp32 W [N x K]: the
+    per-channel n-bit weight quantizer of App. A.1.1 (floor, 2^n grid, real
+    zero point), sw = alpha 2^n / (2^n - 1) the dequantisation factor."""
+    W = _np(W, np.float32)
+    N = W.shape[0]
+    K = W.size // N if N else 0
+    Q = np.empty((N, K), np.uint8)
+    alpha = np.empty(N, np.float32)
+    z = np.empty(N, np.float32)
+    sw = np.empty(N, np.float32)
+    rc = lib().oracle_weight_quant(_ptr(W), N, K, nbits, _ptr(Q), _ptr(alpha), _ptr(z), _ptr(sw))
+    if rc != OK:
+        raise ValueError(f"oracle_weight_quant rc={rc}")
+    return Q, alpha, z, sw
+
+
+def row_sums(X) -> np.ndarray:
+    """int64 [M]: sum_k X[m][k] of int8 codes (the weight zero point's term)."""
+    return np.asarray(X).astype(np.int64).reshape(np.asarray(X).shape[0], -1).sum(axis=1)
+
+
+def _layer_args(act, sx):
+    if act is None:
+        return 0, float(sx), 0.0, 0.0
+    ax, zx = act
+    return 1, 0.0, float(ax), float(zx)
+
+
+def layer_dequant(X, W, sw, b: int, sx: float = 0.0, act=None, zw=None, bias=None):
+    """(acc int32, y fp64) of sum_k x_hat w_hat_b (+ bias): x_hat = sx X, or
+    alpha (X + 128 - z) with act = (alpha, z); w_hat_b = sw W_b, or
+    sw (W_b + 128 - zw[n]) with per-channel zero points zw."""
+    X = _np(X, np.int8)
+    W = _np(W, np.int8)
+    sw = _np(sw, np.float32)
+    zw = None if zw is None else _np(zw, np.float32)
+    bias = None if bias is None else _np(bias, np.float32)
+    M, K = X.shape
+    N = W.shape[0]
+    acc = np.empty((M, N), np.int32)
+    y = np.empty((M, N), np.float64)
+    asym, sxv, ax, zx = _layer_args(act, sx)
+    rc = lib().oracle_layer_dequant(_ptr(X), asym, sxv, ax, zx, _ptr(W), _ptr(sw), _ptr(zw),
+                                    _ptr(bias), M, N, K, b, _ptr(acc), _ptr(y))
+    if rc == EOVERFLOW:
+        raise OverflowError("accumulator outside int32")
+    if rc != OK:
+        raise ValueError(f"oracle_layer_dequant rc={rc}")
+    return acc, y
+
+
+def layer_dequant_entries(X, W, sw, b, rows, cols, sx=0.0, act=None, zw=None, bias=None):
+    """The (rows[i], cols[i]) outputs of layer_dequant."""
+    X = _np(X, np.int8)
+    W = _np(W, np.int8)
+    sw = _np(sw, np.float32)
+    zw = None if zw is None else _np(zw, np.float32)
+    bias = None if bias is None else _np(bias, np.float32)
+    rows = _np(rows, np.int64)
+    cols = _np(cols, np.int64)
+    K = X.shape[1]
+    acc = np.empty(rows.size, np.int32)
+    y = np.empty(rows.size, np.float64)
+    asym, sxv, ax, zx = _layer_args(act, sx)
+    rc = lib().oracle_layer_dequant_entries(_ptr(X), asym, sxv, ax, zx, _ptr(W), _ptr(sw),
+                                            _ptr(zw), _ptr(bias), K, b, _ptr(rows), _ptr(cols),
+                                            rows.size, _ptr(acc), _ptr(y))
+    if rc == EOVERFLOW:
+        raise OverflowError("accumulator outside int32")
+    if rc != OK:
+        raise ValueError(f"oracle_layer_dequant_entries rc={rc}")
     return acc, y
 
 

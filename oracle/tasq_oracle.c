@@ -434,3 +434,140 @@ int oracle_masked_linear_asym_entries(const uint8_t *Q, const int8_t *W, double 
     }
     return overflow ? ORACLE_EOVERFLOW : ORACLE_OK;
 }
+
+/*
+ * Weight quantizer of App. A.1.1 (Eqs. weight_quant, weight_scale,
+ * weight_dequant), n bits, one scale and zero point per output channel
+ * (row of W [N][K]):
+ *   alpha = (max(w) - min(w)) / 2^n,   z = -min(w) / alpha,
+ *   Q = clamp(floor(w / alpha + z), 0, 2^n - 1),
+ *   w_hat = 2^n / (2^n - 1) * alpha * (Q - z),
+ * and sw = alpha * 2^n / (2^n - 1), the per-channel factor of w_hat, so that
+ * w_hat = sw * (Q - z).  Each operation is one IEEE single-precision
+ * operation in this order, as for the activation quantizer; sw is
+ * (alpha * 2^n) / (2^n - 1), the product exact.  A constant row takes
+ * alpha = 1, z = -min (every code 0).  W must be finite.
+ */
+int oracle_weight_quant(const float *W, int64_t N, int64_t K, int nbits, uint8_t *Q,
+                        float *alpha_out, float *z_out, float *sw_out)
+{
+    if (N < 0 || K <= 0 || nbits < 1 || nbits > 8)
+        return ORACLE_EDIM;
+    const float levels = (float)(1 << nbits);
+    const float top = levels - 1.0f;
+    for (int64_t n = 0; n < N; ++n) {
+        const float *w = W + n * K;
+        float mn = w[0], mx = w[0];
+        for (int64_t k = 1; k < K; ++k) {
+            if (w[k] < mn)
+                mn = w[k];
+            if (w[k] > mx)
+                mx = w[k];
+        }
+        float alpha, z;
+        if (mx == mn) {
+            alpha = 1.0f;
+            z = -mn;
+        } else {
+            float range = mx - mn;
+            alpha = range / levels;
+            z = -mn / alpha;
+        }
+        for (int64_t k = 0; k < K; ++k) {
+            float t = w[k] / alpha;
+            t = t + z;
+            float f = floorf(t);
+            if (f < 0.0f)
+                f = 0.0f;
+            if (f > top)
+                f = top;
+            Q[n * K + k] = (uint8_t)f;
+        }
+        float scaled = alpha * levels;
+        alpha_out[n] = alpha;
+        z_out[n] = z;
+        sw_out[n] = scaled / top;
+    }
+    return ORACLE_OK;
+}
+
+/*
+ * The layer with both operands dequantised (App. A.1), in fp64 from the
+ * definitions, summed in ascending k:
+ *   y[m][n] = sum_k x_hat[m][k] * w_hat_b[n][k]  (+ bias[n]),
+ *   x_hat = sx * X                     (symmetric codes X, asym_x = 0), or
+ *   x_hat = ax * ((X + 128) - zx)      (asymmetric codes Q = X + 128),
+ *   w_hat_b = sw[n] * W_b              (zw == NULL: zero point 0), or
+ *   w_hat_b = sw[n] * ((W_b + 128) - zw[n])   (the masked code Q_b = W_b + 128
+ *                                              with the channel's real zero point);
+ *   acc[m][n] = sum_k X[m][k] * W_b[n][k]  int32, the product of the signed
+ *   codes the int8 matrix instruction consumes.
+ * X, W int8 signed codes; other arguments as oracle_masked_linear.
+ */
+static double xhat_of(int8_t x, int asym_x, double sx, double ax, double zx)
+{
+    return asym_x ? ax * (((double)x + 128.0) - zx) : sx * (double)x;
+}
+
+int oracle_layer_dequant(const int8_t *X, int asym_x, double sx, double ax, double zx,
+                         const int8_t *W, const float *sw, const float *zw, const float *bias,
+                         int64_t M, int64_t N, int64_t K, int b, int32_t *acc, double *y)
+{
+    if (b < 1 || b > 8)
+        return ORACLE_EBITS;
+    if (M < 0 || N < 0 || K < 0)
+        return ORACLE_EDIM;
+    int overflow = 0;
+#pragma omp parallel for schedule(static) reduction(| : overflow)
+    for (int64_t m = 0; m < M; ++m) {
+        for (int64_t n = 0; n < N; ++n) {
+            int64_t s = 0;
+            double v = 0.0;
+            for (int64_t k = 0; k < K; ++k) {
+                const int64_t wb = masked_value(W[n * K + k], b);
+                const int8_t x = X[m * K + k];
+                s += (int64_t)x * wb;
+                const double what = zw ? (double)sw[n] * (((double)wb + 128.0) - (double)zw[n])
+                                       : (double)sw[n] * (double)wb;
+                v += xhat_of(x, asym_x, sx, ax, zx) * what;
+            }
+            if (s >= ((int64_t)1 << 31) || s < -((int64_t)1 << 31))
+                overflow = 1;
+            if (acc)
+                acc[m * N + n] = (int32_t)s;
+            if (y)
+                y[m * N + n] = v + (bias ? (double)bias[n] : 0.0);
+        }
+    }
+    return overflow ? ORACLE_EOVERFLOW : ORACLE_OK;
+}
+
+/* Entries (rows[i], cols[i]) of oracle_layer_dequant. */
+int oracle_layer_dequant_entries(const int8_t *X, int asym_x, double sx, double ax, double zx,
+                                 const int8_t *W, const float *sw, const float *zw,
+                                 const float *bias, int64_t K, int b, const int64_t *rows,
+                                 const int64_t *cols, int64_t count, int32_t *acc, double *y)
+{
+    if (b < 1 || b > 8)
+        return ORACLE_EBITS;
+    int overflow = 0;
+#pragma omp parallel for schedule(static) reduction(| : overflow)
+    for (int64_t i = 0; i < count; ++i) {
+        const int64_t m = rows[i], n = cols[i];
+        int64_t s = 0;
+        double v = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+            const int64_t wb = masked_value(W[n * K + k], b);
+            const int8_t x = X[m * K + k];
+            s += (int64_t)x * wb;
+            const double what = zw ? (double)sw[n] * (((double)wb + 128.0) - (double)zw[n])
+                                   : (double)sw[n] * (double)wb;
+            v += xhat_of(x, asym_x, sx, ax, zx) * what;
+        }
+        if (s >= ((int64_t)1 << 31) || s < -((int64_t)1 << 31))
+            overflow = 1;
+        acc[i] = (int32_t)s;
+        y[i] = v + (bias ? (double)bias[n] : 0.0);
+    }
+    return overflow ? ORACLE_EOVERFLOW : ORACLE_OK;
+}

@@ -273,6 +273,17 @@ def activations_f32(seed: int, rows, K: int, shape: str = "outlier") -> torch.Te
     raise ValueError(shape)
 
 
+def weights_f32(seed: int, N: int, K: int) -> torch.Tensor:
+    """fp32 [N x K] real-valued weights for the weight quantizer: N(0, 1)
+    scaled per output channel by sigma_n ~ U[0.01, 0.05) and shifted by
+    mu_n ~ U[-0.005, 0.005) (channels of different spread and a small
+    offset, so that per-channel zero points differ from the centre)."""
+    z = _draw_rows(torch.arange(N), K, "cpu", torch.float32, lambda idx: normal_f32(seed, 6, idx))
+    sigma = uniform_f32(seed, 7, torch.arange(N), 0.01, 0.05).reshape(N, 1)
+    mu = uniform_f32(seed, 8, torch.arange(N), -0.005, 0.005).reshape(N, 1)
+    return z * sigma + mu
+
+
 def bf16_bits(seed: int, tid: int, shape, emin: int = -9, emax: int = -3) -> torch.Tensor:
     """int16 [shape] bit patterns of random bfloat16 values: a uniform sign,
     a uniform exponent in [emin, emax] and a uniform 7-bit mantissa, i.e.

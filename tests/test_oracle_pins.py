@@ -638,3 +638,130 @@ def test_lowrank_entries_match_full():
     rows, cols = rng.integers(0, 11, 50), rng.integers(0, 21, 50)
     e = oracle.lowrank_entries(x, D, U, rows, cols)
     assert np.allclose(e, lr[rows, cols], rtol=1e-13, atol=0)
+
+
+# ------------------------------------------------------ weight quantizer
+
+def test_weight_quant_exact_grid_and_clamp():
+    """A row on the grid min + j alpha (alpha = 2/256 exactly): code j, the
+    midpoints floor to j, and max (j = 256) clamps to 255."""
+    j = np.arange(257)
+    on = np.concatenate([-1.0 + j / 128.0, [0.0]]).astype(np.float32)
+    mid = np.concatenate([[-1.0], -1.0 + (np.arange(256) + 0.5) / 128.0, [1.0]])
+    W = np.stack([on, mid.astype(np.float32)])
+    Q, alpha, z, sw = oracle.weight_quant(W)
+    assert alpha.tolist() == [2.0 ** -7] * 2 and z.tolist() == [128.0] * 2
+    assert Q[0].tolist() == np.minimum(j, 255).tolist() + [128]
+    assert Q[1, 1:257].tolist() == list(range(256)) and Q[1, 0] == 0 and Q[1, 257] == 255
+    assert sw[0] == np.float32(np.float32(2.0 ** -7 * 256) / np.float32(255.0))
+
+
+def test_weight_quant_truncquant_prefix():
+    """Eq. truncquant: the (n-1)-bit code is the n-bit code without its LSB,
+    for every n, so masking the stored 8-bit code reproduces the coarser
+    quantizers; for weights normalised to [0, 1] the 8-bit code is
+    floor(256 w) (the printed Q_n = floor(W 2^n), clamped at w = 1)."""
+    rng = np.random.default_rng(21)
+    W = rng.standard_normal((6, 500)).astype(np.float32)
+    Q8 = oracle.weight_quant(W, 8)[0].astype(np.int64)
+    for n in range(1, 8):
+        Qn = oracle.weight_quant(W, n)[0].astype(np.int64)
+        assert np.array_equal(Qn, Q8 >> (8 - n)), n
+    u = (rng.integers(0, 4097, (3, 300)) / 4096.0).astype(np.float32)
+    u[:, 0], u[:, 1] = 0.0, 1.0
+    Qu = oracle.weight_quant(u, 8)[0].astype(np.int64)
+    assert np.array_equal(Qu, np.minimum(np.floor(u.astype(np.float64) * 256), 255))
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_weight_quant_properties(seed):
+    rng = np.random.default_rng(seed)
+    W = (rng.standard_normal((9, 777)) * rng.uniform(0.01, 3.0, (9, 1))
+         + rng.uniform(-2, 2, (9, 1))).astype(np.float32)
+    Q, alpha, z, sw = oracle.weight_quant(W)
+    for n in range(9):
+        assert Q[n, W[n].argmin()] == 0 and Q[n, W[n].argmax()] == 255
+        order = np.argsort(W[n], kind="stable")
+        assert np.all(np.diff(Q[n, order].astype(int)) >= 0)
+        # floor: alpha (Q - z) <= w < alpha (Q + 1 - z), up to fp32 slack
+        a, zz = float(alpha[n]), float(z[n])
+        w = W[n].astype(np.float64)
+        lo = a * (Q[n] - zz)
+        slack = 8 * 2.0 ** -24 * (np.abs(w) + a * (abs(zz) + 256))
+        assert np.all(lo <= w + slack) and np.all(w < lo + a + slack)
+        assert abs(float(sw[n]) - a * 256 / 255) <= 2.0 ** -23 * a
+
+
+def test_weight_quant_constant_row():
+    Q, alpha, z, sw = oracle.weight_quant(np.full((2, 5), -0.5, np.float32))
+    assert not Q.any() and alpha.tolist() == [1.0, 1.0] and z.tolist() == [0.5, 0.5]
+
+
+def test_row_sums():
+    X = rand_i8((5, 37))
+    assert oracle.row_sums(X).tolist() == [sum(int(v) for v in row) for row in X]
+
+
+@pytest.mark.parametrize("b", [8, 5, 1])
+def test_layer_dequant_reduces_to_masked_linear(b):
+    X, W = rand_i8((11, 90)), rand_i8((13, 90))
+    sw = RNG.uniform(1e-3, 1e-2, 13).astype(np.float32)
+    acc, y = oracle.layer_dequant(X, W, sw, b, sx=0.02)
+    ra, ry = oracle.masked_linear(X, W, 0.02, sw, b)
+    assert np.array_equal(acc, ra)
+    mag = 0.02 * (np.abs(X.astype(np.float64)) @ np.abs(oracle.mask(W, b).astype(np.float64)).T
+                  ) * sw.astype(np.float64)
+    assert np.all(np.abs(y - ry) <= 1e-13 * mag)
+
+
+@pytest.mark.parametrize("b", [8, 6, 3])
+def test_layer_dequant_factored_zero_points(b):
+    """sum_k x_hat w_hat_b against the expanded form through numpy's int64
+    matmul: symmetric activations give sx sw (acc + (128 - zw) rowsum(X));
+    asymmetric ones add (128 - zx) colsum_b and K (128 - zx)(128 - zw)."""
+    X, W = rand_i8((7, 150)), rand_i8((9, 150))
+    sw = RNG.uniform(1e-3, 1e-2, 9).astype(np.float32)
+    zw = RNG.uniform(60, 190, 9).astype(np.float32)
+    Wb = oracle.mask(W, b).astype(np.int64)
+    acc = X.astype(np.int64) @ Wb.T
+    rs = X.astype(np.int64).sum(1)[:, None]
+    cs = Wb.sum(1)[None, :]
+    swd, zwd = sw.astype(np.float64), zw.astype(np.float64)
+    a1, y1 = oracle.layer_dequant(X, W, sw, b, sx=0.02, zw=zw)
+    e1 = 0.02 * swd * (acc + (128.0 - zwd) * rs)
+    assert np.array_equal(a1, acc)
+    assert np.all(np.abs(y1 - e1) <= 1e-12 * (np.abs(0.02 * swd) * (np.abs(acc) + np.abs(
+        (128 - zwd) * rs))))
+    ax, zx = 0.031, 97.25
+    a2, y2 = oracle.layer_dequant(X, W, sw, b, act=(ax, zx), zw=zw)
+    e2 = ax * swd * (acc + (128 - zx) * cs + (128.0 - zwd) * (rs + 150 * (128 - zx)))
+    mag = ax * swd * (np.abs(acc) + np.abs((128 - zx) * cs) + np.abs((128 - zwd) * rs)
+                      + 150 * np.abs((128 - zx) * (128 - zwd)))
+    assert np.all(np.abs(y2 - e2) <= 1e-12 * mag)
+
+
+def test_layer_dequant_exact_rational_tiny():
+    X, W = rand_i8((2, 5)), rand_i8((3, 5))
+    sw = np.array([0.25, 0.5, 0.125], np.float32)
+    zw = np.array([100.5, 130.0, 77.25], np.float32)
+    acc, y = oracle.layer_dequant(X, W, sw, 4, act=(0.5, 3.75), zw=zw)
+    Wb = oracle.mask(W, 4)
+    for m in range(2):
+        for n in range(3):
+            e = sum((Fraction(1, 2) * (int(X[m, k]) + 128 - Fraction(15, 4)))
+                    * (Fraction(float(sw[n])) * (int(Wb[n, k]) + 128 - Fraction(float(zw[n]))))
+                    for k in range(5))
+            assert Fraction(y[m, n]) == e
+
+
+def test_layer_dequant_entries_match_full():
+    X, W = rand_i8((9, 64)), rand_i8((10, 64))
+    sw = RNG.uniform(1e-3, 1e-2, 10).astype(np.float32)
+    zw = RNG.uniform(0, 255, 10).astype(np.float32)
+    bias = RNG.uniform(-1, 1, 10).astype(np.float32)
+    acc, y = oracle.layer_dequant(X, W, sw, 6, act=(0.02, 130.5), zw=zw, bias=bias)
+    rows, cols = RNG.integers(0, 9, 30), RNG.integers(0, 10, 30)
+    ae, ye = oracle.layer_dequant_entries(X, W, sw, 6, rows, cols, act=(0.02, 130.5), zw=zw,
+                                          bias=bias)
+    assert np.array_equal(ae, acc[rows, cols])
+    assert np.allclose(ye, y[rows, cols], rtol=1e-13, atol=0)
