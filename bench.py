@@ -238,7 +238,8 @@ def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
     quantizer, the grouped launch and both, and the quantizer's HBM roofline
     (algorithmic bytes: 4 read + 1 written per element, plus 4 per element of
     the projection with the branch)."""
-    xs, codes, Ts, plain, lowrank, hold = [], [], [], [], [], []
+    xs, codes, Ts, plain, lowrank, wzero, hold = [], [], [], [], [], [], []
+    rsums = []
     params = torch.empty((len(wl.layers), T.TASQ_ACT_PARAMS_FLOATS), dtype=torch.float32,
                          device=device)
     gen = torch.Generator(device=device)
@@ -256,27 +257,36 @@ def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
         q = torch.empty((spec.M, spec.K), dtype=torch.int8, device=device)
         Tl = torch.empty((spec.M, rank), dtype=torch.float32, device=device)
         cs = T.weight_colsums(W)
+        zw = 128.0 + 8.0 * torch.randn(spec.N, generator=gen, device=device)
+        rs = torch.empty(spec.M, dtype=torch.int32, device=device)
+        rsums.append(rs)
         xs.append((x, down))
         codes.append(q)
         Ts.append(Tl)
-        hold += [cs, up]
+        hold += [cs, up, zw]
         plain.append(T.make_layer(q, W, 0.0, sw, None, None, y, act=params[l], colsums=cs))
         lowrank.append(T.make_layer(q, W, 0.0, sw, None, None, y, act=params[l], colsums=cs,
                                     lowrank=(Tl, up)))
+        wzero.append(T.make_layer(q, W, 0.0, sw, None, None, y, act=params[l], colsums=cs,
+                                  wzero=(zw, rs)))
     torch.cuda.synchronize()
 
-    def quantize_all(with_lr):
+    def quantize_all(kind):
         for l, (x, down) in enumerate(xs):
-            if with_lr:
+            if kind == "lowrank":
                 T.quantize_activations_lowrank(x, down, out=codes[l], params=params[l], T=Ts[l])
             else:
                 T.quantize_activations(x, out=codes[l], params=params[l])
+            if kind == "wzero":
+                T.row_sums(codes[l], out=rsums[l])
 
     ev = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
     elems = sum(float(s.M * s.K) for s in wl.layers)
     out = {}
-    for name, layers, with_lr in (("plain", plain, False), (f"lowrank_r{rank}", lowrank, True)):
-        quantize_all(with_lr)
+    for name, layers, kind in (("plain", plain, "plain"), (f"lowrank_r{rank}", lowrank, "lowrank"),
+                               ("zero_point_weights", wzero, "wzero")):
+        with_lr = kind == "lowrank"
+        quantize_all(kind)
         T.run_schedule(layers, table, wl.S, wl.T, 0, 1, workspace=ws)
         torch.cuda.synchronize()
         q_ms, g_ms = [], []
@@ -286,7 +296,7 @@ def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
             for t in range(wl.T):
                 e0, e1, e2 = ev(), ev(), ev()
                 e0.record()
-                quantize_all(with_lr)
+                quantize_all(kind)
                 e1.record()
                 T.run_schedule(layers, table, wl.S, wl.T, t, t + 1, workspace=ws)
                 e2.record()
@@ -297,6 +307,8 @@ def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
         qm = float(np.mean([a.elapsed_time(b) for a, b in q_ms]))
         gm = float(np.mean([a.elapsed_time(b) for a, b in g_ms]))
         alg = 5.0 * elems + (4.0 * rank * sum(float(s.M) for s in wl.layers) if with_lr else 0)
+        if kind == "wzero":            # the row sums read the codes once more
+            alg += elems + 4.0 * sum(float(s.M) for s in wl.layers)
         ach = alg / (qm * 1e-3) / 1e9
         out[name] = {
             "ms_per_denoising_step": round(a0.elapsed_time(a1) / reps / wl.T, 4),
@@ -304,9 +316,38 @@ def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
             "quantizer_roofline": {
                 "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(ach / PEAK_HBM_GBS, 4), "algorithmic_bytes": alg,
-                "kernels": ("k_lowrank_down<true>, k_act_quantize per layer" if with_lr
-                            else "k_act_range, k_act_quantize per layer")}}
+                "kernels": {"plain": "k_act_range, k_act_quantize per layer",
+                            "lowrank": "k_lowrank_down<true>, k_act_quantize per layer",
+                            "wzero": "k_act_range, k_act_quantize, k_row_sums per layer"}[kind]}}
     return out
+
+
+def weight_quantizer(wl, device, reps=3):
+    """The offline step before the weight buffer exists: the per-channel
+    weight quantizer over the fp32 weights of all 112 layers (seeded normal
+    draws, per-channel spread).  Milliseconds per pass and its HBM roofline
+    (algorithmic bytes: 4 read + 1 written per weight)."""
+    gen = torch.Generator(device=device)
+    Ws = []
+    for l, spec in enumerate(wl.layers):
+        gen.manual_seed(wl.seed * 7000 + l)
+        Ws.append(0.03 * torch.randn((spec.N, spec.K), generator=gen, device=device))
+    T.quantize_weights(Ws[0])
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        for W in Ws:
+            T.quantize_weights(W)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    elems = sum(float(s.N * s.K) for s in wl.layers)
+    ach = 5.0 * elems / (ms * 1e-3) / 1e9
+    return {"ms_all_layers": round(ms, 4), "weights": elems,
+            "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                         "algorithmic_bytes": 5.0 * elems, "kernel": "k_weight_quantize"}}
 
 
 def cpu_baseline(wl, table, budget_s=15.0):
@@ -426,10 +467,12 @@ def main():
         log("timing the weight-streaming schedule at M=16")
         skinny = skinny_schedule(wl, table, keep, dev)
 
-    act = None
+    act = wq = None
     if not args.no_act and not args.per_layer:
         log("timing the asymmetric-activation schedule")
         act = act_schedule(wl, table, keep, ws, dev)
+        log("timing the weight quantizer")
+        wq = weight_quantizer(wl, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -452,6 +495,7 @@ def main():
         "roofline": roof,
         "skinny_schedule": skinny,
         "asymmetric_activations": act,
+        "weight_quantizer": wq,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -119,6 +119,17 @@ enum {
  *   lowrank_rank    16 or 32 (TASQ_ERR_DIM otherwise).  lowrank_T and
  *                   lowrank_up must be 16-byte aligned (TASQ_ERR_ALIGN);
  *                   linear layers only (TASQ_ERR_LAYOUT on a conv).
+ *   w_zero          device fp32 [N] per-channel weight zero points from
+ *                   tasq_quantize_weights, or NULL (zero points 0).  When
+ *                   given, W holds the codes Q - 128 of App. A.1.1, sw the
+ *                   factor 256/255 alpha, and the masked weight dequantises
+ *                   to sw[n] (W_b + 128 - w_zero[n]), so y gains
+ *                   scale * (128 - w_zero[n]) * R[m] inside the dequantised
+ *                   sum, R[m] = x_rowsums[m] (+ K (128 - z) with
+ *                   act_params).  acc is unchanged.
+ *   x_rowsums       device int32 [M] from tasq_row_sums of X; required with
+ *                   w_zero.  Both 4-byte aligned (TASQ_ERR_ALIGN); linear
+ *                   layers only (TASQ_ERR_LAYOUT on a conv).
  */
 typedef struct tasq_opts {
     int32_t variant;
@@ -132,6 +143,8 @@ typedef struct tasq_opts {
     const float *lowrank_T;
     const uint16_t *lowrank_up;
     int32_t lowrank_rank;
+    const float *w_zero;
+    const int32_t *x_rowsums;
 } tasq_opts;
 
 /*
@@ -246,6 +259,34 @@ int tasq_quantize_activations(const float *x, int M, int K, int8_t *X_out, float
 int tasq_weight_colsums(const int8_t *W, int N, int K, int32_t *colsums_out, void *stream);
 
 /*
+ * Offline weight quantizer (App. A.1.1, Eqs. weight_quant, weight_scale,
+ * weight_dequant) at the stored precision n = 8, per output channel:
+ *   alpha = (max - min) / 256,  z = -min / alpha (kept real),
+ *   Q = clamp(floor(w / alpha + z), 0, 255),  W_out = Q - 128,
+ *   sw = alpha * 256 / 255, so that w_hat = sw * (Q - z).
+ * Decided in IEEE single precision (correctly rounded division, then
+ * addition, then floor); a constant row takes alpha = 1, z = -min.  The
+ * 2^n grid makes every lower precision a prefix of the stored code (Eq.
+ * truncquant), so W_out is the shared buffer of every stage as it is.
+ *   W        fp32 [N][K] device, finite, 4-byte aligned.
+ *   W_out    int8 [N][K] device: the codes, for tasq_masked_linear and the
+ *            packers.
+ *   alpha_out, z_out, sw_out  fp32 [N] device (z_out is the w_zero and
+ *            sw_out the sw of tasq_masked_linear).
+ * N == 0 enqueues nothing.  Errors: TASQ_ERR_NULL, _DIM (negative sizes,
+ * K == 0 with N > 0), _OVERFLOW (K > TASQ_MAX_K), _ALIGN, _HIP.
+ */
+int tasq_quantize_weights(const float *W, int N, int K, int8_t *W_out, float *alpha_out,
+                          float *z_out, float *sw_out, void *stream);
+
+/*
+ * Row sums of int8 activation codes, out[m] = sum_k X[m][k] (int32 [M]),
+ * the x_rowsums that a weight zero point needs.  M == 0 enqueues nothing.
+ * Errors: TASQ_ERR_NULL, _DIM, _OVERFLOW (K > TASQ_MAX_K), _HIP.
+ */
+int tasq_row_sums(const int8_t *X, int M, int K, int32_t *out, void *stream);
+
+/*
  * Down projection of the 16-bit low-rank branch (Sec. 4.1 setup: a frozen
  * rank-16 or rank-32 branch beside the quantized weight):
  *   T[m][j] = sum_k bf16(x[m][k]) * down[j][k],
@@ -300,6 +341,8 @@ typedef struct tasq_layer {
     const float *lowrank_T;     /* low-rank branch (see tasq_opts) or NULL */
     const uint16_t *lowrank_up;
     int32_t lowrank_rank;
+    const float *w_zero;        /* weight zero points (see tasq_opts) or NULL */
+    const int32_t *x_rowsums;
 } tasq_layer;
 
 /*

@@ -40,6 +40,7 @@ EXPORTS = (
     "tasq_masked_linear", "tasq_masked_conv3x3", "tasq_pack_planes", "tasq_planes_bytes",
     "tasq_pack_weights", "tasq_packed_weight_bytes", "tasq_quantize_activations",
     "tasq_weight_colsums", "tasq_lowrank_down", "tasq_quantize_activations_lowrank",
+    "tasq_quantize_weights", "tasq_row_sums",
     "tasq_stage_of_step", "tasq_run_schedule",
     "tasq_workspace_bytes", "tasq_schedule_workspace_bytes", "tasq_status_string",
 )
@@ -51,7 +52,8 @@ class Opts(ctypes.Structure):
                 ("workspace_bytes", ctypes.c_size_t), ("W_packed", ctypes.c_void_p),
                 ("act_params", ctypes.c_void_p), ("colsums", ctypes.c_void_p),
                 ("lowrank_T", ctypes.c_void_p), ("lowrank_up", ctypes.c_void_p),
-                ("lowrank_rank", ctypes.c_int32)]
+                ("lowrank_rank", ctypes.c_int32), ("w_zero", ctypes.c_void_p),
+                ("x_rowsums", ctypes.c_void_p)]
 
 
 class Layer(ctypes.Structure):
@@ -63,7 +65,8 @@ class Layer(ctypes.Structure):
                 ("y", ctypes.c_void_p), ("W_packed", ctypes.c_void_p),
                 ("act_params", ctypes.c_void_p), ("colsums", ctypes.c_void_p),
                 ("lowrank_T", ctypes.c_void_p), ("lowrank_up", ctypes.c_void_p),
-                ("lowrank_rank", ctypes.c_int32)]
+                ("lowrank_rank", ctypes.c_int32), ("w_zero", ctypes.c_void_p),
+                ("x_rowsums", ctypes.c_void_p)]
 
 
 class TasqError(RuntimeError):
@@ -100,6 +103,10 @@ def lib() -> ctypes.CDLL:
         L.tasq_quantize_activations.restype = i32
         L.tasq_weight_colsums.argtypes = [vp, i32, i32, vp, vp]
         L.tasq_weight_colsums.restype = i32
+        L.tasq_quantize_weights.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp]
+        L.tasq_quantize_weights.restype = i32
+        L.tasq_row_sums.argtypes = [vp, i32, i32, vp, vp]
+        L.tasq_row_sums.restype = i32
         L.tasq_lowrank_down.argtypes = [vp, i32, i32, vp, i32, vp, vp]
         L.tasq_lowrank_down.restype = i32
         L.tasq_quantize_activations_lowrank.argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp]

@@ -38,7 +38,7 @@ def _need(t: Optional[torch.Tensor], dtype, shape, name):
 
 
 def _opts(variant, planes, workspace, split_k, packed=None, act=None, colsums=None,
-          lowrank=None) -> Opts:
+          lowrank=None, wzero=None) -> Opts:
     o = Opts()
     o.variant = variant
     o.split_k = split_k
@@ -50,6 +50,8 @@ def _opts(variant, planes, workspace, split_k, packed=None, act=None, colsums=No
     o.colsums = _ptr(colsums)
     if lowrank is not None:
         o.lowrank_T, o.lowrank_up, o.lowrank_rank = _lowrank_fields(lowrank)
+    if wzero is not None:
+        o.w_zero, o.x_rowsums = _ptr(wzero[0]), _ptr(wzero[1])
     return o
 
 
@@ -130,6 +132,32 @@ def quantize_activations(x: torch.Tensor, out: Optional[torch.Tensor] = None,
     return out, params
 
 
+def quantize_weights(W: torch.Tensor):
+    """(codes int8 [N, ...], alpha, z, sw fp32 [N]) of fp32 weights W
+    [N, ...]: the per-channel 8-bit quantizer of App. A.1.1; z is the
+    w_zero and sw the sw of masked_linear."""
+    N = W.shape[0]
+    K = W.numel() // N if N else 0
+    _need(W, torch.float32, tuple(W.shape), "W")
+    Q = torch.empty(W.shape, dtype=torch.int8, device=W.device)
+    alpha, z, sw = (torch.empty(N, dtype=torch.float32, device=W.device) for _ in range(3))
+    check(_lib.lib().tasq_quantize_weights(_ptr(W), N, K, _ptr(Q), _ptr(alpha), _ptr(z),
+                                           _ptr(sw), _stream()), "tasq_quantize_weights")
+    return Q, alpha, z, sw
+
+
+def row_sums(X: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """int32 [M]: sum_k X[m, k] of int8 codes X [M, K]."""
+    M = X.shape[0]
+    K = X.numel() // M if M else 0
+    _need(X, torch.int8, tuple(X.shape), "X")
+    if out is None:
+        out = torch.empty(M, dtype=torch.int32, device=X.device)
+    _need(out, torch.int32, (M,), "out")
+    check(_lib.lib().tasq_row_sums(_ptr(X), M, K, _ptr(out), _stream()), "tasq_row_sums")
+    return out
+
+
 def lowrank_down(x: torch.Tensor, down: torch.Tensor, out: Optional[torch.Tensor] = None):
     """T = bf16(x) down^T, fp32 [M, r], of fp32 x [M, K] and a bfloat16 (or
     int16 bit-pattern) down projection [r, K]."""
@@ -192,12 +220,13 @@ def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: tor
                   planes: Optional[torch.Tensor] = None, packed: Optional[torch.Tensor] = None,
                   workspace: Optional[torch.Tensor] = None, split_k: int = 0,
                   act: Optional[torch.Tensor] = None, colsums: Optional[torch.Tensor] = None,
-                  lowrank=None):
+                  lowrank=None, wzero=None):
     """(acc int32 [M, N] or None, y fp32 [M, N] or None) of the masked layer.
     With ``act`` (params of quantize_activations) and ``colsums`` X holds
     asymmetric activation codes and sx is ignored.  ``lowrank`` = (T, up)
     adds the low-rank branch T up^T to y (T from lowrank_down, up bfloat16
-    [N, r])."""
+    [N, r]).  ``wzero`` = (z_w fp32 [N], row sums int32 [M]) takes W as
+    zero-pointed codes (quantize_weights)."""
     M, K = X.shape
     N = sw.shape[0]
     _need(X, torch.int8, (M, K), "X")
@@ -216,7 +245,7 @@ def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: tor
         if wb:
             workspace = torch.empty(wb, dtype=torch.uint8, device=X.device)
     _need(colsums, torch.int32, (8, N), "colsums")
-    o = _opts(variant, planes, workspace, split_k, packed, act, colsums, lowrank)
+    o = _opts(variant, planes, workspace, split_k, packed, act, colsums, lowrank, wzero)
     rc = _lib.lib().tasq_masked_linear(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias), M, N,
                                        K, int(b), _ptr(acc), _ptr(y), ctypes.byref(o), _stream())
     check(rc, "tasq_masked_linear")
@@ -250,7 +279,7 @@ def masked_conv3x3(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: to
 
 
 def make_layer(X, W, sx, sw, bias=None, acc=None, y=None, planes=None, kind=None,
-               packed=None, act=None, colsums=None, lowrank=None) -> Layer:
+               packed=None, act=None, colsums=None, lowrank=None, wzero=None) -> Layer:
     """A tasq_layer for run_schedule; tensors must stay alive while in use."""
     L = Layer()
     if kind is None:
@@ -271,6 +300,8 @@ def make_layer(X, W, sx, sw, bias=None, acc=None, y=None, planes=None, kind=None
     L.colsums = _ptr(colsums)
     if lowrank is not None:
         L.lowrank_T, L.lowrank_up, L.lowrank_rank = _lowrank_fields(lowrank)
+    if wzero is not None:
+        L.w_zero, L.x_rowsums = _ptr(wzero[0]), _ptr(wzero[1])
     return L
 
 

@@ -30,6 +30,7 @@ SOURCES = [
     "pack_planes.hip",
     "pack_weights.hip",
     "act_quant.hip",
+    "weight_quant.hip",
     "skinny.hip",
     "tiles.cpp",
     "tasq_api.cpp",

@@ -50,9 +50,10 @@ struct Cfg {
     static constexpr int CPR = BK / 16;                 // 16-byte chunks per row
     static constexpr int A_LOADS = BM * CPR / NT;
     static constexpr int B_LOADS = BN * CPR / NT;
-    // LDS of the A operand, also holding the low-rank operands in the
-    // epilogue: T rows as bfloat16 hi and lo parts, then rows of U.
-    static constexpr int LR_BYTES = (2 * BM + BN) * kLrPitch;
+    // LDS of the A operand, also holding the epilogue's staged operands:
+    // T rows as bfloat16 hi and lo parts, rows of U, then one fp32 row term
+    // per tile row (the weight zero point's activation sums).
+    static constexpr int LR_BYTES = (2 * BM + BN) * kLrPitch + 4 * BM;
     static constexpr int SMA = NSTAGE * BM * CPR > (LR_BYTES + 15) / 16 ? NSTAGE * BM * CPR
                                                                        : (LR_BYTES + 15) / 16;
     static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must hold 32x32 blocks");
@@ -501,6 +502,36 @@ __device__ __forceinline__ void stage_lowrank(const LayerDesc &d, int m0, int n0
     }
 }
 
+// Stages, per tile row m, the activation sum that multiplies a weight zero
+// point: R[m] = sum_k x_code[m][k] (+ K (128 - z_x) for asymmetric codes,
+// whose x_hat carries the offset 128 - z_x in every element).
+template <class C>
+__device__ __forceinline__ void stage_rowsums(const LayerDesc &d, int m0, char *lds)
+{
+    float *R = reinterpret_cast<float *>(lds + (2 * C::BM + C::BN) * kLrPitch);
+    const float off = d.act ? (float)d.K * (128.0f - d.act[1]) : 0.0f;
+    for (int e = threadIdx.x; e < C::BM; e += C::NT)
+        R[e] = m0 + e < d.M ? (float)d.xrs[m0 + e] + off : 0.0f;
+}
+
+// Adds f * R[row] to the 16 registers of a lane in a 32x32 block starting
+// at tile row rl (register v: row rl + 8*(v/4) + 4*(l/32) + v%4): four
+// 16-byte LDS reads.
+template <class C>
+__device__ __forceinline__ void add_rowsum_block(const char *lds, int rl, int lane, float f,
+                                                 v16f &out)
+{
+    const float *R = reinterpret_cast<const float *>(lds + (2 * C::BM + C::BN) * kLrPitch);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const float4 t = *reinterpret_cast<const float4 *>(R + rl + 8 * q + 4 * (lane >> 5));
+        out[4 * q + 0] += f * t.x;
+        out[4 * q + 1] += f * t.y;
+        out[4 * q + 2] += f * t.z;
+        out[4 * q + 3] += f * t.w;
+    }
+}
+
 // The 32x32 block (rows rl.., columns cl.. of the tile) of T U^T from the
 // staged operands: per 16-wide step of the rank, one bfloat16 MFMA on the hi
 // and one on the lo part of T, accumulated in fp32.  Same register layout
@@ -529,8 +560,10 @@ __device__ __forceinline__ v16f lowrank_block(const char *lds, int r, int rl, in
 // value y = float(acc) * (sx * sw[n]) + bias[n].  With asymmetric
 // activations (d.act) the zero point enters through the channel sum of W_b:
 // y = (float(acc) + (128 - z) * colsum_b[n]) * (alpha * sw[n]) + bias[n].
-// With a low-rank branch (d.lr_T) y also gains (T U^T)[m][n], computed here
-// from operands staged in the (then idle) LDS.  Register v of a 32x32
+// With a low-rank branch (d.lr_T) y also gains (T U^T)[m][n], and with
+// per-channel weight zero points (d.wz: w_hat = sw (W_b + 128 - z_n)) the
+// term (128 - z_n) R[m] joins the accumulator, R[m] the row's activation
+// sum; both are computed from operands staged in the (then idle) LDS.  Register v of a 32x32
 // accumulator in lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32, so
 // each store instruction covers two 128-byte row segments.  Rows past M
 // fall past the buffer end and are dropped; columns past N carry kOOB.
@@ -543,9 +576,13 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
     const int wave = tid >> 6;
     const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
     const bool lowrank = d.lr_T != nullptr && d.y != nullptr;
-    if (lowrank) {
+    const bool wzero = d.wz != nullptr && d.y != nullptr;
+    if (lowrank || wzero) {
         __syncthreads();            // every wave is done with the main loop's LDS
-        stage_lowrank<C>(d, m0, n0, lds);
+        if (lowrank)
+            stage_lowrank<C>(d, m0, n0, lds);
+        if (wzero)
+            stage_rowsums<C>(d, m0, lds);
         __syncthreads();
     }
     const uint32_t outb = (uint32_t)d.M * (uint32_t)d.N * 4u;
@@ -557,7 +594,7 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
     for (int j = 0; j < C::FN; ++j) {
         const int n = n0 + wn * C::WTN + j * 32 + (lane & 31);
         const bool nok = n < d.N;
-        float scale = 0.f, bias = 0.f, corr = 0.f;
+        float scale = 0.f, bias = 0.f, corr = 0.f, wsc = 0.f;
         if (nok) {
             if (d.act) {
                 scale = d.act[0] * d.sw[n];
@@ -567,6 +604,8 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
             }
             if (d.bias)
                 bias = d.bias[n];
+            if (wzero)
+                wsc = (128.0f - d.wz[n]) * scale;
         }
         const uint32_t base = nok ? ((uint32_t)mrow * (uint32_t)d.N + (uint32_t)n) * 4u : kOOB;
         if (d.acc) {
@@ -580,14 +619,18 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
         if (d.y) {
 #pragma unroll
             for (int i = 0; i < C::FM; ++i) {
-                if (lowrank) {
-                    const v16f lr = lowrank_block<C>(lds, d.lr_r, wm * C::WTM + i * 32,
-                                                     wn * C::WTN + j * 32, lane);
+                if (lowrank || wzero) {
+                    v16f extra = {};
+                    if (lowrank)
+                        extra = lowrank_block<C>(lds, d.lr_r, wm * C::WTM + i * 32,
+                                                 wn * C::WTN + j * 32, lane);
+                    if (wzero)
+                        add_rowsum_block<C>(lds, wm * C::WTM + i * 32, lane, wsc, extra);
 #pragma unroll
                     for (int v = 0; v < 16; ++v)
                         st32(ry, base + (uint32_t)(i * 32 + 8 * (v >> 2) + (v & 3)) * rowb,
                              __builtin_bit_cast(uint32_t, ((float)acc[i][j][v] + corr) * scale +
-                                                              bias + lr[v]));
+                                                              bias + extra[v]));
                 } else {
 #pragma unroll
                     for (int v = 0; v < 16; ++v)

@@ -37,7 +37,7 @@ struct CfgP {
     static constexpr int CPR = BK / 16, KK = BK / 32;
     static constexpr int SA = BM * CPR;                 // v4i per LDS stage
     // LDS of the kernel: two stages, or the epilogue's low-rank operands.
-    static constexpr int LR_BYTES = (2 * BM + BN) * kLrPitch;
+    static constexpr int LR_BYTES = (2 * BM + BN) * kLrPitch + 4 * BM;
     static constexpr int SM = 2 * SA > (LR_BYTES + 15) / 16 ? 2 * SA : (LR_BYTES + 15) / 16;
     static constexpr int A_LOADS = BM * CPR / NT;
     static constexpr int B_LOADS = 0;                   // weights bypass LDS

@@ -217,6 +217,13 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
                 for (int q = 0; q < d.lr_r; ++q)
                     lr = fmaf(t[q], __uint_as_float((uint32_t)u[q] << 16), lr);
             }
+            // Weight zero point: (128 - z_n) times the row's activation sum
+            // (plus K (128 - z_x) for asymmetric codes).
+            if (d.wz) {
+                const float R = (float)d.xrs[row] +
+                                (d.act ? (float)d.K * (128.0f - d.act[1]) : 0.0f);
+                lr += (128.0f - d.wz[nn]) * scale * R;
+            }
             d.y[o] = ((float)sum + corr) * scale + bias + lr;
         }
     }

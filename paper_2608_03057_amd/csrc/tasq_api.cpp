@@ -220,6 +220,8 @@ LayerDesc make_desc(const tasq_layer &L, const tasq_opts *o)
     d.Wp = L.W_packed ? L.W_packed : (o ? o->W_packed : nullptr);
     d.act = L.act_params ? L.act_params : (o ? o->act_params : nullptr);
     d.colsums = L.colsums ? L.colsums : (o ? o->colsums : nullptr);
+    d.wz = L.w_zero ? L.w_zero : (o ? o->w_zero : nullptr);
+    d.xrs = L.w_zero ? L.x_rowsums : (o ? o->x_rowsums : nullptr);
     if (L.lowrank_T) {
         d.lr_T = L.lowrank_T;
         d.lr_U = L.lowrank_up;
@@ -272,6 +274,20 @@ int validate_layer(const tasq_layer &L, const tasq_opts *o)
     if ((reinterpret_cast<uintptr_t>(local.act_params) & 3) ||
         (reinterpret_cast<uintptr_t>(local.colsums) & 3))
         return TASQ_ERR_ALIGN;
+    // Weight zero points: the layer's own fields, else the call's.
+    if (L.w_zero) {
+        local.w_zero = L.w_zero;
+        local.x_rowsums = L.x_rowsums;
+    }
+    if (has_out && L.y && local.w_zero) {
+        if (!local.x_rowsums)
+            return TASQ_ERR_NULL;
+        if ((reinterpret_cast<uintptr_t>(local.w_zero) & 3) ||
+            (reinterpret_cast<uintptr_t>(local.x_rowsums) & 3))
+            return TASQ_ERR_ALIGN;
+        if (L.kind == TASQ_KIND_CONV3X3)
+            return TASQ_ERR_LAYOUT;
+    }
     // Low-rank branch: the layer's own fields, else the call's.
     if (L.lowrank_T) {
         local.lowrank_T = L.lowrank_T;
@@ -469,6 +485,41 @@ int tasq_quantize_activations(const float *x, int M, int K, int8_t *X_out, float
         return TASQ_ERR_ALIGN;
     hipError_t e = tasq::launch_quantize_activations(x, n, X_out, act_params,
                                                      static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}
+
+int tasq_quantize_weights(const float *W, int N, int K, int8_t *W_out, float *alpha_out,
+                          float *z_out, float *sw_out, void *stream)
+{
+    if (N < 0 || K < 0 || (N > 0 && K == 0))
+        return TASQ_ERR_DIM;
+    if (K > TASQ_MAX_K)
+        return TASQ_ERR_OVERFLOW;
+    if (N == 0)
+        return TASQ_OK;
+    if (!W || !W_out || !alpha_out || !z_out || !sw_out)
+        return TASQ_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(W) & 3) || (reinterpret_cast<uintptr_t>(alpha_out) & 3) ||
+        (reinterpret_cast<uintptr_t>(z_out) & 3) || (reinterpret_cast<uintptr_t>(sw_out) & 3))
+        return TASQ_ERR_ALIGN;
+    hipError_t e = tasq::launch_quantize_weights(W, N, K, W_out, alpha_out, z_out, sw_out,
+                                                 static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}
+
+int tasq_row_sums(const int8_t *X, int M, int K, int32_t *out, void *stream)
+{
+    if (M < 0 || K < 0)
+        return TASQ_ERR_DIM;
+    if (K > TASQ_MAX_K)
+        return TASQ_ERR_OVERFLOW;
+    if (M == 0)
+        return TASQ_OK;
+    if (!out || (K > 0 && !X))
+        return TASQ_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(out) & 3)
+        return TASQ_ERR_ALIGN;
+    hipError_t e = tasq::launch_row_sums(X, M, K, out, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
 }
 

@@ -22,6 +22,8 @@ struct LayerDesc {
     const int32_t *colsums; // [8][N] channel sums of W_b (with act)
     const float *lr_T;      // low-rank branch x~ D^T, fp32 [M][lr_r], or null
     const uint16_t *lr_U;   // its up projection, bfloat16 [N][lr_r]
+    const float *wz;        // per-channel weight zero points [N] or null
+    const int32_t *xrs;     // row sums of the activation codes [M] (with wz)
     int32_t *acc;           // [M][N] or null
     float *y;               // [M][N] or null
     float sx;
@@ -114,6 +116,9 @@ constexpr int kLowrankMaxRank = 32;
 // Returns the number of workgroups (partial ranges) through *groups.
 hipError_t launch_lowrank_down(const float *x, int M, int K, const uint16_t *D, int r, float *T,
                                uint32_t *part, int *groups, hipStream_t stream);
+hipError_t launch_quantize_weights(const float *W, int N, int K, int8_t *Q, float *alpha,
+                                   float *z, float *sw, hipStream_t stream);
+hipError_t launch_row_sums(const int8_t *X, int M, int K, int32_t *out, hipStream_t stream);
 hipError_t launch_quantize_activations_lowrank(const float *x, int M, int K, int8_t *q,
                                                float *params, const uint16_t *D, int r, float *T,
                                                hipStream_t stream);

@@ -99,6 +99,9 @@ def opts(**kw):
     (dict(opts=opts(lowrank_T=FAKE, lowrank_up=FAKE, lowrank_rank=0)), _lib.TASQ_ERR_DIM),
     (dict(opts=opts(lowrank_T=FAKE + 4, lowrank_up=FAKE, lowrank_rank=16)), _lib.TASQ_ERR_ALIGN),
     (dict(opts=opts(lowrank_T=FAKE, lowrank_up=FAKE + 8, lowrank_rank=32)), _lib.TASQ_ERR_ALIGN),
+    (dict(opts=opts(w_zero=FAKE)), _lib.TASQ_ERR_NULL),
+    (dict(opts=opts(w_zero=FAKE + 2, x_rowsums=FAKE)), _lib.TASQ_ERR_ALIGN),
+    (dict(opts=opts(w_zero=FAKE, x_rowsums=FAKE + 1)), _lib.TASQ_ERR_ALIGN),
 ])
 def test_masked_linear_rejects(kw, code):
     assert lin(**kw) == code
@@ -169,6 +172,25 @@ def test_lowrank_down_rejects():
     assert g(None, 0, 4, None, None, None, 32, None, None) == _lib.TASQ_OK
 
 
+def test_quantize_weights_and_row_sums_reject():
+    q = L.tasq_quantize_weights
+    assert q(None, 4, 4, FAKE, FAKE, FAKE, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert q(FAKE, 4, 4, FAKE, FAKE, None, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert q(FAKE, 4, 0, FAKE, FAKE, FAKE, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert q(FAKE, -1, 4, FAKE, FAKE, FAKE, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert q(FAKE, 4, 131072, FAKE, FAKE, FAKE, FAKE, None) == _lib.TASQ_ERR_OVERFLOW
+    assert q(FAKE + 2, 4, 4, FAKE, FAKE, FAKE, FAKE, None) == _lib.TASQ_ERR_ALIGN
+    assert q(FAKE, 4, 4, FAKE, FAKE, FAKE, FAKE + 1, None) == _lib.TASQ_ERR_ALIGN
+    assert q(None, 0, 4, None, None, None, None, None) == _lib.TASQ_OK
+    r = L.tasq_row_sums
+    assert r(None, 4, 4, FAKE, None) == _lib.TASQ_ERR_NULL
+    assert r(FAKE, 4, 4, None, None) == _lib.TASQ_ERR_NULL
+    assert r(FAKE, -1, 4, FAKE, None) == _lib.TASQ_ERR_DIM
+    assert r(FAKE, 4, 131072, FAKE, None) == _lib.TASQ_ERR_OVERFLOW
+    assert r(FAKE, 4, 4, FAKE + 2, None) == _lib.TASQ_ERR_ALIGN
+    assert r(None, 0, 4, None, None) == _lib.TASQ_OK
+
+
 def test_weight_colsums_rejects():
     c = L.tasq_weight_colsums
     assert c(None, 4, 4, FAKE, None) == _lib.TASQ_ERR_NULL
@@ -188,6 +210,10 @@ def test_schedule_asymmetric_layer_needs_colsums():
     assert sched([layer(), conv_lr], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_LAYOUT
     assert sched([layer(lowrank_T=FAKE, lowrank_up=FAKE, lowrank_rank=32)] * 2, tbl, 4, 20,
                  0, 0) == _lib.TASQ_OK
+    conv_wz = layer(kind=_lib.KIND_CONV3X3, H=2, Wd=2, C=16, M=4, K=144, w_zero=FAKE,
+                    x_rowsums=FAKE)
+    assert sched([layer(), conv_wz], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_LAYOUT
+    assert sched([layer(w_zero=FAKE)], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_NULL
     assert sched([layer(), layer(act_params=FAKE)], tbl, 4, 20, 0, 1) == _lib.TASQ_ERR_NULL
     assert sched([layer(act_params=FAKE, colsums=FAKE + 2), layer()], tbl, 4, 20, 0, 1) \
         == _lib.TASQ_ERR_ALIGN
