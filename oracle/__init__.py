@@ -455,3 +455,67 @@ def run_schedule(layers, table, S: int, T: int, t_begin: int, t_end: int, sx: fl
                                        layer.get("bias"))
             out[l] = (acc, y, b)
     return out
+
+
+# ------------------------------------------------ BitOPs and cycle accounting
+#
+# Sec. 4 reports Eff. W-bit (average operating weight precision) and Rel.
+# BitOPs (compute normalised to static W8A8) per schedule; Sec. 3.3 / 4.3
+# measure the bit-serial engine, whose cycles grow with the product of
+# weight and activation planes L R with no cost for switching precision
+# (Tab. measured: 528 cycles for four W1A4 tiles, i.e. 33 cycles per plane
+# pair per tile), and give per-tile totals for three dataflows at R = 4
+# (Tab. codesign), each linear in L.
+
+TPE_CYCLES_PER_PLANE_PAIR = 33
+# (slope, intercept) of total cycles per tile at R = 4 (Tab. codesign).
+TPE_TILE_LAW_R4 = {"naive": (4560, 173), "weight_stationary": (2850, 173),
+                   "activation_stationary": (570, 2603)}
+
+
+def tpe_cycles_measured(tile_bits, R: int = 4) -> int:
+    """Cycles of tiles run at weight precisions tile_bits and R activation
+    planes under the measured law (no switching overhead)."""
+    return sum(TPE_CYCLES_PER_PLANE_PAIR * int(L) * R for L in tile_bits)
+
+
+def tpe_tile_cycles(dataflow: str, L: int) -> int:
+    slope, icpt = TPE_TILE_LAW_R4[dataflow]
+    return slope * L + icpt
+
+
+def fetch_planes(dataflow: str, L: int, R: int) -> int:
+    """Bit planes fetched per tile (Tab. codesign model column)."""
+    return {"naive": 2 * L * R, "weight_stationary": L + L * R,
+            "activation_stationary": L + R}[dataflow]
+
+
+def schedule_cost(macs_per_layer, table, S: int, T: int, t_begin: int, t_end: int,
+                  act_bits: int) -> dict:
+    """Accounting of steps t_begin..t_end-1 of a schedule, summed over every
+    (layer, step) GEMM with b = table[l][stage(t)]:
+      macs, b_eff = sum MACs b / macs (MAC-weighted), b_mean = plain mean of
+      b over (layer, step), bitops = sum MACs b a, rel_bitops = bitops /
+      (64 macs), rel_cycles_measured = sum MACs b a / sum MACs 8 a (the
+      measured law), rel_cycles_as_a4 = sum MACs (570 b + 2603) / sum MACs
+      (570*8 + 2603) (activation-stationary tile law at R = 4)."""
+    macs = bw = bitops = c_as = c_as8 = 0
+    bsum = count = 0
+    for t in range(t_begin, t_end):
+        s = stage_of_step(t, S, T)
+        for l, mac in enumerate(macs_per_layer):
+            b = int(table[l][s])
+            macs += mac
+            bw += mac * b
+            bitops += mac * b * act_bits
+            c_as += mac * tpe_tile_cycles("activation_stationary", b)
+            c_as8 += mac * tpe_tile_cycles("activation_stationary", 8)
+            bsum += b
+            count += 1
+    if count == 0:
+        return dict(macs=0.0, b_eff=0.0, b_mean=0.0, bitops=0.0, rel_bitops=0.0,
+                    rel_cycles_measured=0.0, rel_cycles_as_a4=0.0)
+    return dict(macs=float(macs), b_eff=bw / macs if macs else 0.0, b_mean=bsum / count,
+                bitops=float(bitops), rel_bitops=bitops / (64 * macs) if macs else 0.0,
+                rel_cycles_measured=bitops / (8 * act_bits * macs) if macs else 0.0,
+                rel_cycles_as_a4=c_as / c_as8 if macs else 0.0)

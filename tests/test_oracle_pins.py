@@ -765,3 +765,55 @@ def test_layer_dequant_entries_match_full():
                                           bias=bias)
     assert np.array_equal(ae, acc[rows, cols])
     assert np.allclose(ye, y[rows, cols], rtol=1e-13, atol=0)
+
+
+# ------------------------------------------------ BitOPs and cycle accounting
+
+def _golden_rows(name):
+    from conftest import golden_path
+    rows = []
+    for line in open(golden_path(name)):
+        line = line.strip()
+        if line and not line.startswith("#"):
+            rows.append(line.split())
+    return rows
+
+
+def test_rel_bitops_matches_printed_table():
+    """Every (A-bit, Eff. W-bit, Rel. BitOPs) triple the quality table prints
+    satisfies Rel = W A / 64 to its two printed decimals, and the schedule
+    accounting of a one-layer schedule at that constant precision gives it."""
+    for a, w100, rel100 in (map(int, r) for r in _golden_rows("bitops_quality.txt")):
+        assert round(w100 / 100 * a / 64, 2) == rel100 / 100
+    for a, b in ((8, 8), (8, 4), (4, 4), (16, 8)):
+        c = oracle.schedule_cost([100], [[b]], 1, 1, 0, 1, a)
+        assert c["rel_bitops"] == b * a / 64 and c["b_eff"] == b
+
+
+def test_tpe_cycle_laws_match_printed_tables():
+    rows = _golden_rows("tpe_cycles.txt")
+    for r in rows:
+        if r[0] == "measured":
+            assert oracle.tpe_cycles_measured([int(v) for v in r[1:5]]) == int(r[5])
+        elif r[0] == "fetch":
+            assert oracle.fetch_planes(r[1], 8, 4) == int(r[2])
+        else:
+            assert oracle.tpe_tile_cycles(r[0], int(r[1])) == int(r[2])
+
+
+def test_schedule_cost_hand_worked():
+    """Two layers (100 and 300 MACs), S = 2 stages over T = 4 steps, table
+    [[8, 4], [2, 6]]: steps 0, 1 at (8, 2), steps 2, 3 at (4, 6)."""
+    c = oracle.schedule_cost([100, 300], [[8, 4], [2, 6]], 2, 4, 0, 4, 8)
+    macs = 4 * 400
+    bw = 2 * (100 * 8 + 300 * 2) + 2 * (100 * 4 + 300 * 6)
+    assert c["macs"] == macs and c["b_eff"] == bw / macs
+    assert c["b_mean"] == (8 + 2 + 8 + 2 + 4 + 6 + 4 + 6) / 8
+    assert c["rel_bitops"] == bw * 8 / (64 * macs)
+    assert c["rel_cycles_measured"] == bw / (8 * macs)
+    num = 2 * (100 * (570 * 8 + 2603) + 300 * (570 * 2 + 2603)) + \
+        2 * (100 * (570 * 4 + 2603) + 300 * (570 * 6 + 2603))
+    assert c["rel_cycles_as_a4"] == num / (macs * (570 * 8 + 2603))
+    # a sub-range of steps counts only those steps
+    c2 = oracle.schedule_cost([100, 300], [[8, 4], [2, 6]], 2, 4, 3, 4, 8)
+    assert c2["macs"] == 400 and c2["b_eff"] == (100 * 4 + 300 * 6) / 400
