@@ -474,6 +474,17 @@ def main():
         log("timing the weight quantizer")
         wq = weight_quantizer(wl, dev)
 
+    # The paper's compute accounting of the same schedule next to the
+    # measured wall-time ratios (table vs static 8-bit weights).
+    cost = T.schedule_cost([(sp.M, sp.N, sp.K) for sp in wl.layers], table, wl.S, wl.T, 0,
+                           wl.T, 8)
+    accounting = {k: round(v, 4) if k not in ("macs", "bitops") else v for k, v in cost.items()}
+    accounting["measured_ratio_vs_static_b8"] = round(ms / ms8, 4)
+    if skinny is not None:
+        accounting["measured_ratio_vs_static_b8_m16_planes"] = round(
+            skinny["ms_per_denoising_step"]["planes_tasq"] /
+            skinny["ms_per_denoising_step"]["planes_b8"], 4)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle sample")
@@ -492,6 +503,7 @@ def main():
                         "static_max_over_stages": round(msmax, 4)},
         "margin_vs_static_b8": round(1.0 - ms / ms8, 4),
         "mean_bits": round(float(table.float().mean()), 3),
+        "accounting": accounting,
         "roofline": roof,
         "skinny_schedule": skinny,
         "asymmetric_activations": act,

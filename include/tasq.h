@@ -377,6 +377,41 @@ size_t tasq_schedule_workspace_bytes(const tasq_layer *layers, int L);
 /* Static description of a status code; never NULL. */
 const char *tasq_status_string(int status);
 
+/*
+ * Compute accounting of steps t_begin..t_end-1 of a schedule (same layers
+ * and table as tasq_run_schedule), summed over every (layer, step) GEMM
+ * with b = b_table[l][floor(t*S/T)] and MACs = M*N*K:
+ *   macs                 total multiply-accumulates;
+ *   b_eff                MAC-weighted mean of b, the Eff. W-bit of the
+ *                        quality-compute table (Sec. 4; the paper does not
+ *                        define the weighting);
+ *   b_mean               plain mean of b over (layer, step);
+ *   bitops               sum MACs * b * act_bits;
+ *   rel_bitops           bitops / (64 macs), Rel. BitOPs against static W8A8;
+ *   rel_cycles_measured  cycles relative to static 8-bit weights under the
+ *                        bit-serial engine's measured law (cycles grow as
+ *                        weight x activation planes, switching is free;
+ *                        Tab. measured), = b_eff / 8;
+ *   rel_cycles_as_a4     the same under the activation-stationary per-tile
+ *                        law at 4 activation planes, 570 L + 2603 cycles
+ *                        (Tab. codesign).
+ * Host only; reads no device memory.  Errors: TASQ_ERR_NULL, _RANGE (S, T,
+ * step range, act_bits outside 1..16), _DIM, _BITS (a table entry outside
+ * 1..8).  *out is zeroed first.
+ */
+typedef struct tasq_cost {
+    double macs;
+    double b_eff;
+    double b_mean;
+    double bitops;
+    double rel_bitops;
+    double rel_cycles_measured;
+    double rel_cycles_as_a4;
+} tasq_cost;
+
+int tasq_schedule_cost(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
+                       int t_begin, int t_end, int act_bits, tasq_cost *out);
+
 #ifdef __cplusplus
 }
 #endif

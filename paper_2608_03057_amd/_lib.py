@@ -40,7 +40,7 @@ EXPORTS = (
     "tasq_masked_linear", "tasq_masked_conv3x3", "tasq_pack_planes", "tasq_planes_bytes",
     "tasq_pack_weights", "tasq_packed_weight_bytes", "tasq_quantize_activations",
     "tasq_weight_colsums", "tasq_lowrank_down", "tasq_quantize_activations_lowrank",
-    "tasq_quantize_weights", "tasq_row_sums",
+    "tasq_quantize_weights", "tasq_row_sums", "tasq_schedule_cost",
     "tasq_stage_of_step", "tasq_run_schedule",
     "tasq_workspace_bytes", "tasq_schedule_workspace_bytes", "tasq_status_string",
 )
@@ -54,6 +54,11 @@ class Opts(ctypes.Structure):
                 ("lowrank_T", ctypes.c_void_p), ("lowrank_up", ctypes.c_void_p),
                 ("lowrank_rank", ctypes.c_int32), ("w_zero", ctypes.c_void_p),
                 ("x_rowsums", ctypes.c_void_p)]
+
+
+class Cost(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("macs", "b_eff", "b_mean", "bitops", "rel_bitops",
+                                               "rel_cycles_measured", "rel_cycles_as_a4")]
 
 
 class Layer(ctypes.Structure):
@@ -103,6 +108,8 @@ def lib() -> ctypes.CDLL:
         L.tasq_quantize_activations.restype = i32
         L.tasq_weight_colsums.argtypes = [vp, i32, i32, vp, vp]
         L.tasq_weight_colsums.restype = i32
+        L.tasq_schedule_cost.argtypes = [vp, i32, vp, i32, i32, i32, i32, i32, vp]
+        L.tasq_schedule_cost.restype = i32
         L.tasq_quantize_weights.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp]
         L.tasq_quantize_weights.restype = i32
         L.tasq_row_sums.argtypes = [vp, i32, i32, vp, vp]

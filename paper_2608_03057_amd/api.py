@@ -315,6 +315,31 @@ def schedule_workspace_bytes(layers: Sequence[Layer]) -> int:
     return _lib.lib().tasq_schedule_workspace_bytes(arr, len(layers))
 
 
+def schedule_cost(layers, table, S: int, T: int, t_begin: int, t_end: int,
+                  act_bits: int = 8) -> dict:
+    """Compute accounting of a schedule (tasq_schedule_cost): ``layers`` are
+    Layer structs or (M, N, K) shapes, ``table`` a uint8 [L, S] host array.
+    Host only."""
+    structs = []
+    for ly in layers:
+        if isinstance(ly, Layer):
+            structs.append(ly)
+        else:
+            st = Layer()
+            st.kind = _lib.KIND_LINEAR
+            st.M, st.N, st.K = (int(v) for v in ly)
+            structs.append(st)
+    table = torch.as_tensor(table).to(torch.uint8).contiguous().cpu()
+    L = len(structs)
+    if tuple(table.shape) != (L, S):
+        raise ValueError(f"table must be [{L}, {S}]")
+    arr = _layer_array(structs)
+    out = _lib.Cost()
+    check(_lib.lib().tasq_schedule_cost(arr, L, table.data_ptr(), S, T, t_begin, t_end,
+                                        act_bits, ctypes.byref(out)), "tasq_schedule_cost")
+    return {name: getattr(out, name) for name, _ in _lib.Cost._fields_}
+
+
 def run_schedule(layers: Sequence[Layer], table: torch.Tensor, S: int, T: int, t_begin: int,
                  t_end: int, *, workspace: Optional[torch.Tensor] = None,
                  variant: int = _lib.VARIANT_AUTO) -> None:

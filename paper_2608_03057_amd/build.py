@@ -33,6 +33,7 @@ SOURCES = [
     "weight_quant.hip",
     "skinny.hip",
     "tiles.cpp",
+    "cost.cpp",
     "tasq_api.cpp",
 ]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
