@@ -229,8 +229,15 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
     }
 }
 
+// Occupancy: with one 32-token block (MT = 1) the streaming loop fits 80
+// VGPRs, i.e. 6 waves per SIMD (three 8-wave workgroups per CU); the
+// epilogue's optional terms must not push it past that.
+template <int MT>
+constexpr int skinny_waves_per_eu() { return MT == 1 ? 6 : 4; }
+
 template <int SRC, int MT>
-__global__ void __launch_bounds__(SK_WAVES * 64) k_skinny(LayerDesc d)
+__global__ void __launch_bounds__(SK_WAVES * 64)
+__attribute__((amdgpu_waves_per_eu(skinny_waves_per_eu<MT>()))) k_skinny(LayerDesc d)
 {
     __shared__ int red[SK_WAVES * MT * 16 * SK_PAD];
     skinny_block<SRC, MT>(d, d.bits, blockIdx.x, red);
@@ -240,6 +247,7 @@ __global__ void __launch_bounds__(SK_WAVES * 64) k_skinny(LayerDesc d)
 // d.tile_begin is the layer's first block.
 template <int SRC, int MT>
 __global__ void __launch_bounds__(SK_WAVES * 64)
+__attribute__((amdgpu_waves_per_eu(skinny_waves_per_eu<MT>())))
 k_skinny_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *table, int S, int stage)
 {
     __shared__ int red[SK_WAVES * MT * 16 * SK_PAD];
