@@ -174,7 +174,7 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
 
-constexpr int kDownWaves = 8;
+constexpr int kDownWaves = 16;
 
 __device__ __forceinline__ uint32_t bf16_rne(float f)
 {
@@ -182,10 +182,26 @@ __device__ __forceinline__ uint32_t bf16_rne(float f)
     return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-template <bool RANGE>
+__device__ __forceinline__ v4u pack_bf16(float4 lo, float4 hi)
+{
+    return v4u{bf16_rne(lo.x) | (bf16_rne(lo.y) << 16), bf16_rne(lo.z) | (bf16_rne(lo.w) << 16),
+               bf16_rne(hi.x) | (bf16_rne(hi.y) << 16), bf16_rne(hi.z) | (bf16_rne(hi.w) << 16)};
+}
+
+__device__ __forceinline__ void fold_range(float4 v, float &mn, float &mx)
+{
+    mn = fminf(fminf(mn, v.x), fminf(v.y, fminf(v.z, v.w)));
+    mx = fmaxf(fmaxf(mx, v.x), fmaxf(v.y, fmaxf(v.z, v.w)));
+}
+
+// FAST: K % 8 == 0 and x, D 16-byte aligned, so an in-range K step covers
+// all 8 elements of a lane; each wave then issues the loads of 4 of its K
+// steps before their MFMAs (enough bytes in flight with one workgroup per
+// CU).  Otherwise every element is loaded on its own with bounds checks.
+template <bool RANGE, bool FAST>
 __global__ void __launch_bounds__(64 * kDownWaves)
 k_lowrank_down(const float *__restrict__ x, int M, int K, const uint16_t *__restrict__ D, int r,
-               float *__restrict__ T, uint32_t *__restrict__ part, bool fast)
+               float *__restrict__ T, uint32_t *__restrict__ part)
 {
     __shared__ float red[kDownWaves][16][64];
     __shared__ uint32_t smin[kDownWaves], smax[kDownWaves];
@@ -202,32 +218,43 @@ k_lowrank_down(const float *__restrict__ x, int M, int K, const uint16_t *__rest
         const float *xr = x + (size_t)(rok ? row : 0) * (size_t)K;
         const uint16_t *dr = D + (size_t)(j < r ? j : 0) * (size_t)K;
         v16f acc = {};
-        for (int s = wave; s < nsteps; s += kDownWaves) {
-            const int k = 16 * s + 8 * half;
-            float xv[8];
-            v4u bw;
-            if (fast) {
-                // K % 8 == 0 and 16-byte aligned rows: k < K covers all 8.
-                const bool ok = rok && k < K;
-                float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
-                if (ok) {
-                    const float4 *p = reinterpret_cast<const float4 *>(xr + k);
-                    lo = p[0];
-                    hi = p[1];
-                }
-                xv[0] = lo.x; xv[1] = lo.y; xv[2] = lo.z; xv[3] = lo.w;
-                xv[4] = hi.x; xv[5] = hi.y; xv[6] = hi.z; xv[7] = hi.w;
-                if (ok) {
+        if constexpr (FAST) {
+            constexpr int U = 4;
+            for (int s0 = wave; s0 < nsteps; s0 += U * kDownWaves) {
+                float4 lo[U], hi[U];
+                v4u bw[U];
+                bool ok[U];
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        mn = fminf(mn, xv[e]);
-                        mx = fmaxf(mx, xv[e]);
+                for (int u = 0; u < U; ++u) {
+                    const int k = 16 * (s0 + u * kDownWaves) + 8 * half;
+                    const bool kin = k < K;
+                    ok[u] = rok && kin;
+                    lo[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                    hi[u] = lo[u];
+                    if (ok[u]) {
+                        const float4 *p = reinterpret_cast<const float4 *>(xr + k);
+                        lo[u] = p[0];
+                        hi[u] = p[1];
                     }
+                    bw[u] = v4u{0, 0, 0, 0};
+                    if (j < r && kin)
+                        bw[u] = *reinterpret_cast<const v4u *>(dr + k);
                 }
-                bw = v4u{0, 0, 0, 0};
-                if (j < r && k < K)
-                    bw = *reinterpret_cast<const v4u *>(dr + k);
-            } else {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    if (RANGE && ok[u]) {
+                        fold_range(lo[u], mn, mx);
+                        fold_range(hi[u], mn, mx);
+                    }
+                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(v8bf, pack_bf16(lo[u], hi[u])),
+                        __builtin_bit_cast(v8bf, bw[u]), acc, 0, 0, 0);
+                }
+            }
+        } else {
+            for (int s = wave; s < nsteps; s += kDownWaves) {
+                const int k = 16 * s + 8 * half;
+                float xv[8];
                 uint32_t dv[8];
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
@@ -239,16 +266,14 @@ k_lowrank_down(const float *__restrict__ x, int M, int K, const uint16_t *__rest
                     }
                     dv[e] = (j < r && ok) ? (uint32_t)dr[k + e] : 0u;
                 }
-                bw = v4u{dv[0] | (dv[1] << 16), dv[2] | (dv[3] << 16), dv[4] | (dv[5] << 16),
-                         dv[6] | (dv[7] << 16)};
+                const v4u bw = v4u{dv[0] | (dv[1] << 16), dv[2] | (dv[3] << 16),
+                                   dv[4] | (dv[5] << 16), dv[6] | (dv[7] << 16)};
+                const v4u aw = pack_bf16(make_float4(xv[0], xv[1], xv[2], xv[3]),
+                                         make_float4(xv[4], xv[5], xv[6], xv[7]));
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, aw),
+                                                              __builtin_bit_cast(v8bf, bw), acc,
+                                                              0, 0, 0);
             }
-            const v4u aw = v4u{bf16_rne(xv[0]) | (bf16_rne(xv[1]) << 16),
-                               bf16_rne(xv[2]) | (bf16_rne(xv[3]) << 16),
-                               bf16_rne(xv[4]) | (bf16_rne(xv[5]) << 16),
-                               bf16_rne(xv[6]) | (bf16_rne(xv[7]) << 16)};
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, aw),
-                                                          __builtin_bit_cast(v8bf, bw), acc, 0, 0,
-                                                          0);
         }
         // Register v of lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32.
 #pragma unroll
@@ -351,12 +376,16 @@ hipError_t launch_lowrank_down(const float *x, int M, int K, const uint16_t *D, 
     const int G = grid_for(M, 32, kActPartials);
     if (groups)
         *groups = G;
-    if (part)
-        hipLaunchKernelGGL(k_lowrank_down<true>, dim3(G), dim3(64 * kDownWaves), 0, stream, x, M,
-                           K, D, r, T, part, fast);
+    const dim3 g(G), b(64 * kDownWaves);
+    if (part && fast)
+        hipLaunchKernelGGL((k_lowrank_down<true, true>), g, b, 0, stream, x, M, K, D, r, T, part);
+    else if (part)
+        hipLaunchKernelGGL((k_lowrank_down<true, false>), g, b, 0, stream, x, M, K, D, r, T, part);
+    else if (fast)
+        hipLaunchKernelGGL((k_lowrank_down<false, true>), g, b, 0, stream, x, M, K, D, r, T, part);
     else
-        hipLaunchKernelGGL(k_lowrank_down<false>, dim3(G), dim3(64 * kDownWaves), 0, stream, x, M,
-                           K, D, r, T, part, fast);
+        hipLaunchKernelGGL((k_lowrank_down<false, false>), g, b, 0, stream, x, M, K, D, r, T,
+                           part);
     return hipGetLastError();
 }
 
