@@ -226,6 +226,111 @@ def skinny_sweep(device, steps=64):
     return rows
 
 
+def shape_sweep(device, reps=50, warmup=10):
+    """Single layers of the four per-shape workloads (one 1152->1152 layer at
+    256 tokens; the PixArt, SANA and SDXL-Turbo blocks, the latter with its
+    3x3 conv), fp32 output, each timed alone: `warmup` launches, then `reps`
+    launches each bracketed by HIP events on the launch stream, the Infinity
+    Cache flushed before each (a 512 MB buffer written between launches,
+    outside the events).  Per shape: median / p10 / p90 microseconds at b = 8
+    and at the lowest b of the layer's table row, the roofline of the shape
+    (2MNK ops against the dense int8 MFMA peak, M*K + N*K + 4*M*N bytes
+    against HBM), the packed-weight kernel's median, and, as external
+    context only, the vendor int8 GEMM (hipBLASLt through torch._int_mm,
+    int32 output, b = 8)."""
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=device)
+    ev = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        ts = []
+        for _ in range(reps):
+            flush.zero_()
+            a, b = ev(), ev()
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e3)
+        ts.sort()
+        return ts[len(ts) // 2], ts[len(ts) // 10], ts[(9 * len(ts)) // 10]
+
+    rows = []
+    for cfg in range(4):
+        wl = inputs.workload(cfg)
+        table = inputs.b_table(wl)
+        for l, spec in enumerate(wl.layers):
+            conv = spec.kind == "conv3x3"
+            X = inputs.x_full(wl, l, device=device)
+            W = inputs.w_full(wl, l)
+            if conv:
+                W = W.reshape(spec.N, 3, 3, spec.C)
+            W = W.to(device)
+            sw = inputs.sw_full(wl, l).to(device)
+            P = T.pack_weights(W)
+            yb = torch.empty((spec.M, spec.N), dtype=torch.float32, device=device)
+            if conv:
+                yb = yb.reshape(spec.H, spec.Wd, spec.N)
+            bmin = int(table[l].min())
+            row = {"workload": wl.name, "layer": spec.name, "M": spec.M, "N": spec.N,
+                   "K": spec.K, "kind": spec.kind, "b_low": bmin}
+            for bits in (8, bmin):
+                if conv:
+                    f = lambda b=bits: T.masked_conv3x3(X, W, wl.sx, sw, b, want_acc=False, y=yb)
+                    fp = lambda b=bits: T.masked_conv3x3(X, None, wl.sx, sw, b, packed=P,
+                                                         want_acc=False, y=yb)
+                else:
+                    f = lambda b=bits: T.masked_linear(X, W, wl.sx, sw, b, want_acc=False, y=yb)
+                    fp = lambda b=bits: T.masked_linear(X, None, wl.sx, sw, b, packed=P,
+                                                        want_acc=False, y=yb)
+                med, p10, p90 = timed(f)
+                row[f"b{bits}_us"] = {"median": round(med, 2), "p10": round(p10, 2),
+                                      "p90": round(p90, 2)}
+                row[f"b{bits}_packed_us_median"] = round(timed(fp)[0], 2)
+            ops = 2.0 * spec.M * spec.N * spec.K
+            byts = float(spec.M * (spec.C if conv else spec.K) + spec.N * spec.K
+                         + 4 * spec.M * spec.N)
+            t_mfma, t_hbm = ops / (PEAK_INT8_TOPS * 1e12), byts / (PEAK_HBM_GBS * 1e9)
+            med8 = row["b8_us"]["median"]
+            row.update({"tops_b8": round(ops / (med8 * 1e-6) / 1e12, 1),
+                        "bound": "mfma" if t_mfma > t_hbm else "hbm",
+                        "roofline_us": round(max(t_mfma, t_hbm) * 1e6, 2),
+                        "frac_b8": round(max(t_mfma, t_hbm) * 1e6 / med8, 3)})
+            if not conv and hasattr(torch, "_int_mm"):
+                try:
+                    row["vendor_int8_int32out_us_median"] = round(
+                        timed(lambda: torch._int_mm(X, W.t()))[0], 2)
+                except RuntimeError:
+                    row["vendor_int8_int32out_us_median"] = None
+            rows.append(row)
+            del X, W, P
+    return rows
+
+
+def config_schedules(device, steps=5, warmup=2):
+    """The schedules of the per-shape workloads (PixArt, SANA and SDXL-Turbo
+    blocks with their tables): milliseconds per denoising step with one
+    grouped launch per step and with per-layer launches."""
+    rows = []
+    for cfg in (1, 2, 3):
+        wl = inputs.workload(cfg)
+        table = inputs.b_table(wl)
+        layers, keep = build_workload(wl, device, packed=False)
+        ws = torch.empty(schedule_ws := T.schedule_workspace_bytes(layers), dtype=torch.uint8,
+                         device=device)
+        g = time_schedule(layers, table, wl, ws, steps, warmup) / wl.T
+        p = time_schedule(layers, table, wl, None, steps, warmup) / wl.T
+        ops = gemm_ops(wl)
+        rows.append({"workload": wl.name, "schedule": {
+            "grouped_ms_per_step": round(g, 4), "per_layer_ms_per_step": round(p, 4),
+            "grouped_tops": round(ops / (g * 1e-3) / 1e12, 1),
+            "per_layer_tops": round(ops / (p * 1e-3) / 1e12, 1),
+            "workspace_bytes": schedule_ws}})
+        del layers, keep, ws
+    return rows
+
+
 def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
     """The asymmetric-activation form of the same schedule: each layer's input
     arrives as fp32 (seeded normal draws with a few large channels), is
@@ -385,6 +490,9 @@ def main():
     ap.add_argument("--skinny-sweep", action="store_true",
                     help="only time single weight-streaming layers (M = 1, 16, 64) and print one "
                          "JSON line per layer shape")
+    ap.add_argument("--shape-sweep", action="store_true",
+                    help="only time the single layers of the four per-shape workloads (median / "
+                         "p10 / p90 over 50 cache-flushed launches) and print one JSON line each")
     ap.add_argument("--no-skinny", action="store_true",
                     help="skip the extra weight-streaming (M=16) schedule measurement")
     ap.add_argument("--no-act", action="store_true",
@@ -412,6 +520,12 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": src.numel(), "reps": 3}), flush=True)
+        return
+    if args.shape_sweep:
+        for row in shape_sweep("cuda"):
+            print(json.dumps(row), flush=True)
+        for row in config_schedules("cuda"):
+            print(json.dumps(row), flush=True)
         return
     if args.skinny_sweep:
         for row in skinny_sweep("cuda"):

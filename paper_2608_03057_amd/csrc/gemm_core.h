@@ -689,10 +689,11 @@ __global__ void __launch_bounds__(C::NT, C::OCC) k_masked_gemm(LayerDesc d)
 }
 
 // Grouped launch over every layer of one denoising step: workgroup t finds
-// its layer by binary search over the tile prefix, and that layer's b from
-// the (layer, stage) table (App. G.1: a table lookup, no re-launch).  CONV
-// adds the implicit-GEMM path for 3x3 conv layers; without it every layer
-// must be linear.
+// its segment (a run of one layer's tiles) by binary search over the
+// segments' first work units, and the layer's b from the (layer, stage)
+// table (App. G.1: a table lookup, no re-launch).  CONV adds the
+// implicit-GEMM path for 3x3 conv layers; without it every layer must be
+// linear.
 template <class C, bool CONV>
 __global__ void __launch_bounds__(C::NT, C::OCC)
 k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *table, int S,
@@ -710,10 +711,10 @@ k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
             hi = mid - 1;
     }
     const LayerDesc d = descs[lo];
-    const int bits = table[lo * S + stage];
+    const int bits = table[d.layer * S + stage];
     const uint32_t wmask = keep_mask_dword(bits);
     int tm, tn;
-    tile_coords(t - d.tile_begin, d.tiles_m, d.tiles_n, tm, tn);
+    tile_coords(t - d.tile_begin + d.tile_first, d.tiles_m, d.tiles_n, tm, tn);
     const int m0 = tm * C::BM, n0 = tn * C::BN;
     v16i acc[C::FM][C::FN];
     if (CONV && d.kind == KIND_CONV3X3)

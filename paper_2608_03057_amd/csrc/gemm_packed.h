@@ -217,10 +217,10 @@ k_gemm_packed_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
             hi = mid - 1;
     }
     const LayerDesc d = descs[lo];
-    const int bits = table[lo * S + stage];
+    const int bits = table[d.layer * S + stage];
     const uint32_t wmask = keep_mask_dword(bits);
     int tm, tn;
-    tile_coords(t - d.tile_begin, d.tiles_m, d.tiles_n, tm, tn);
+    tile_coords(t - d.tile_begin + d.tile_first, d.tiles_m, d.tiles_n, tm, tn);
     const int m0 = tm * C::BM, n0 = tn * C::BN;
     v16i acc[C::FM][C::FN];
     if (CONV && d.kind == KIND_CONV3X3)

@@ -261,7 +261,7 @@ k_skinny_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *tabl
             hi = mid - 1;
     }
     const LayerDesc d = descs[lo];
-    skinny_block<SRC, MT>(d, table[lo * S + stage], t - d.tile_begin, red);
+    skinny_block<SRC, MT>(d, table[d.layer * S + stage], t - d.tile_begin + d.tile_first, red);
 }
 
 template <int SRC>

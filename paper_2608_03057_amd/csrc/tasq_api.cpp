@@ -18,6 +18,46 @@ namespace {
 
 constexpr size_t kWsAlign = 256;
 
+// XCDs of the device; the grouped GEMM kernels give each one a contiguous
+// run of work units (xcd_remap in gemm_core.h).
+constexpr int kXcds = 8;
+constexpr int kComputeUnits = 256;
+constexpr double kImbalanceLimit = 1.10;
+
+// Heaviest XCD run over the mean, for the per-layer tile order, a tile
+// costing about its K plus a fixed part for loading and writing the tile.
+double xcd_imbalance(const std::vector<LayerDesc> &descs, long long G)
+{
+    const long long per = (G + kXcds - 1) / kXcds;
+    long long tall = G % kXcds;
+    if (tall == 0)
+        tall = kXcds;
+    double work[kXcds] = {0};
+    size_t l = 0;
+    long long used = 0;          // tiles of layer l already assigned
+    double total = 0;
+    for (int x = 0; x < kXcds; ++x) {
+        long long cnt = x < tall ? per : per - 1;
+        while (cnt > 0 && l < descs.size()) {
+            const long long n = (long long)descs[l].tiles_m * descs[l].tiles_n - used;
+            const long long take = n < cnt ? n : cnt;
+            const double w = (double)take * ((double)descs[l].K + 1024.0);
+            work[x] += w;
+            total += w;
+            cnt -= take;
+            used += take;
+            if (used == (long long)descs[l].tiles_m * descs[l].tiles_n) {
+                ++l;
+                used = 0;
+            }
+        }
+    }
+    double mx = 0;
+    for (double w : work)
+        mx = w > mx ? w : mx;
+    return total > 0 ? mx / (total / kXcds) : 1.0;
+}
+
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -122,11 +162,25 @@ int pick_tile(long long M, long long N)
     return tasq::TILE_64x64_K128_W4_PF2;
 }
 
-// Tile of the grouped per-step launch.
-int pick_grouped_tile()
+// Tile of the grouped per-step launch: 256x256, unless one 256x256 tile of
+// the longest-K layer costs more than a compute unit's even share of the
+// whole step; then that tile alone sets the step time (the 3x3 conv of the
+// SDXL-Turbo block: K = 11520 against 0.5 GOP per CU), and 128x128 tiles cut
+// it by four (measured 0.230 -> 0.178 ms per step there, no change on the
+// DiT blocks, which keep 256x256).
+int pick_grouped_tile(const std::vector<LayerDesc> &descs)
 {
     const int f = forced_tile();
-    return f >= 0 ? f : tasq::TILE_256x256_K128_W8_PF1;
+    if (f >= 0)
+        return f;
+    double total = 0, longest = 0;
+    for (const LayerDesc &d : descs) {
+        total += 2.0 * d.M * (double)d.N * d.K;
+        const double tile = 2.0 * 256 * 256 * (double)d.K;
+        longest = tile > longest ? tile : longest;
+    }
+    return longest > total / kComputeUnits ? tasq::TILE_128x128_K128_W4_PF2
+                                           : tasq::TILE_256x256_K128_W8_PF1;
 }
 
 bool use_bitplane(const tasq_opts *o) { return o && o->variant == TASQ_VARIANT_BITPLANE; }
@@ -599,7 +653,8 @@ size_t tasq_schedule_workspace_bytes(const tasq_layer *layers, int L)
     (void)layers;
     if (L <= 0)
         return 0;
-    return round_up((size_t)L * sizeof(LayerDesc), kWsAlign) + round_up((size_t)L * 64, kWsAlign);
+    return round_up((size_t)L * kXcds * sizeof(LayerDesc), kWsAlign) +
+           round_up((size_t)L * 64, kWsAlign);
 }
 
 int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
@@ -680,7 +735,7 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
             ts = ops.shape;
             launch_step = ops.grouped;
         } else {
-            const tasq::TileOps &ops = tasq::tile_ops(pick_grouped_tile());
+            const tasq::TileOps &ops = tasq::tile_ops(pick_grouped_tile(descs));
             ts = ops.shape;
             launch_step = ops.grouped;
         }
@@ -689,6 +744,8 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
             LayerDesc &d = descs[l];
             d.tiles_m = (d.M + ts.bm - 1) / ts.bm;
             d.tiles_n = (d.N + ts.bn - 1) / ts.bn;
+            d.tile_first = 0;
+            d.layer = l;
             d.tile_begin = (int)total;
             total += (long long)d.tiles_m * d.tiles_n;
             if (total > 0x7fffffffLL)
@@ -696,15 +753,44 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         }
         if (total == 0)
             return TASQ_OK;
+        // The GEMM kernels give each XCD one contiguous run of the work
+        // units (for L2 locality), equal in count.  When the layers' tiles
+        // differ in cost (K) and the layer order leaves one run much heavier
+        // than the others, every layer is cut into kXcds rounds instead, so
+        // that each run holds about an eighth of every layer.
+        std::vector<LayerDesc> segs;
+        if (!all_skinny && xcd_imbalance(descs, total) > kImbalanceLimit) {
+            try {
+                segs.reserve((size_t)L * kXcds);
+            } catch (const std::bad_alloc &) {
+                return TASQ_ERR_HIP;
+            }
+            long long begin = 0;
+            for (int r = 0; r < kXcds; ++r)
+                for (int l = 0; l < L; ++l) {
+                    const long long n = (long long)descs[l].tiles_m * descs[l].tiles_n;
+                    const long long lo = n * r / kXcds, hi = n * (r + 1) / kXcds;
+                    if (hi <= lo)
+                        continue;
+                    LayerDesc d = descs[l];
+                    d.tile_first = (int)lo;
+                    d.tile_begin = (int)begin;
+                    begin += hi - lo;
+                    segs.push_back(d);
+                }
+        } else {
+            segs = descs;
+        }
+        const int nseg = (int)segs.size();
         char *ws = static_cast<char *>(opts->workspace);
         LayerDesc *d_descs = reinterpret_cast<LayerDesc *>(ws);
         uint8_t *d_table = reinterpret_cast<uint8_t *>(
-            ws + round_up((size_t)L * sizeof(LayerDesc), kWsAlign));
+            ws + round_up((size_t)L * kXcds * sizeof(LayerDesc), kWsAlign));
         std::vector<uint8_t> table((size_t)L * 64, 0);
         for (int l = 0; l < L; ++l)
             for (int s = 0; s < S; ++s)
                 table[(size_t)l * S + s] = b_table[(size_t)l * S + s];
-        if (hipMemcpyAsync(d_descs, descs.data(), (size_t)L * sizeof(LayerDesc),
+        if (hipMemcpyAsync(d_descs, segs.data(), (size_t)nseg * sizeof(LayerDesc),
                            hipMemcpyHostToDevice, st) != hipSuccess)
             return TASQ_ERR_HIP;
         if (hipMemcpyAsync(d_table, table.data(), (size_t)L * S, hipMemcpyHostToDevice, st) !=
@@ -713,9 +799,9 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         for (int t = t_begin; t < t_end; ++t) {
             const int s = tasq_stage_of_step(t, S, T);
             const hipError_t e =
-                all_skinny ? tasq::launch_skinny_grouped(d_descs, L, (int)total, max_m, src,
+                all_skinny ? tasq::launch_skinny_grouped(d_descs, nseg, (int)total, max_m, src,
                                                          d_table, S, s, st)
-                           : launch_step(d_descs, L, (int)total, d_table, S, s, any_conv, st);
+                           : launch_step(d_descs, nseg, (int)total, d_table, S, s, any_conv, st);
             if (e != hipSuccess)
                 return TASQ_ERR_HIP;
         }

@@ -33,7 +33,9 @@ struct LayerDesc {
     int32_t bits;           // effective precision b (single calls)
     int32_t lr_r;           // rank of the low-rank branch (16 or 32) when lr_T is set
     int32_t tiles_m, tiles_n;
-    int32_t tile_begin;     // first tile of this layer in a grouped launch
+    int32_t tile_begin;     // first work unit of this segment in a grouped launch
+    int32_t tile_first;     // the segment's first tile within its layer
+    int32_t layer;          // row of the segment's layer in the (layer, stage) table
 };
 
 // Per-byte keep mask for b effective bits, replicated over the 4 bytes of a
