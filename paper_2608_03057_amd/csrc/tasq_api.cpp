@@ -113,11 +113,12 @@ int forced_tile() { return forced("TASQ_TILE", tasq::TILE_COUNT); }
 
 int forced_ptile() { return forced("TASQ_PTILE", tasq::PTILE_COUNT); }
 
-// Packed-weight tile of a single launch, from a measured sweep over the
-// DiT/UNet layer shapes: the 256x256 tile for very large products and for
-// long K with enough tiles, the 128x128 tile for narrow layers (N <= 1280)
-// with many tokens, the 4-wave 128x256 tile (two workgroups per CU) while
-// it gives a tile per CU, and 64x64 tiles below that.
+// Packed-weight tile of a single launch, from a sweep of every tile over the
+// DiT/UNet layer shapes with the Infinity Cache flushed before each launch:
+// the 256x256 tile once it gives at least 140 tiles (even half a wave of
+// 256x256 tiles beats 2-3 waves of smaller ones from about there), the
+// 4-wave 128x256 tile (two workgroups per CU) while it gives 200 tiles, and
+// 64x64 tiles below that.
 int pick_packed_tile(long long M, long long N, long long K)
 {
     const int f = forced_ptile();
@@ -125,13 +126,9 @@ int pick_packed_tile(long long M, long long N, long long K)
         return f;
     const long long t256 = ((M + 255) / 256) * ((N + 255) / 256);
     const long long t128x256 = ((M + 127) / 128) * ((N + 255) / 256);
-    if (M * N * K >= (1LL << 38))
+    if (t256 >= 140 || M * N * K >= (1LL << 38))
         return tasq::PTILE_256x256_K128_W8;
-    if (N <= 1280 && M >= 2048)
-        return tasq::PTILE_128x128_K64_W4;
-    if (K >= 4096 && t256 >= 128)
-        return tasq::PTILE_256x256_K128_W8;
-    if (t128x256 >= 256)
+    if (t128x256 >= 200)
         return tasq::PTILE_128x256_K128_W4;
     return tasq::PTILE_64x64_K128_W4;
 }
@@ -143,10 +140,9 @@ int pick_packed_grouped_tile()
     return f >= 0 ? f : tasq::PTILE_256x256_K128_W8;
 }
 
-// Tile used for a single (non-grouped) launch, from the measured sweep on
-// the DiT/UNet layer shapes: 256x256 tiles (8 waves, BK 128) while they still
-// give at least one tile per compute unit, 128x128 tiles for mid-size
-// problems, 64x64 tiles below that so that more workgroups cover the 256
+// Tile used for a single (non-grouped) launch, from the same sweep: 256x256
+// tiles (8 waves, BK 128) from 140 tiles up, 128x128 tiles while they give
+// 200 tiles, 64x64 tiles below that so that more workgroups cover the 256
 // compute units.
 int pick_tile(long long M, long long N)
 {
@@ -155,9 +151,9 @@ int pick_tile(long long M, long long N)
         return f;
     const long long t256 = ((M + 255) / 256) * ((N + 255) / 256);
     const long long t128 = ((M + 127) / 128) * ((N + 127) / 128);
-    if (t256 >= 256)
+    if (t256 >= 140)
         return tasq::TILE_256x256_K128_W8_PF1;
-    if (t128 >= 256)
+    if (t128 >= 200)
         return tasq::TILE_128x128_K128_W4_PF2;
     return tasq::TILE_64x64_K128_W4_PF2;
 }
