@@ -83,8 +83,17 @@ enum {
 /*
  * Optional controls; pass NULL for defaults (AUTO variant, no workspace).
  *   variant         TASQ_VARIANT_*.
- *   split_k         reserved, must be >= 0: every output tile accumulates all
- *                   of K in one workgroup.
+ *   split_k         single-layer calls with the row-major weight (not the
+ *                   packed, bit-plane or weight-streaming paths): 0 = the
+ *                   library may cut K into ranges when few output tiles
+ *                   would leave compute units idle, and does so only when
+ *                   workspace holds tasq_workspace_bytes(M, N, K) bytes;
+ *                   1 = never; s >= 2 = cut K into (at most) s ranges,
+ *                   which needs s*M*N*4 bytes of workspace
+ *                   (TASQ_ERR_WORKSPACE otherwise).  The ranges' int32
+ *                   partial sums are added in a fixed order, so every
+ *                   output is identical to the unsplit one.  Negative:
+ *                   TASQ_ERR_RANGE.  Schedules ignore it.
  *   W_planes        bit-plane copy of W as written by tasq_pack_planes; needed
  *                   by the BITPLANE variant (W may then be NULL).
  *   W_packed        W in the MFMA operand order as written by
@@ -92,7 +101,8 @@ enum {
  *                   by AUTO when present (W may then be NULL).
  *   workspace       device scratch, 256-byte aligned, owned by the caller;
  *                   holds the schedule's device-side layer list and bit
- *                   table.  Size from tasq_schedule_workspace_bytes.
+ *                   table (size from tasq_schedule_workspace_bytes), or a
+ *                   single layer's split-K partial sums (split_k).
  *                   Contents need no initialisation and are left
  *                   unspecified.
  *   workspace_bytes its size in bytes.
@@ -367,8 +377,9 @@ typedef struct tasq_layer {
 int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
                       int t_begin, int t_end, const tasq_opts *opts, void *stream);
 
-/* Workspace a single layer call may use: 0, no single-layer path needs one
- * (kept so that callers can size a workspace without knowing the kernels). */
+/* Workspace with which a single layer call (split_k = 0) cuts K into ranges:
+ * splits * M * N * 4 bytes, or 0 when it would not split this shape (enough
+ * output tiles, or K too short).  A smaller workspace runs unsplit. */
 size_t tasq_workspace_bytes(int M, int N, int K);
 
 /* Workspace for the grouped schedule over these layers (host array). */

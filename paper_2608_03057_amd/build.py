@@ -32,6 +32,7 @@ SOURCES = [
     "act_quant.hip",
     "weight_quant.hip",
     "skinny.hip",
+    "splitk.hip",
     "tiles.cpp",
     "cost.cpp",
     "tasq_api.cpp",

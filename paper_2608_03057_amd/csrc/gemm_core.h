@@ -104,6 +104,12 @@ __device__ __forceinline__ void st32(rsrc_t r, uint32_t off, uint32_t v)
     __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 2);
 }
 
+// A cacheable store, for data re-read right after (split-K partials).
+__device__ __forceinline__ void st32_cached(rsrc_t r, uint32_t off, uint32_t v)
+{
+    __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 0);
+}
+
 __device__ __forceinline__ v4i zero4() { return v4i{0, 0, 0, 0}; }
 
 // ------------------------------------------------- fallback (unaligned) loads
@@ -567,7 +573,7 @@ __device__ __forceinline__ v16f lowrank_block(const char *lds, int r, int rl, in
 // accumulator in lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32, so
 // each store instruction covers two 128-byte row segments.  Rows past M
 // fall past the buffer end and are dropped; columns past N carry kOOB.
-template <class C>
+template <class C, bool NT = true>
 __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
                                          const v16i (&acc)[C::FM][C::FN], int bits, char *lds)
 {
@@ -613,8 +619,12 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
             for (int i = 0; i < C::FM; ++i)
 #pragma unroll
                 for (int v = 0; v < 16; ++v)
-                    st32(ra, base + (uint32_t)(i * 32 + 8 * (v >> 2) + (v & 3)) * rowb,
-                         (uint32_t)acc[i][j][v]);
+                    if constexpr (NT)
+                        st32(ra, base + (uint32_t)(i * 32 + 8 * (v >> 2) + (v & 3)) * rowb,
+                             (uint32_t)acc[i][j][v]);
+                    else
+                        st32_cached(ra, base + (uint32_t)(i * 32 + 8 * (v >> 2) + (v & 3)) * rowb,
+                                    (uint32_t)acc[i][j][v]);
         }
         if (d.y) {
 #pragma unroll
@@ -724,6 +734,32 @@ k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
     epilogue<C>(d, m0, n0, acc, bits, reinterpret_cast<char *>(smA));
 }
 
+// Split-K: work unit u holds tile u / splits and the K range of split
+// sp = u % splits, [sp * kchunk, min(K, (sp + 1) * kchunk)) with kchunk a
+// multiple of BK; its int32 partial tile goes to part + sp * M * N ([M][N]),
+// summed in split order by k_split_finish.  The splits of one tile are
+// consecutive units, so they run in one XCD and share its L2.
+template <class C, int KIND>
+__global__ void __launch_bounds__(C::NT, C::OCC)
+k_masked_gemm_split(LayerDesc d, int32_t *part, int splits, int kchunk)
+{
+    __shared__ v4i smA[C::SMA];
+    __shared__ v4i smB[C::NSTAGE * C::BN * C::CPR];
+    const int u = xcd_remap(blockIdx.x, gridDim.x);
+    const int t = u / splits, sp = u - t * splits;
+    int tm, tn;
+    tile_coords(t, d.tiles_m, d.tiles_n, tm, tn);
+    const int m0 = tm * C::BM, n0 = tn * C::BN;
+    const int k0 = sp * kchunk;
+    const int k1 = min(d.K, k0 + kchunk);
+    v16i acc[C::FM][C::FN];
+    mainloop<C, true, KIND, false>(d, keep_mask_dword(d.bits), m0, n0, k0, k1, acc, smA, smB);
+    LayerDesc dp = d;
+    dp.acc = part + (size_t)sp * (size_t)d.M * (size_t)d.N;
+    dp.y = nullptr;
+    epilogue<C, false>(dp, m0, n0, acc, d.bits, reinterpret_cast<char *>(smA));
+}
+
 // ---------------------------------------------------------------- launchers
 
 template <class C>
@@ -753,6 +789,27 @@ hipError_t launch_single_cfg(const LayerDesc &din, bool aligned, hipStream_t str
     } else {
         hipLaunchKernelGGL((k_masked_gemm<C, false, KIND_LINEAR, false>), g, b, 0, stream, d);
     }
+    return hipGetLastError();
+}
+
+// Split-K partials of one aligned layer (see k_masked_gemm_split); the
+// caller checks splits * M * N * 4 < 2^31 (32-bit buffer offsets).
+template <class C>
+hipError_t launch_split_cfg(const LayerDesc &din, int32_t *part, int splits, int kchunk,
+                            hipStream_t stream)
+{
+    LayerDesc d = din;
+    fill_tiles<C>(d);
+    const long long grid = (long long)d.tiles_m * d.tiles_n * splits;
+    if (grid > 0x7fffffffLL || splits < 1 || kchunk % C::BK != 0)
+        return hipErrorInvalidValue;
+    dim3 g((unsigned)grid), b(C::NT);
+    if (d.kind == KIND_CONV3X3)
+        hipLaunchKernelGGL((k_masked_gemm_split<C, KIND_CONV3X3>), g, b, 0, stream, d, part,
+                           splits, kchunk);
+    else
+        hipLaunchKernelGGL((k_masked_gemm_split<C, KIND_LINEAR>), g, b, 0, stream, d, part,
+                           splits, kchunk);
     return hipGetLastError();
 }
 
@@ -793,7 +850,8 @@ hipError_t launch_grouped_cfg(const LayerDesc *d_descs, int L, int total_tiles,
     const TileOps &NAME()                                                                   \
     {                                                                                       \
         static const TileOps ops = {{CFG::BM, CFG::BN, CFG::BK}, &launch_single_cfg<CFG>,   \
-                                    &launch_planes_cfg<CFG>, &launch_grouped_cfg<CFG>};     \
+                                    &launch_planes_cfg<CFG>, &launch_grouped_cfg<CFG>,      \
+                                    &launch_split_cfg<CFG>};                                \
         return ops;                                                                         \
     }
 

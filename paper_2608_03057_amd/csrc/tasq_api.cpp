@@ -158,6 +158,46 @@ int pick_tile(long long M, long long N)
     return tasq::TILE_64x64_K128_W4_PF2;
 }
 
+// Split-K of single-layer calls with the row-major weight.  A layer with few
+// output tiles and a long K leaves most of the chip idle while each
+// workgroup walks all of K; cutting K into s ranges gives s times the
+// workgroups, at the price of writing and re-reading s int32 partial
+// outputs (summed in a fixed order, so the result is exact and identical).
+// Measured on the DiT/UNet shapes (cache flushed before each launch), the
+// partial traffic outweighs the gain unless K is long and the 256x256 tiles
+// few: the SDXL-Turbo 3x3 conv (K = 11520, 20 tiles) runs 75 -> 44 us with
+// 10 ranges, while K <= 5600 layers ran 0-3x slower split.
+constexpr int kSplitMinChunk = 1024;     // at least this much K per split
+constexpr int kSplitMinK = 8192;
+constexpr int kSplitMaxTiles = 64;
+
+int auto_splits(long long M, long long N, long long K)
+{
+    const long long t256 = ((M + 255) / 256) * ((N + 255) / 256);
+    if (t256 > kSplitMaxTiles || t256 == 0 || K < kSplitMinK)
+        return 1;
+    long long s = kComputeUnits / t256;
+    const long long smax = K / kSplitMinChunk;
+    if (s > smax)
+        s = smax;
+    return s >= 2 ? (int)s : 1;
+}
+
+// K range per split (a multiple of 128, the largest BK) and the resulting
+// number of non-empty splits.
+void split_geometry(int K, int s, int &kchunk, int &splits)
+{
+    const int per = (K + s - 1) / s;
+    kchunk = (per + 127) / 128 * 128;
+    splits = (K + kchunk - 1) / kchunk;
+}
+
+int pick_split_tile()
+{
+    const int f = forced_tile();
+    return f >= 0 ? f : tasq::TILE_256x256_K128_W8_PF1;
+}
+
 // Tile of the grouped per-step launch: 256x256, unless one 256x256 tile of
 // the longest-K layer costs more than a compute unit's even share of the
 // whole step; then that tile alone sets the step time (the 3x3 conv of the
@@ -230,7 +270,8 @@ bool skinny_source(const LayerDesc &d, const tasq_opts *o, tasq::SkinnyWeights &
     return d.W && aligned16(d.W);
 }
 
-int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
+int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream,
+                 bool allow_split = false)
 {
     if (d.M == 0 || d.N == 0)
         return TASQ_OK;
@@ -255,7 +296,31 @@ int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream)
         else
             aligned = (d.K % 16) == 0 && aligned16(d.X) && aligned16(d.W);
         aligned = aligned && fits_buffers(d);
-        e = tasq::tile_ops(pick_tile(d.M, d.N)).single(d, aligned, stream);
+        // Split-K: forced (split_k >= 2, needs the workspace) or chosen
+        // (split_k == 0, only with a large enough workspace).
+        const int req = o ? o->split_k : 0;
+        int splits = 1, kchunk = 0;
+        if (allow_split && req != 1 && d.K > 128) {
+            const int s = req >= 2 ? req : auto_splits(d.M, d.N, d.K);
+            if (s > 1) {
+                split_geometry(d.K, s, kchunk, splits);
+                const unsigned long long need = 4ULL * splits * (unsigned long long)d.M * d.N;
+                const bool ws_ok = o && o->workspace && o->workspace_bytes >= need &&
+                                   need < (1ULL << 31);
+                if (!ws_ok && req >= 2)
+                    return TASQ_ERR_WORKSPACE;
+                if (!ws_ok || !aligned)
+                    splits = 1;
+            }
+        }
+        if (splits > 1) {
+            int32_t *part = static_cast<int32_t *>(o->workspace);
+            e = tasq::tile_ops(pick_split_tile()).split(d, part, splits, kchunk, stream);
+            if (e == hipSuccess)
+                e = tasq::launch_split_finish(d, part, splits, stream);
+        } else {
+            e = tasq::tile_ops(pick_tile(d.M, d.N)).single(d, aligned, stream);
+        }
     }
     return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
 }
@@ -425,10 +490,15 @@ size_t tasq_planes_bytes(int N, int K)
 
 size_t tasq_workspace_bytes(int M, int N, int K)
 {
-    (void)M;
-    (void)N;
-    (void)K;
-    return 0;   // no single-layer path uses a workspace
+    if (M <= 0 || N <= 0 || K <= 128)
+        return 0;
+    const int s = auto_splits(M, N, K);
+    if (s < 2)
+        return 0;
+    int kchunk, splits;
+    split_geometry(K, s, kchunk, splits);
+    const unsigned long long need = 4ULL * splits * (unsigned long long)M * N;
+    return need < (1ULL << 31) ? (size_t)need : 0;
 }
 
 int tasq_masked_linear(const int8_t *X, const int8_t *W, float sx, const float *sw,
@@ -454,7 +524,7 @@ int tasq_masked_linear(const int8_t *X, const int8_t *W, float sx, const float *
         return TASQ_ERR_BITS;
     LayerDesc d = make_desc(L, opts);
     d.bits = b;
-    return launch_layer(d, opts, static_cast<hipStream_t>(stream));
+    return launch_layer(d, opts, static_cast<hipStream_t>(stream), true);
 }
 
 int tasq_masked_conv3x3(const int8_t *X, const int8_t *W, float sx, const float *sw,
@@ -490,7 +560,7 @@ int tasq_masked_conv3x3(const int8_t *X, const int8_t *W, float sx, const float 
         return TASQ_ERR_BITS;
     LayerDesc d = make_desc(L, opts);
     d.bits = b;
-    return launch_layer(d, opts, static_cast<hipStream_t>(stream));
+    return launch_layer(d, opts, static_cast<hipStream_t>(stream), true);
 }
 
 int tasq_pack_planes(const int8_t *W, int N, int K, uint32_t *planes_out, void *stream)

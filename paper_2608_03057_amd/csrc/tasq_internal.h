@@ -61,7 +61,14 @@ struct TileOps {
     hipError_t (*grouped)(const LayerDesc *d_descs, int L, int total_tiles,
                           const uint8_t *d_table, int S, int stage, bool any_conv,
                           hipStream_t stream);
+    // Split-K partials (aligned operands only) into part[splits][M][N].
+    hipError_t (*split)(const LayerDesc &d, int32_t *part, int splits, int kchunk,
+                        hipStream_t stream);
 };
+
+// Sums split-K partials and applies the dequantisation epilogue (splitk.hip).
+hipError_t launch_split_finish(const LayerDesc &d, const int32_t *part, int splits,
+                               hipStream_t stream);
 
 // Tile configurations, indexed by TileId.
 enum TileId : int {

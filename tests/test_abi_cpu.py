@@ -124,6 +124,25 @@ def test_packed_variant_accepts_missing_w_only_with_packed():
     assert lin(W=None, M=0, opts=opts(variant=_lib.VARIANT_PACKED)) == _lib.TASQ_ERR_LAYOUT
 
 
+def test_workspace_bytes_split_k():
+    """Workspace of the split-K choice: only for K >= 8192 with at most 64
+    tiles of 256x256; s ranges of at least 1024 of K, as many as fill the 256
+    CUs once, rounded to 128-wide chunks (the SDXL-Turbo conv: 11 ranges
+    asked, chunks of 1152, 10 used)."""
+    assert L.tasq_workspace_bytes(1024, 1280, 11520) == 10 * 1024 * 1280 * 4
+    assert L.tasq_workspace_bytes(256, 256, 16384) == 16 * 256 * 256 * 4
+    assert L.tasq_workspace_bytes(1024, 1280, 5120) == 0       # K too short
+    assert L.tasq_workspace_bytes(8192, 3456, 1152) == 0      # enough tiles
+    assert L.tasq_workspace_bytes(1024, 1280, 1280) == 0      # K too short
+    assert L.tasq_workspace_bytes(0, 1280, 5120) == 0
+
+
+def test_forced_split_without_workspace_rejected():
+    assert lin(M=300, N=64, K=512, opts=opts(split_k=4)) == _lib.TASQ_ERR_WORKSPACE
+    assert lin(M=300, N=64, K=512, opts=opts(split_k=4, workspace=FAKE,
+                                              workspace_bytes=1024)) == _lib.TASQ_ERR_WORKSPACE
+
+
 def test_packed_weight_bytes():
     assert L.tasq_packed_weight_bytes(1152, 1152) == 1152 * 1152
     assert L.tasq_packed_weight_bytes(33, 129) == 64 * 256

@@ -1,0 +1,116 @@
+"""GPU parity of split-K single-layer calls: K cut into ranges whose int32
+partials are summed in a fixed order, then dequantised with every epilogue
+term.  Accumulators must equal the oracle's bit for bit at every split
+count; fp32 outputs meet the same bars as the unsplit kernels (the finish
+kernel forms the same expression, with the low-rank branch as fp32 FMAs)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_03057_amd as T
+from paper_2608_03057_amd import inputs
+from test_gpu_parity import DEV, check_outputs, f32
+from test_gpu_lowrank import branch, dev_bf16, eps_lr, lr_magnitude
+
+pytestmark = pytest.mark.gpu
+SX = f32(0.02)
+
+
+def workspace(nbytes):
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=DEV)
+
+
+@pytest.mark.parametrize("split", [2, 3, 5, 8])
+@pytest.mark.parametrize("shape", [(300, 200, 1152), (257, 33, 1008), (512, 512, 4608)])
+def test_forced_split_linear(split, shape):
+    M, N, K = shape
+    X, W, sw, bias = inputs.random_case(M + N + K + split, M, N, K)
+    X[0, 0] = -128
+    W[0, 0] = -128
+    ws = workspace(split * M * N * 4)
+    for b in (8, 5, 1):
+        use_bias = bias if b != 5 else None
+        acc, y = T.masked_linear(X.to(DEV), W.to(DEV), SX, sw.to(DEV), b,
+                                 None if use_bias is None else use_bias.to(DEV), workspace=ws,
+                                 split_k=split)
+        _, y2 = T.masked_linear(X.to(DEV), W.to(DEV), SX, sw.to(DEV), b, want_acc=False,
+                                workspace=ws, split_k=split)
+        torch.cuda.synchronize()
+        ra, ry = oracle.masked_linear(X, W, SX, sw, b, use_bias)
+        check_outputs(acc, y, ra, ry, SX, sw, use_bias, f"split {split} {shape} b={b}")
+        _, ry2 = oracle.masked_linear(X, W, SX, sw, b)
+        check_outputs(None, y2, ra, ry2, SX, sw, None, f"split {split} {shape} y-only b={b}")
+
+
+@pytest.mark.parametrize("split", [2, 4])
+def test_forced_split_conv(split):
+    H, Wd, C, N = 9, 9, 48, 70
+    X, _, sw, bias = inputs.random_case(77 + split, H * Wd, N, C)
+    X = X.reshape(H, Wd, C)
+    Wt = inputs.random_case(78 + split, 1, N, 9 * C)[1].reshape(N, 3, 3, C)
+    ws = workspace(split * H * Wd * N * 4)
+    for b in (8, 3):
+        acc, y = T.masked_conv3x3(X.to(DEV), Wt.to(DEV), SX, sw.to(DEV), b, bias.to(DEV),
+                                  workspace=ws, split_k=split)
+        torch.cuda.synchronize()
+        ra, ry = oracle.conv3x3(X, Wt, SX, sw, b, bias)
+        check_outputs(acc, y, ra, ry, SX, sw, bias, f"split conv {split} b={b}")
+
+
+def test_forced_split_every_epilogue_term():
+    M, N, K = 300, 200, 1152
+    Wf = inputs.weights_f32(81, N, K)
+    Qd, alpha, zwd, swd = T.quantize_weights(Wf.to(DEV))
+    rQ, _, zw, rsw = oracle.weight_quant(Wf)
+    Wc = (rQ.astype(np.int16) - 128).astype(np.int8)
+    x, D, U = branch(82, M, K, 32, N)
+    q, params, Tg = T.quantize_activations_lowrank(x.to(DEV), dev_bf16(D))
+    ax, zx, Qx = oracle.act_quant(x)
+    Xc = (Qx.astype(np.int16) - 128).astype(np.int8)
+    rs = T.row_sums(q)
+    cs = T.weight_colsums(Qd)
+    ws = workspace(4 * M * N * 4)
+    acc, y = T.masked_linear(q, Qd, 0.0, swd, 6, act=params, colsums=cs,
+                             lowrank=(Tg, dev_bf16(U)), wzero=(zwd, rs), workspace=ws, split_k=4)
+    torch.cuda.synchronize()
+    ra, ry = oracle.layer_dequant(Xc, Wc, rsw, 6, act=(ax, zx), zw=zw)
+    _, lr64 = oracle.lowrank(x, D, U)
+    _, S = lr_magnitude(x, D, U)
+    assert np.array_equal(acc.cpu().numpy(), ra)
+    R = oracle.row_sums(Xc) + K * (128.0 - zx)
+    corr = (128.0 - zx) * oracle.weight_colsums(Wc)[5].astype(np.float64)
+    scale = ax * rsw.astype(np.float64)
+    mag = np.abs(scale) * (np.abs(ra.astype(np.float64)) + np.abs(corr)
+                           + np.abs((128.0 - zw.astype(np.float64)) * R[:, None]))
+    err = np.abs(y.cpu().numpy().astype(np.float64) - (ry + lr64))
+    assert float(np.max(err - 1e-6 * mag - eps_lr(K) * S)) <= 0.0
+
+
+def test_auto_split_full_size_conv_equals_unsplit():
+    """The SDXL-Turbo 3x3 conv (1024 pixels, K = 11520 -> 1280) with the
+    workspace the library asks for: split automatically, the int32 output
+    equal to the unsplit call's and y within the bar on sampled rows."""
+    wl = inputs.workload(3)
+    l = 8
+    spec = wl.layers[l]
+    X = inputs.x_full(wl, l).to(DEV)
+    Wt = inputs.w_full(wl, l).reshape(spec.N, 3, 3, spec.C).to(DEV)
+    sw = inputs.sw_full(wl, l).to(DEV)
+    need = T.workspace_bytes(spec.M, spec.N, spec.K)
+    assert need > 0
+    ws = workspace(need)
+    a1, y1 = T.masked_conv3x3(X, Wt, SX, sw, 6, workspace=ws)
+    a2, y2 = T.masked_conv3x3(X, Wt, SX, sw, 6)
+    torch.cuda.synchronize()
+    assert torch.equal(a1, a2)
+    assert torch.equal(y1, y2)
+
+
+def test_forced_split_needs_workspace():
+    X, W, sw, _ = inputs.random_case(5, 300, 64, 512)
+    with pytest.raises(T.TasqError):
+        T.masked_linear(X.to(DEV), W.to(DEV), SX, sw.to(DEV), 8, split_k=4)
+    small = workspace(1024)
+    with pytest.raises(T.TasqError):
+        T.masked_linear(X.to(DEV), W.to(DEV), SX, sw.to(DEV), 8, split_k=4, workspace=small)
