@@ -493,6 +493,9 @@ def main():
     ap.add_argument("--shape-sweep", action="store_true",
                     help="only time the single layers of the four per-shape workloads (median / "
                          "p10 / p90 over 50 cache-flushed launches) and print one JSON line each")
+    ap.add_argument("--skinny-only", action="store_true",
+                    help="only time the 112-layer schedule at M = 16 (weight streaming) and print "
+                         "its JSON")
     ap.add_argument("--no-skinny", action="store_true",
                     help="skip the extra weight-streaming (M=16) schedule measurement")
     ap.add_argument("--no-act", action="store_true",
@@ -530,6 +533,12 @@ def main():
     if args.skinny_sweep:
         for row in skinny_sweep("cuda"):
             print(json.dumps(row), flush=True)
+        return
+    if args.skinny_only:
+        wl = inputs.workload(4)
+        keep = [(None, inputs.w_full(wl, l).to("cuda"), inputs.sw_full(wl, l).to("cuda"), None)
+                for l in range(len(wl.layers))]
+        print(json.dumps(skinny_schedule(wl, inputs.b_table(wl), keep, "cuda")), flush=True)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the path shards by "
