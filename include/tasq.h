@@ -199,13 +199,17 @@ int tasq_masked_conv3x3(const int8_t *X, const int8_t *W, float sx, const float 
  * Bit-plane relayout of a stored weight (App. G.2: plane p holds bit p of
  * the two's-complement code, p = 0 least significant).
  *   W          int8 [N][K] device (read only).
- *   planes_out uint32 [8][KB][N][4] device, KB = ceil(K / 128): word
- *              planes[q][kb][n][w] holds, in bit 8*(e%4) + e/4, bit
- *              p = 7 - q of W[n][128*kb + 32*w + e] (e = 0..31), so a shift
- *              by s and a mask 0x01010101 yield the bits of elements
- *              4s..4s+3 in four consecutive bytes.  Plane q = 0 is the sign
- *              plane; the top b planes are the contiguous prefix of b*KB*N*4
- *              words.  Bits past K are zero.  Size tasq_planes_bytes(N, K).
+ *   planes_out uint32 [8][KB][N][4] device, KB = ceil(K / 128): the
+ *              words planes[q][kb][n][0..3] hold bit p = 7 - q of
+ *              W[n][128*kb + r], r = 0..127.  With s = r / 32, h = (r%32)/16,
+ *              i = (r%16)/4, c = r%4, element r sits in word 2h + s/2 at bit
+ *              (8c + 4(s%2) + i + p) mod 32: each word holds one 16-element
+ *              half of two 32-element sub-steps, and plane p's word is
+ *              rotated left by p, so that the planes' bits of four
+ *              consecutive elements merge with one AND-OR per plane and one
+ *              rotate.  Plane q = 0 is the sign plane; the top b planes are
+ *              the contiguous prefix of b*KB*N*4 words.  Bits past K are
+ *              zero.  Size tasq_planes_bytes(N, K).
  * A one-time conversion of the stored buffer, not a per-step cost.  A
  * caller that keeps only the planes (and passes W = NULL with the BITPLANE
  * variant) stores the weight once, at the same 8 bits per element.

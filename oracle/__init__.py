@@ -210,8 +210,9 @@ def conv3x3_entries(X, Wt, sx, sw, b, pix, cols, bias=None):
 
 def pack_planes(W) -> np.ndarray:
     """uint32 [8 x ceil(K/128) x N x 4] bit planes, most significant plane
-    first; word w of block kb holds elements 128*kb + 32*w .. +31 of a row,
-    element e of the word at bit 8*(e % 4) + e // 4."""
+    first (q = 7 - p).  Element j of a row, r = j % 128, with s = r // 32,
+    h = (r % 32) // 16, i = (r % 16) // 4, c = r % 4, lands in word
+    2*h + s // 2 of block j // 128 at bit (8*c + 4*(s % 2) + i + p) % 32."""
     W = _np(W, np.int8)
     N, K = W.shape
     KB = (K + 127) // 128

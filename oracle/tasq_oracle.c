@@ -249,10 +249,14 @@ int oracle_conv3x3_entries(const int8_t *X, const int8_t *Wt, double sx, const f
  * Bit planes of the stored two's-complement weight (App. G.2: plane p is bit
  * p of the code, p = 0 the least significant).  Layout, in uint32 words:
  *   planes[q][kb][n][w],  q = 7 - p (most significant plane first, so the
- *   top b planes are one contiguous prefix), kb = j / 128, w = (j % 128) / 32.
- * Within a word, element e = j % 32 of the word's 32 elements sits at bit
- * 8 * (e % 4) + e / 4 (group of four e / 4 in bit e / 4 of each byte).
- * KB = ceil(K / 128); bits past K are zero.
+ *   top b planes are one contiguous prefix), kb = j / 128.
+ * Element j of row n, with r = j % 128, is sub-step s = r / 32, half
+ * h = (r % 32) / 16, group i = (r % 16) / 4 and byte c = r % 4 of its
+ * 16-element half; it goes to word w = 2 h + s / 2, at bit
+ *   (8 c + g + p) mod 32,  g = 4 (s % 2) + i.
+ * (A word holds one half's 16 elements of two sub-steps; plane p's word is
+ * the plain byte-sliced word rotated left by p bits.)  KB = ceil(K / 128);
+ * bits past K are zero.  A storage layout of the same bits, not arithmetic.
  */
 int oracle_pack_planes(const int8_t *W, int64_t N, int64_t K, uint32_t *planes)
 {
@@ -264,9 +268,11 @@ int oracle_pack_planes(const int8_t *W, int64_t N, int64_t K, uint32_t *planes)
         for (int64_t n = 0; n < N; ++n)
             for (int64_t j = 0; j < K; ++j) {
                 uint32_t bit = ((uint32_t)(uint8_t)W[n * K + j] >> p) & 1u;
-                int64_t word = ((q * KB + j / 128) * N + n) * 4 + (j % 128) / 32;
-                int e = (int)(j % 32);
-                planes[word] |= bit << (8 * (e % 4) + e / 4);
+                int r = (int)(j % 128);
+                int s = r / 32, h = (r % 32) / 16, i = (r % 16) / 4, c = r % 4;
+                int w = 2 * h + s / 2, g = 4 * (s % 2) + i;
+                int64_t word = ((q * KB + j / 128) * N + n) * 4 + w;
+                planes[word] |= bit << ((8 * c + g + p) % 32);
             }
     }
     return ORACLE_OK;

@@ -28,6 +28,7 @@
 namespace tasq {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
@@ -95,6 +96,11 @@ __device__ __forceinline__ v4i ld16(rsrc_t r, uint32_t off)
     return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
+__device__ __forceinline__ v2i ld8(rsrc_t r, uint32_t off)
+{
+    return __builtin_bit_cast(v2i, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+
 // Output stores carry the non-temporal hint (cache-policy bit 1 on gfx950):
 // the outputs are written once and never re-read by the kernel, and without
 // the hint they evict the activation and weight tiles that neighbouring
@@ -156,21 +162,33 @@ __device__ __forceinline__ v4i load_conv_any(const LayerDesc &d, int m, int kbyt
 
 // ----------------------------------------------------------- bit planes
 
-// Four consecutive weights of plane q, placed at bit 7 - q of four bytes and
-// OR-ed into acc.  Plane words keep element 4s + j at bit 8j + s, so rotating
-// right by s - (7 - q) moves the bits of elements 4s .. 4s+3 to bit 7 - q of
-// bytes 0..3 (other bits are masked off): one v_alignbit_b32 and one
-// v_and_or_b32 per four weights per plane.
-__device__ __forceinline__ uint32_t plane_group(uint32_t word, int s, int up, uint32_t acc)
+// Plane words are stored rotated (tasq_pack_planes): element (group g, byte
+// c) of plane p's word sits at bit (8c + g + p) mod 32, so for one group the
+// planes' bits land on disjoint positions 0x01010101 << ((g + p) % 8).
+// plane_bits adds plane p's bits of group g to a merged word with one
+// v_and_or_b32; plane_place rotates the merged word right by g, which puts
+// bit p of each of the group's four codes at bit p of bytes 0..3.
+__device__ __forceinline__ uint32_t plane_bits(uint32_t word, int g, int p, uint32_t merged)
 {
-    const uint32_t rot = __builtin_amdgcn_alignbit(word, word, (uint32_t)(s - up) & 31u);
-    return (rot & (0x01010101u << up)) | acc;
+    uint32_t r = (word & (0x01010101u << ((g + p) & 7))) | merged;
+    // An empty register barrier: left to itself the compiler re-associates
+    // a chain of these into separate ANDs and three-input ORs (about 1.5
+    // instructions per plane instead of one v_and_or_b32).  The instruction
+    // itself stays compiler-generated, so the wait states that a VALU result
+    // needs before a matrix instruction reads it are still inserted.
+    asm("" : "+v"(r));
+    return r;
 }
 
-// Chunk (row n, kbyte..kbyte+15) of W_b rebuilt from the top b bit planes
-// (App. G.2: the b-bit operand is the top b planes of the stored buffer;
-// the dropped planes are never read).  Plane q contributes bit 7 - q of
-// each byte; the result is the two's-complement byte of W_b.
+__device__ __forceinline__ uint32_t plane_place(uint32_t merged, int g)
+{
+    return __builtin_amdgcn_alignbit(merged, merged, (uint32_t)g);
+}
+
+// Chunk (row n, kbyte..kbyte+15, kbyte a multiple of 16) of W_b rebuilt from
+// the top b bit planes (App. G.2: the b-bit operand is the top b planes of
+// the stored buffer; the dropped planes are never read).  Plane q holds bit
+// 7 - q of each code; the result is the two's-complement byte of W_b.
 __device__ __forceinline__ v4i load_planes(const uint32_t *P, int N, int K, int b, int n,
                                            int kbyte)
 {
@@ -178,18 +196,20 @@ __device__ __forceinline__ v4i load_planes(const uint32_t *P, int N, int K, int 
         return zero4();
     const int KB = (K + 127) >> 7;
     const size_t plane_stride = (size_t)KB * (size_t)N * 4;
-    const uint32_t *base = P + ((size_t)(kbyte >> 7) * N + n) * 4 + ((kbyte & 127) >> 5);
-    const int s0 = (kbyte & 16) >> 2;        // groups 0..3 or 4..7 of the word
+    const int s = (kbyte & 127) >> 5, h = (kbyte >> 4) & 1;
+    const uint32_t *base = P + ((size_t)(kbyte >> 7) * N + n) * 4 + 2 * h + (s >> 1);
+    const int g0 = 4 * (s & 1);
     uint32_t d0 = 0, d1 = 0, d2 = 0, d3 = 0;
     for (int q = 0; q < b; ++q) {
         const uint32_t w = base[q * plane_stride];
-        const int up = 7 - q;
-        d0 = plane_group(w, s0 + 0, up, d0);
-        d1 = plane_group(w, s0 + 1, up, d1);
-        d2 = plane_group(w, s0 + 2, up, d2);
-        d3 = plane_group(w, s0 + 3, up, d3);
+        const int p = 7 - q;
+        d0 = plane_bits(w, g0 + 0, p, d0);
+        d1 = plane_bits(w, g0 + 1, p, d1);
+        d2 = plane_bits(w, g0 + 2, p, d2);
+        d3 = plane_bits(w, g0 + 3, p, d3);
     }
-    return v4i{(int)d0, (int)d1, (int)d2, (int)d3};
+    return v4i{(int)plane_place(d0, g0 + 0), (int)plane_place(d1, g0 + 1),
+               (int)plane_place(d2, g0 + 2), (int)plane_place(d3, g0 + 3)};
 }
 
 // ------------------------------------------------------------------ staging

@@ -1,10 +1,15 @@
 // Bit-plane relayout of the stored weight buffer (one-time).
 //
-// planes[q][kb][n][w]: bit 8*(e%4) + e/4 holds bit (7 - q) of element
-// W[n][128*kb + 32*w + e] (App. G.2: plane p is bit p of the two's-complement
-// code; most significant plane first so that the top b planes form one
-// contiguous prefix).  With this order, (word >> s) & 0x01010101 puts the
-// bits of elements 4s .. 4s+3 in the low bit of four consecutive bytes.
+// planes[q][kb][n][w] holds bit p = 7 - q of the codes of W[n][128*kb ..]
+// (App. G.2: plane p is bit p of the two's-complement code; most significant
+// plane first so that the top b planes form one contiguous prefix).  The
+// 128 elements of a block split into four sub-steps of 32 (s), each into two
+// halves of 16 (h) of four groups (i) of four bytes (c).  Word w = 2h + t
+// holds half h of sub-steps 2t and 2t+1; element (s, h, i, c) sits at bit
+// (8c + g + p) mod 32 with g = 4(s % 2) + i.  Rotating each plane's word left
+// by p puts the b planes' bits of one group g on disjoint positions, so the
+// reader merges them with one AND-OR per plane and one rotate right by g
+// yields bit p of each of the group's four bytes.
 #include "tasq_internal.h"
 
 namespace tasq {
@@ -15,26 +20,28 @@ __global__ void k_pack_planes(const int8_t *__restrict__ W, int N, int K, int KB
                               uint32_t *__restrict__ planes)
 {
     const long long words = (long long)KB * N * 4;
-    for (long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x; g < words;
-         g += (long long)gridDim.x * blockDim.x) {
-        const int w = (int)(g & 3);
-        const long long rest = g >> 2;
+    for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < words;
+         idx += (long long)gridDim.x * blockDim.x) {
+        const int w = (int)(idx & 3);
+        const long long rest = idx >> 2;
         const int n = (int)(rest % N);
         const int kb = (int)(rest / N);
-        const int j0 = kb * 128 + w * 32;
+        const int h = w >> 1, t = w & 1;
         uint32_t pw[8] = {0, 0, 0, 0, 0, 0, 0, 0};
         const int8_t *row = W + (size_t)n * (size_t)K;
-        for (int i = 0; i < 32; ++i) {
-            const int j = j0 + i;
+        for (int e = 0; e < 32; ++e) {
+            const int sl = e >> 4;                 // which of the word's two sub-steps
+            const int i = (e >> 2) & 3, c = e & 3;
+            const int j = kb * 128 + 32 * (2 * t + sl) + 16 * h + 4 * i + c;
             const uint32_t v = j < K ? (uint32_t)(uint8_t)row[j] : 0u;
-            const int pos = 8 * (i & 3) + (i >> 2);
+            const int g = 4 * sl + i;
 #pragma unroll
             for (int p = 0; p < 8; ++p)
-                pw[p] |= ((v >> p) & 1u) << pos;
+                pw[p] |= ((v >> p) & 1u) << ((8 * c + g + p) & 31);
         }
 #pragma unroll
         for (int p = 0; p < 8; ++p)
-            planes[(size_t)(7 - p) * (size_t)words + (size_t)g] = pw[p];
+            planes[(size_t)(7 - p) * (size_t)words + (size_t)idx] = pw[p];
     }
 }
 

@@ -8,8 +8,8 @@
 //     contiguous 1 KB, so a wave's weight loads are fully coalesced;
 //   * bit planes, reading only the top b planes (App. G.2; the dropped
 //     planes are never fetched): b/8 byte per weight, rebuilt into the
-//     two's-complement bytes of W_b in registers (a rotate and an AND-OR
-//     place 4 bits of a plane in 4 bytes).
+//     two's-complement bytes of W_b in registers (one AND-OR per plane and
+//     one rotate per 4 weights, from the rotated plane words).
 // A workgroup owns 32 output channels; its 8 waves take interleaved
 // 128-byte K blocks and compute acc^T = W_b X^T with v_mfma_i32_32x32x32_i8
 // (A = 32 weight rows, B = up to 32 activation rows per m-tile).  The waves'
@@ -30,20 +30,12 @@ constexpr int SK_PAD = 65;            // LDS row pitch (ints) of the reduction b
 
 enum SkinnySource : int { SRC_ROWS = 0, SRC_PACKED = 1, SRC_PLANES = 2 };
 
-// The lane half's 16 weights of plane word w (groups 4h .. 4h+3) placed at
-// bit `up` of 16 bytes and OR-ed into 4 dwords.
-__device__ __forceinline__ void plane_half(uint32_t w, int h, int up, v4i &acc)
-{
-    acc.x = (int)plane_group(w, 4 * h + 0, up, (uint32_t)acc.x);
-    acc.y = (int)plane_group(w, 4 * h + 1, up, (uint32_t)acc.y);
-    acc.z = (int)plane_group(w, 4 * h + 2, up, (uint32_t)acc.z);
-    acc.w = (int)plane_group(w, 4 * h + 3, up, (uint32_t)acc.w);
-}
-
-// Output channels 32*nb .. 32*nb+31 of layer d at b bits.  red holds
-// SK_WAVES * MT * 16 rows of SK_PAD ints.
-template <int SRC, int MT>
-__device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, int *red)
+// Weight stream of output channels 32*nb .. 32*nb+31 of layer d at b bits:
+// each wave's int32 partial sums go to red, SK_WAVES * MT * 16 rows of
+// SK_PAD ints.  BP is b as a compile-time count for the plane source (one
+// copy of the loop per b, so the plane loop has no branches), 0 otherwise.
+template <int SRC, int MT, int BP>
+__device__ __forceinline__ void skinny_stream(const LayerDesc &d, int b, int nb, int *red)
 {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -71,10 +63,11 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
     uint32_t offW;
     uint32_t plane_stride = 0;
     if constexpr (SRC == SRC_PLANES) {
-        // words planes[q][kb][n][0..3]
+        // words planes[q][kb][n][2h], [2h + 1]: this lane half's 16 weights
+        // of sub-steps 0, 1 and of 2, 3
         plane_stride = (uint32_t)nkb * (uint32_t)d.N * 16u;
         rW = make_rsrc(d.P, 8u * plane_stride);
-        offW = n < d.N ? (uint32_t)n * 16u : kOOB;
+        offW = n < d.N ? (uint32_t)n * 16u + 8u * (uint32_t)h : kOOB;
     } else if constexpr (SRC == SRC_PACKED) {
         // unit (nb, 4*kb + s), this lane's 16 bytes
         const int NB = (d.N + 31) / 32;
@@ -87,13 +80,11 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
 
     // One K block's operands: every load of the block is issued before any
     // is used.  Latency is covered by the other waves of the CU rather than
-    // by a second buffer, which would halve the waves that fit.  Planes: the
-    // two lanes of a weight row (halves h = 0, 1) need the same plane words,
-    // so lane half h loads planes h, h+2, .. (64 distinct 16-byte chunks per
-    // load) and v_permlane32_swap hands each half the other's words.
-    constexpr int NWORDS = 4;
+    // by a second buffer, which would halve the waves that fit.  Planes: one
+    // 8-byte load per plane (a wave reads 32 rows x 16 contiguous bytes).
     struct Block {
-        v4i w[NWORDS];
+        v4i w[4];
+        v2i pw[8];
         v4i x[4][MT];
     };
     auto load = [&](int kb, Block &bl) {
@@ -101,11 +92,10 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
         if constexpr (SRC == SRC_PLANES) {
             const uint32_t base = offW + (uint32_t)kb * (uint32_t)d.N * 16u;
 #pragma unroll
-            for (int qq = 0; qq < 4; ++qq) {
-                const int q = 2 * qq + h;
-                bl.w[qq] = zero4();
-                if (2 * qq < b)
-                    bl.w[qq] = ld16(rW, q < b ? base + (uint32_t)q * plane_stride : kOOB);
+            for (int q = 0; q < 8; ++q) {
+                bl.pw[q] = v2i{0, 0};
+                if (q < BP)
+                    bl.pw[q] = ld8(rW, base + (uint32_t)q * plane_stride);
             }
         } else {
 #pragma unroll
@@ -130,20 +120,22 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
         for (int s = 0; s < 4; ++s) {
             v4i wq = zero4();
             if constexpr (SRC == SRC_PLANES) {
+                // groups 4(s % 2) .. +3 of word s / 2 of each plane
+                uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
+                const int g0 = 4 * (s & 1);
 #pragma unroll
-                for (int qq = 0; qq < 4; ++qq) {
-                    if (2 * qq < b) {
-                        // even plane 2qq from the lower lanes, odd plane
-                        // 2qq+1 (zero past b) from the upper lanes
-                        const v4i wv = bl.w[qq];
-                        const int words[4] = {wv.x, wv.y, wv.z, wv.w};
-                        const int mine = words[s];
-                        const auto sw2 = __builtin_amdgcn_permlane32_swap(mine, mine, false, false);
-                        plane_half((uint32_t)sw2[0], h, 7 - 2 * qq, wq);
-                        if (2 * qq + 1 < b)
-                            plane_half((uint32_t)sw2[1], h, 6 - 2 * qq, wq);
+                for (int q = 0; q < 8; ++q) {
+                    if (q < BP) {
+                        const uint32_t w = (uint32_t)(s < 2 ? bl.pw[q].x : bl.pw[q].y);
+                        const int p = 7 - q;
+                        m0 = plane_bits(w, g0 + 0, p, m0);
+                        m1 = plane_bits(w, g0 + 1, p, m1);
+                        m2 = plane_bits(w, g0 + 2, p, m2);
+                        m3 = plane_bits(w, g0 + 3, p, m3);
                     }
                 }
+                wq = v4i{(int)plane_place(m0, g0 + 0), (int)plane_place(m1, g0 + 1),
+                         (int)plane_place(m2, g0 + 2), (int)plane_place(m3, g0 + 3)};
             } else {
                 wq = bl.w[s];
                 wq.x &= msk;
@@ -174,7 +166,31 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
 #pragma unroll
         for (int v = 0; v < 16; ++v)
             red[((wave * MT + mt) * 16 + v) * SK_PAD + lane] = acc[mt][v];
+}
+
+// Output channels 32*nb .. 32*nb+31 of layer d at b bits: the weight stream,
+// then the fixed-order reduction of the waves' partials and the epilogue.
+template <int SRC, int MT>
+__device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, int *red)
+{
+    if constexpr (SRC == SRC_PLANES) {
+        switch (b) {
+        case 1: skinny_stream<SRC, MT, 1>(d, b, nb, red); break;
+        case 2: skinny_stream<SRC, MT, 2>(d, b, nb, red); break;
+        case 3: skinny_stream<SRC, MT, 3>(d, b, nb, red); break;
+        case 4: skinny_stream<SRC, MT, 4>(d, b, nb, red); break;
+        case 5: skinny_stream<SRC, MT, 5>(d, b, nb, red); break;
+        case 6: skinny_stream<SRC, MT, 6>(d, b, nb, red); break;
+        case 7: skinny_stream<SRC, MT, 7>(d, b, nb, red); break;
+        default: skinny_stream<SRC, MT, 8>(d, b, nb, red); break;
+        }
+    } else {
+        skinny_stream<SRC, MT, 0>(d, b, nb, red);
+    }
     __syncthreads();
+
+    const int tid = threadIdx.x;
+    const int n0 = nb * 32;
 
     // Thread t writes channel n0 + t%32 of tokens t/32 + 16*i: 32 threads
     // cover one 128-byte output row segment.

@@ -261,29 +261,48 @@ def test_conv_entries_match_full():
 # ---------------------------------------------------------------- bit planes
 
 def unpack(planes, K):
-    """Bit plane q (q = 7 - p) back to a {0,1} int64 array [8 x N x K]."""
+    """Bit plane q (q = 7 - p) back to a {0,1} int64 array [8 x N x K].
+    Element j: r = j % 128 is sub-step r // 32, half (r % 32) // 16, group
+    (r % 16) // 4, byte r % 4; word 2*half + sub-step // 2, and plane p's bit
+    at (8*byte + 4*(sub-step % 2) + group + p) mod 32."""
     Q, KB, N, _ = planes.shape
     j = np.arange(K)
-    blk = planes[:, j // 128, :, :]                          # [8, K, N, 4]
-    w = ((j % 128) // 32)[None, :, None, None]
-    words = np.take_along_axis(blk, np.broadcast_to(w, blk.shape[:3] + (1,)), 3)[..., 0]
-    e = j % 32
-    pos = 8 * (e % 4) + e // 4                               # bit of element e in its word
-    bits = (words.astype(np.int64) >> pos[None, :, None]) & 1
+    r = j % 128
+    s, h, i, c = r // 32, (r % 32) // 16, (r % 16) // 4, r % 4
+    w = 2 * h + s // 2
+    g = 4 * (s % 2) + i
+    words = planes[:, j // 128, :, :]                        # [8, K, N, 4]
+    words = np.take_along_axis(words, np.broadcast_to(w[None, :, None, None],
+                                                      words.shape[:3] + (1,)), 3)[..., 0]
+    p = (7 - np.arange(Q))[:, None]                          # [8, 1]
+    pos = (8 * c[None, :] + g[None, :] + p) % 32             # [8, K]
+    bits = (words.astype(np.int64) >> pos[:, :, None]) & 1
     return bits.transpose(0, 2, 1)
 
 
 def test_planes_bit_position_worked_example():
-    """Word 0 of a row whose elements 0..31 are 1, 0, 0, ..., 0 except element
-    5 = -128: element 0 sets bit 0 of plane p=0 (q=7); element 5 (group 1,
-    byte 1) sets bit 8*1 + 1 = 9 of the sign plane (q=0)."""
-    W = np.zeros((1, 32), np.int8)
+    """Positions worked out by hand from the layout definition:
+    element 0 = 1 (sub-step 0, half 0, group 0, byte 0) sets bit
+    (0 + 0 + p=0) = 0 of word 0 of plane p = 0 (q = 7);
+    element 5 = -128 (group 1, byte 1) sets bit (8 + 1 + 7) = 16 of word 0
+    of the sign plane (q = 0);
+    element 63 = -128 (sub-step 1, half 1, group 3, byte 3: word 2*1 + 0 = 2)
+    sets bit (24 + 4 + 3 + 7) mod 32 = 6 of word 2 of the sign plane;
+    element 100 = 2 (sub-step 3, half 0, group 1, byte 0: word 1) sets bit
+    (0 + 4 + 1 + 1) = 6 of word 1 of plane p = 1 (q = 6)."""
+    W = np.zeros((1, 128), np.int8)
     W[0, 0] = 1
     W[0, 5] = -128
+    W[0, 63] = -128
+    W[0, 100] = 2
     planes = oracle.pack_planes(W)
     assert int(planes[7, 0, 0, 0]) == 1 << 0
-    assert int(planes[0, 0, 0, 0]) == 1 << 9
-    assert not planes[1:7].any()
+    assert int(planes[0, 0, 0, 0]) == 1 << 16
+    assert int(planes[0, 0, 0, 2]) == 1 << 6
+    assert int(planes[6, 0, 0, 1]) == 1 << 6
+    assert not planes[0, 0, 0, 1] and not planes[0, 0, 0, 3]
+    assert not planes[1:6].any()
+    assert not planes[6, 0, 0, [0, 2, 3]].any() and not planes[7, 0, 0, 1:].any()
 
 
 @pytest.mark.parametrize("N,K", [(1, 1), (5, 31), (7, 32), (3, 100), (4, 300)])
