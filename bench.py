@@ -46,6 +46,8 @@ def traffic_file(kernel: str) -> str:
 # Sources the grouped kernel of each weight layout is built from: recorded
 # counter readings stay valid while none of these files changes.
 KERNEL_SOURCES = {
+    "k_masked_gemm_persistent": ["gemm_core.h", "tasq_internal.h",
+                                 "tile_256x256_k128_w8_pf1.hip", "tasq_api.cpp"],
     "k_masked_gemm_grouped": ["gemm_core.h", "tasq_internal.h", "tile_256x256_k128_w8_pf1.hip",
                               "tasq_api.cpp"],
     "k_gemm_packed_grouped": ["gemm_core.h", "gemm_packed.h", "tasq_internal.h",
@@ -53,7 +55,19 @@ KERNEL_SOURCES = {
 }
 
 
-def kernel_source_sha256(kernel: str = "k_masked_gemm_grouped") -> str:
+def step_kernel(weights: str) -> str:
+    """The kernel of one denoising step of the 28-block schedule: the
+    persistent grouped launch for row-major weights (unless the library's
+    TASQ_PERSISTENT=0 tuning switch turns it off), the grouped packed-weight
+    launch otherwise."""
+    if weights == "packed":
+        return "k_gemm_packed_grouped"
+    if os.environ.get("TASQ_PERSISTENT") == "0":
+        return "k_masked_gemm_grouped"
+    return "k_masked_gemm_persistent"
+
+
+def kernel_source_sha256(kernel: str = "k_masked_gemm_persistent") -> str:
     """Hash of the HIP sources of one grouped kernel; ties recorded counter
     readings to the code."""
     h = hashlib.sha256()
@@ -513,8 +527,7 @@ def main():
                          "counters) and exit")
     args = ap.parse_args()
     if args.print_source_hash:
-        print(kernel_source_sha256("k_gemm_packed_grouped" if args.weights == "packed"
-                                   else "k_masked_gemm_grouped"))
+        print(kernel_source_sha256(step_kernel(args.weights)))
         return
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
@@ -565,7 +578,7 @@ def main():
     value = total_ops / (ms * 1e-3) / 1e12
 
     roof = None
-    kname = "k_gemm_packed_grouped" if args.weights == "packed" else "k_masked_gemm_grouped"
+    kname = step_kernel(args.weights)
     if ws is not None:
         launch_ms = time_launches(layers, table, wl, ws, reps=1)
         t_mfma = ops_step / (PEAK_INT8_TOPS * 1e12)

@@ -369,10 +369,15 @@ struct Regs {
 // fragments.  Tile t+1 is stored from the ring half-way through tile t and
 // the ring slot is refilled right away, so a global load has PF whole K
 // tiles to land.
-template <class C, bool ALIGNED, int KIND, bool PLANES = false>
-__device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int m0, int n0,
-                                         int kb, int ke, v16i (&acc)[C::FM][C::FN], v4i *smA,
-                                         v4i *smB)
+//
+// kloop is the loop proper: on entry tile 0 is in LDS stage 0 (visible to
+// every wave) and tiles 1 .. PF are in the ring; mainloop adds the prologue
+// that puts them there.
+template <class C, bool ALIGNED, int KIND, bool PLANES>
+__device__ __forceinline__ void kloop(const LayerDesc &d, uint32_t wmask, int m0, int n0, int kb,
+                                      int nk, const Plan<C, ALIGNED, KIND, PLANES> &plan,
+                                      Regs<C, ALIGNED, KIND, PLANES> (&ring)[C::PF],
+                                      v16i (&acc)[C::FM][C::FN], v4i *smA, v4i *smB)
 {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -382,30 +387,6 @@ __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int
     constexpr int KK = C::BK / 32;
     constexpr int WRITE_KK = KK / 2 - 1;      // sub-step that stores tile t+1
     constexpr int NW = C::A_LOADS + C::B_LOADS;
-
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < C::FN; ++j)
-            acc[i][j] = v16i{};
-
-    const int span = ke - kb;
-    const int nk = (span + C::BK - 1) / C::BK;
-    if (nk <= 0)
-        return;
-
-    Plan<C, ALIGNED, KIND, PLANES> plan;
-    plan.init(d, m0, n0, kb, ke, tid);
-    Regs<C, ALIGNED, KIND, PLANES> ring[C::PF];
-
-    // Prologue: tile 0 into stage 0, tiles 1 .. PF into the ring.
-    ring[0].load(plan, d, m0, n0, kb, 0u, tid);
-    ring[0].store(smA, smB, wmask, tid);
-#pragma unroll
-    for (int u = 0; u < C::PF; ++u)
-        if (1 + u < nk)
-            ring[u].load(plan, d, m0, n0, kb + (1 + u) * C::BK, (uint32_t)(1 + u) * C::BK, tid);
-    __syncthreads();
 
     v4i fa[2][C::FM], fb[2][C::FN];
     auto read = [&](int stage, int kk, v4i (&a)[C::FM], v4i (&b)[C::FN]) {
@@ -478,6 +459,42 @@ __device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int
             __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
     }
+}
+
+template <class C>
+__device__ __forceinline__ void zero_acc(v16i (&acc)[C::FM][C::FN])
+{
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+            acc[i][j] = v16i{};
+}
+
+template <class C, bool ALIGNED, int KIND, bool PLANES = false>
+__device__ __forceinline__ void mainloop(const LayerDesc &d, uint32_t wmask, int m0, int n0,
+                                         int kb, int ke, v16i (&acc)[C::FM][C::FN], v4i *smA,
+                                         v4i *smB)
+{
+    const int tid = threadIdx.x;
+    zero_acc<C>(acc);
+    const int nk = (ke - kb + C::BK - 1) / C::BK;
+    if (nk <= 0)
+        return;
+
+    Plan<C, ALIGNED, KIND, PLANES> plan;
+    plan.init(d, m0, n0, kb, ke, tid);
+    Regs<C, ALIGNED, KIND, PLANES> ring[C::PF];
+
+    // Prologue: tile 0 into stage 0, tiles 1 .. PF into the ring.
+    ring[0].load(plan, d, m0, n0, kb, 0u, tid);
+    ring[0].store(smA, smB, wmask, tid);
+#pragma unroll
+    for (int u = 0; u < C::PF; ++u)
+        if (1 + u < nk)
+            ring[u].load(plan, d, m0, n0, kb + (1 + u) * C::BK, (uint32_t)(1 + u) * C::BK, tid);
+    __syncthreads();
+    kloop<C, ALIGNED, KIND, PLANES>(d, wmask, m0, n0, kb, nk, plan, ring, acc, smA, smB);
 }
 
 // ------------------------------------------------------ low-rank branch
@@ -593,14 +610,20 @@ __device__ __forceinline__ v16f lowrank_block(const char *lds, int r, int rl, in
 // accumulator in lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32, so
 // each store instruction covers two 128-byte row segments.  Rows past M
 // fall past the buffer end and are dropped; columns past N carry kOOB.
-template <class C, bool NT = true>
-__device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
-                                         const v16i (&acc)[C::FM][C::FN], int bits, char *lds)
+//
+// Three parts, so that a persistent kernel can issue the next tile's loads
+// after every read of the epilogue and before its stores: epilogue_stage
+// (the LDS operands, called by every wave), epilogue_cols (the per-column
+// factors of this lane) and epilogue_write (the stores).
+template <class C>
+struct EpiCols {
+    float scale[C::FN], bias[C::FN], corr[C::FN], wsc[C::FN];
+    uint32_t base[C::FN];   // byte offset of (row mrow, column n), kOOB past N
+};
+
+template <class C>
+__device__ __forceinline__ void epilogue_stage(const LayerDesc &d, int m0, int n0, char *lds)
 {
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
     const bool lowrank = d.lr_T != nullptr && d.y != nullptr;
     const bool wzero = d.wz != nullptr && d.y != nullptr;
     if (lowrank || wzero) {
@@ -611,10 +634,16 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
             stage_rowsums<C>(d, m0, lds);
         __syncthreads();
     }
-    const uint32_t outb = (uint32_t)d.M * (uint32_t)d.N * 4u;
-    const rsrc_t ry = make_rsrc(d.y, d.y ? outb : 0u);
-    const rsrc_t ra = make_rsrc(d.acc, d.acc ? outb : 0u);
-    const uint32_t rowb = (uint32_t)d.N * 4u;
+}
+
+template <class C>
+__device__ __forceinline__ void epilogue_cols(const LayerDesc &d, int m0, int n0, int bits,
+                                              EpiCols<C> &ec)
+{
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+    const bool wzero = d.wz != nullptr && d.y != nullptr;
     const int mrow = m0 + wm * C::WTM + 4 * (lane >> 5);
 #pragma unroll
     for (int j = 0; j < C::FN; ++j) {
@@ -633,7 +662,34 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
             if (wzero)
                 wsc = (128.0f - d.wz[n]) * scale;
         }
-        const uint32_t base = nok ? ((uint32_t)mrow * (uint32_t)d.N + (uint32_t)n) * 4u : kOOB;
+        ec.scale[j] = scale;
+        ec.bias[j] = bias;
+        ec.corr[j] = corr;
+        ec.wsc[j] = wsc;
+        ec.base[j] = nok ? ((uint32_t)mrow * (uint32_t)d.N + (uint32_t)n) * 4u : kOOB;
+    }
+}
+
+// EXTRAS = false compiles out the low-rank and weight-zero-point terms (the
+// caller guarantees that no layer has them).
+template <class C, bool NT = true, bool EXTRAS = true, int J0 = 0, int J1 = C::FN>
+__device__ __forceinline__ void epilogue_write(const LayerDesc &d,
+                                               const v16i (&acc)[C::FM][C::FN],
+                                               const EpiCols<C> &ec, const char *lds)
+{
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+    const bool lowrank = EXTRAS && d.lr_T != nullptr && d.y != nullptr;
+    const bool wzero = EXTRAS && d.wz != nullptr && d.y != nullptr;
+    const uint32_t outb = (uint32_t)d.M * (uint32_t)d.N * 4u;
+    const rsrc_t ry = make_rsrc(d.y, d.y ? outb : 0u);
+    const rsrc_t ra = make_rsrc(d.acc, d.acc ? outb : 0u);
+    const uint32_t rowb = (uint32_t)d.N * 4u;
+#pragma unroll
+    for (int j = J0; j < J1; ++j) {
+        const float scale = ec.scale[j], bias = ec.bias[j], corr = ec.corr[j], wsc = ec.wsc[j];
+        const uint32_t base = ec.base[j];
         if (d.acc) {
 #pragma unroll
             for (int i = 0; i < C::FM; ++i)
@@ -671,6 +727,16 @@ __device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
             }
         }
     }
+}
+
+template <class C, bool NT = true>
+__device__ __forceinline__ void epilogue(const LayerDesc &d, int m0, int n0,
+                                         const v16i (&acc)[C::FM][C::FN], int bits, char *lds)
+{
+    epilogue_stage<C>(d, m0, n0, lds);
+    EpiCols<C> ec;
+    epilogue_cols<C>(d, m0, n0, bits, ec);
+    epilogue_write<C, NT>(d, acc, ec, lds);
 }
 
 // Workgroups are dispatched round-robin over the 8 XCDs (workgroup i runs on
@@ -718,6 +784,21 @@ __global__ void __launch_bounds__(C::NT, C::OCC) k_masked_gemm(LayerDesc d)
     epilogue<C>(d, m0, n0, acc, d.bits, reinterpret_cast<char *>(smA));
 }
 
+// Segment (run of one layer's tiles) of work unit t in a grouped launch:
+// the last segment whose first unit is at or before t.
+__device__ __forceinline__ int find_segment(const LayerDesc *__restrict__ descs, int L, int t)
+{
+    int lo = 0, hi = L - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (descs[mid].tile_begin <= t)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
 // Grouped launch over every layer of one denoising step: workgroup t finds
 // its segment (a run of one layer's tiles) by binary search over the
 // segments' first work units, and the layer's b from the (layer, stage)
@@ -732,15 +813,7 @@ k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
     __shared__ v4i smA[C::SMA];
     __shared__ v4i smB[C::NSTAGE * C::BN * C::CPR];
     const int t = xcd_remap(blockIdx.x, gridDim.x);
-    int lo = 0, hi = L - 1;
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if (descs[mid].tile_begin <= t)
-            lo = mid;
-        else
-            hi = mid - 1;
-    }
-    const LayerDesc d = descs[lo];
+    const LayerDesc d = descs[find_segment(descs, L, t)];
     const int bits = table[d.layer * S + stage];
     const uint32_t wmask = keep_mask_dword(bits);
     int tm, tn;
@@ -752,6 +825,125 @@ k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
     else
         mainloop<C, true, KIND_LINEAR>(d, wmask, m0, n0, 0, d.K, acc, smA, smB);
     epilogue<C>(d, m0, n0, acc, bits, reinterpret_cast<char *>(smA));
+}
+
+// Persistent form of the grouped launch (linear layers, aligned operands,
+// no low-rank branch and no weight zero points):
+// one workgroup per compute unit walks the work units of its XCD's
+// contiguous run, unit x*span + j, + wgs, + 2 wgs, ... (the same units a
+// non-persistent launch would give that XCD, in the same order).  What it
+// gains over one workgroup per tile is overlap at the tile boundary: the
+// next tile's first K tiles are loaded into registers after the last read
+// of the epilogue and before its stores, so their latency is spent under
+// the stores, and the stores (write-only, not waited for) drain while the
+// next tile's K loop runs.  A vector-memory wait covers every older load
+// and store, so the next tile's loads are issued before the stores, not
+// after.
+template <class C>
+__device__ __forceinline__ void unit_coords(const LayerDesc &d, int t, int &m0, int &n0)
+{
+    int tm, tn;
+    tile_coords(t - d.tile_begin + d.tile_first, d.tiles_m, d.tiles_n, tm, tn);
+    m0 = tm * C::BM;
+    n0 = tn * C::BN;
+}
+
+template <class C>
+__global__ void __launch_bounds__(C::NT, C::OCC)
+k_masked_gemm_persistent(const LayerDesc *__restrict__ descs, int L, int total,
+                         const uint8_t *__restrict__ table, int S, int stage, int parties)
+{
+    __shared__ v4i smA[C::SMA];
+    __shared__ v4i smB[C::NSTAGE * C::BN * C::CPR];
+    using PlanT = Plan<C, true, KIND_LINEAR, false>;
+    using RegsT = Regs<C, true, KIND_LINEAR, false>;
+    constexpr int NX = 8;
+    const int tid = threadIdx.x;
+    // The XCD's run of units is cut into `parties` contiguous parts, each
+    // walked by wgs / parties of its workgroups (host: gridDim.x % 8 == 0,
+    // wgs % parties == 0), so that one XCD works on several places of the
+    // layer sequence at once.
+    const int wgs = gridDim.x / NX / parties;       // workgroups per part
+    const int x = blockIdx.x % NX, j = blockIdx.x / NX;
+    const int part = j % parties, jj = j / parties;
+    const int span = (total + NX - 1) / NX;
+    const int xbeg = x * span, xend = min(total, xbeg + span);
+    const int pspan = (xend - xbeg + parties - 1) / parties;
+    const int ubeg = xbeg + part * pspan;
+    const int uend = min(xend, ubeg + pspan);
+    int u = ubeg + jj;
+    if (u >= uend)
+        return;
+
+    // The next tile's first K tile is loaded into ring slot 0, which is
+    // free once a K loop has ended, and stored to LDS at the top of the
+    // tile loop, where the slot is refilled with K tile 1 (the prologue of
+    // mainloop, with its first load moved into the previous epilogue).
+    PlanT plan;
+    RegsT ring[C::PF];
+    auto issue_first = [&](const LayerDesc &d, int m0, int n0) {
+        // An opaque copy of the thread index: the chunk offsets are
+        // recomputed here rather than kept live (or spilled) across the tile.
+        int t = tid;
+        asm volatile("" : "+v"(t));
+        plan.init(d, m0, n0, 0, d.K, t);
+        ring[0].load(plan, d, m0, n0, 0, 0u, t);
+    };
+    // b of a segment from the (layer, stage) table, read as an aligned
+    // dword so that the uniform lookup is a scalar load (a vector load here
+    // would wait for every store the wave has in flight).
+    auto bits_of = [&](int sg) {
+        const int idx = descs[sg].layer * S + stage;
+        const uint32_t w = reinterpret_cast<const uint32_t *>(table)[idx >> 2];
+        return (int)((w >> (8 * (idx & 3))) & 0xffu);
+    };
+
+    int seg = find_segment(descs, L, u);
+    int m0, n0;
+    unit_coords<C>(descs[seg], u, m0, n0);
+    int bits = bits_of(seg);
+    issue_first(descs[seg], m0, n0);
+    for (;;) {
+        const LayerDesc &d = descs[seg];
+        const int nk = (d.K + C::BK - 1) / C::BK;
+        const uint32_t wmask = keep_mask_dword(bits);
+        __syncthreads();                            // no wave still reads the previous tile's LDS
+        ring[0].store(smA, smB, wmask, tid);
+        // Unconditional, so that no slot is live around the tile loop: a
+        // tile past K reads zero weights through the buffer bounds and is
+        // never consumed.
+#pragma unroll
+        for (int v = 0; v < C::PF; ++v)
+            ring[v].load(plan, d, m0, n0, (1 + v) * C::BK, (uint32_t)(1 + v) * C::BK, tid);
+        __syncthreads();
+        v16i acc[C::FM][C::FN];
+        zero_acc<C>(acc);
+        kloop<C, true, KIND_LINEAR, false>(d, wmask, m0, n0, 0, nk, plan, ring, acc, smA, smB);
+        const char *lds = reinterpret_cast<const char *>(smA);
+        EpiCols<C> ec;
+        epilogue_cols<C>(d, m0, n0, bits, ec);
+        u += wgs;
+        if (u >= uend) {
+            epilogue_write<C, true, false>(d, acc, ec, lds);
+            break;
+        }
+        // The last tile's stores come first only on this path, so that the
+        // registers of the next tile's first loads are dead in the K loop.
+        // The first half of the stores frees the registers that the next
+        // tile's first K tile is loaded into; the second half then covers
+        // the latency of those loads.
+        constexpr int JH = C::FN / 2;
+        const LayerDesc &dp = d;
+        seg = find_segment(descs, L, u);
+        unit_coords<C>(descs[seg], u, m0, n0);
+        bits = bits_of(seg);
+        __builtin_amdgcn_sched_barrier(0);
+        epilogue_write<C, true, false, 0, JH>(dp, acc, ec, lds);
+        __builtin_amdgcn_sched_barrier(0);
+        issue_first(descs[seg], m0, n0);
+        __builtin_amdgcn_sched_barrier(0);
+        epilogue_write<C, true, false, JH, C::FN>(dp, acc, ec, lds);
+    }
 }
 
 // Split-K: work unit u holds tile u / splits and the K range of split
@@ -864,6 +1056,21 @@ hipError_t launch_grouped_cfg(const LayerDesc *d_descs, int L, int total_tiles,
     return hipGetLastError();
 }
 
+// Persistent grouped launch over linear layers: wgs_per_xcd workgroups on
+// each of the 8 XCDs.
+template <class C>
+hipError_t launch_persistent_cfg(const LayerDesc *d_descs, int L, int total_tiles,
+                                 const uint8_t *d_table, int S, int stage, int wgs_per_xcd,
+                                 int parties, hipStream_t stream)
+{
+    if (wgs_per_xcd < 1 || total_tiles < 1 || parties < 1 || wgs_per_xcd % parties != 0)
+        return hipErrorInvalidValue;
+    dim3 g((unsigned)(8 * wgs_per_xcd)), b(C::NT);
+    hipLaunchKernelGGL((k_masked_gemm_persistent<C>), g, b, 0, stream, d_descs, L, total_tiles,
+                       d_table, S, stage, parties);
+    return hipGetLastError();
+}
+
 // Defines the dispatch entry of one tile configuration (a host function, so
 // the table of host launchers never reaches the device compilation).
 #define TASQ_DEFINE_TILE(NAME, CFG)                                                         \
@@ -871,7 +1078,7 @@ hipError_t launch_grouped_cfg(const LayerDesc *d_descs, int L, int total_tiles,
     {                                                                                       \
         static const TileOps ops = {{CFG::BM, CFG::BN, CFG::BK}, &launch_single_cfg<CFG>,   \
                                     &launch_planes_cfg<CFG>, &launch_grouped_cfg<CFG>,      \
-                                    &launch_split_cfg<CFG>};                                \
+                                    &launch_split_cfg<CFG>, &launch_persistent_cfg<CFG>};   \
         return ops;                                                                         \
     }
 

@@ -113,6 +113,36 @@ int forced_tile() { return forced("TASQ_TILE", tasq::TILE_COUNT); }
 
 int forced_ptile() { return forced("TASQ_PTILE", tasq::PTILE_COUNT); }
 
+// The grouped step over linear layers without low-rank or weight-zero-point
+// terms runs as a persistent launch (one workgroup per compute unit, tile
+// boundaries overlapped) with the 256x256 tile once there are at least two
+// tiles per compute unit.  TASQ_PERSISTENT=0 / 1 forces it off / on whatever
+// the tile and the tile count, and TASQ_PERSISTENT_WGS=n sets the workgroups
+// per XCD (tuning sweeps and tests only).
+bool use_persistent(int tile, long long total)
+{
+    const int f = forced("TASQ_PERSISTENT", 2);
+    if (f >= 0)
+        return f == 1;
+    return tile == tasq::TILE_256x256_K128_W8_PF1 && total >= 2LL * kComputeUnits;
+}
+
+int persistent_wgs_per_xcd()
+{
+    const int f = forced("TASQ_PERSISTENT_WGS", 1025);
+    return f >= 1 ? f : kComputeUnits / kXcds;
+}
+
+// Parts of each XCD's run walked side by side by the persistent launch;
+// TASQ_PERSISTENT_PARTIES=n sets it (tuning sweeps and tests only).  Falls
+// back to 1 when n does not divide the workgroups per XCD.
+int persistent_parties(int wgs_per_xcd)
+{
+    const int f = forced("TASQ_PERSISTENT_PARTIES", 1025);
+    const int p = f >= 1 ? f : 1;
+    return wgs_per_xcd % p == 0 ? p : 1;
+}
+
 // Packed-weight tile of a single launch, from a sweep of every tile over the
 // DiT/UNet layer shapes with the Infinity Cache flushed before each launch:
 // the 256x256 tile once it gives at least 140 tiles (even half a wave of
@@ -793,6 +823,9 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         tasq::TileShape ts = {32, 32, 128};
         hipError_t (*launch_step)(const LayerDesc *, int, int, const uint8_t *, int, int, bool,
                                   hipStream_t) = nullptr;
+        hipError_t (*launch_persistent)(const LayerDesc *, int, int, const uint8_t *, int, int,
+                                        int, int, hipStream_t) = nullptr;
+        int persistent_tile = -1;
         if (all_skinny) {
             // one unit per 32 output channels, all tokens
             ts = {tasq::kSkinnyMaxM, 32, 128};
@@ -801,9 +834,16 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
             ts = ops.shape;
             launch_step = ops.grouped;
         } else {
-            const tasq::TileOps &ops = tasq::tile_ops(pick_grouped_tile(descs));
+            const int tile = pick_grouped_tile(descs);
+            const tasq::TileOps &ops = tasq::tile_ops(tile);
             ts = ops.shape;
             launch_step = ops.grouped;
+            bool extras = false;
+            for (int l = 0; l < L; ++l)
+                extras = extras || descs[l].lr_T != nullptr || descs[l].wz != nullptr;
+            if (!any_conv && !extras)
+                launch_persistent = ops.persistent;
+            persistent_tile = tile;
         }
         long long total = 0;
         for (int l = 0; l < L; ++l) {
@@ -819,6 +859,10 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         }
         if (total == 0)
             return TASQ_OK;
+        if (!use_persistent(persistent_tile, total))
+            launch_persistent = nullptr;
+        const int wgs_per_xcd = persistent_wgs_per_xcd();
+        const int parties = persistent_parties(wgs_per_xcd);
         // The GEMM kernels give each XCD one contiguous run of the work
         // units (for L2 locality), equal in count.  When the layers' tiles
         // differ in cost (K) and the layer order leaves one run much heavier
@@ -867,7 +911,10 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
             const hipError_t e =
                 all_skinny ? tasq::launch_skinny_grouped(d_descs, nseg, (int)total, max_m, src,
                                                          d_table, S, s, st)
-                           : launch_step(d_descs, nseg, (int)total, d_table, S, s, any_conv, st);
+                : launch_persistent
+                    ? launch_persistent(d_descs, nseg, (int)total, d_table, S, s, wgs_per_xcd,
+                                        parties, st)
+                    : launch_step(d_descs, nseg, (int)total, d_table, S, s, any_conv, st);
             if (e != hipSuccess)
                 return TASQ_ERR_HIP;
         }

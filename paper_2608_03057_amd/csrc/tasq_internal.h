@@ -64,6 +64,12 @@ struct TileOps {
     // Split-K partials (aligned operands only) into part[splits][M][N].
     hipError_t (*split)(const LayerDesc &d, int32_t *part, int splits, int kchunk,
                         hipStream_t stream);
+    // Persistent form of grouped over linear layers only: wgs_per_xcd
+    // workgroups per XCD walk the XCD's run of work units, cut into
+    // `parties` parts walked side by side (wgs_per_xcd % parties == 0).
+    hipError_t (*persistent)(const LayerDesc *d_descs, int L, int total_tiles,
+                             const uint8_t *d_table, int S, int stage, int wgs_per_xcd,
+                             int parties, hipStream_t stream);
 };
 
 // Sums split-K partials and applies the dequantisation epilogue (splitk.hip).
