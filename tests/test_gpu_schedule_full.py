@@ -1,4 +1,6 @@
-"""Config 4 at full size in the benchmark's own launch configuration: the
+"""Full-size schedules through tasq_run_schedule with a workspace.
+
+Config 4 at full size in the benchmark's own launch configuration: the
 28-block PixArt-shaped stack (112 linears at M = 8192) through
 tasq_run_schedule with a workspace, i.e. one persistent grouped launch per
 denoising step, fp32 outputs only, inputs drawn exactly as bench.py draws
@@ -6,7 +8,9 @@ them.  After a step range every layer holds the output of the range's last
 step, at that step's stage b; sampled outputs of every layer are checked
 against the oracle entry by entry: fp32 within 1e-6 relative, and, in a
 second pass with int32 outputs requested as well (the general epilogue of
-the same launch), the int32 accumulators bit-exactly."""
+the same launch), the int32 accumulators bit-exactly.  Configs 1-3 (one
+DiT, one SANA and one UNet block with its 3x3 conv) likewise, sampled
+outputs of every layer at the end of each stage."""
 import numpy as np
 import pytest
 import torch
@@ -84,3 +88,64 @@ def test_config4_schedule_bench_launch_sampled():
         b = int(table[l, stage])
         check_layer(wl, l, Ws[l], sws[l], ys[l].cpu(), accs[l].cpu(), b, rng,
                     f"config 4 [{t},{t + 1}) layer {l} b={b} with int32")
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_block_schedules_full_size_sampled(cfg):
+    """Configs 1-3 as full-size schedules through tasq_run_schedule with a
+    workspace (the grouped per-step launch: persistent for the DiT blocks,
+    one workgroup per tile for the UNet block with its 3x3 conv), every step
+    range ending in each stage; sampled outputs of every layer (pixels x all
+    channels for the conv) against the oracle, int32 bit-exact and fp32
+    within 1e-6 relative."""
+    wl = inputs.workload(cfg)
+    table = inputs.b_table(wl)
+    sx = f32(wl.sx)
+    host, keep, layers = [], [], []
+    for l, spec in enumerate(wl.layers):
+        X = inputs.x_full(wl, l)
+        W = inputs.w_full(wl, l)
+        if spec.kind == "conv3x3":
+            W = W.reshape(spec.N, 3, 3, spec.C)
+            shape = (spec.H, spec.Wd, spec.N)
+        else:
+            shape = (spec.M, spec.N)
+        sw = inputs.sw_full(wl, l)
+        Xd, Wd, swd = X.to(DEV), W.to(DEV), sw.to(DEV)
+        acc = torch.full(shape, 12345, dtype=torch.int32, device=DEV)
+        y = torch.full(shape, -7.0, dtype=torch.float32, device=DEV)
+        layers.append(T.make_layer(Xd, Wd, wl.sx, swd, None, acc, y))
+        keep.append((Xd, Wd, swd))
+        host.append((X, W, sw, acc, y))
+    ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
+    rng = np.random.default_rng(50 + cfg)
+    ends = sorted({max(t for t in range(wl.T) if oracle.stage_of_step(t, wl.S, wl.T) == s)
+                   for s in range(wl.S)})
+    for t1 in ends:
+        t0 = max(0, t1 - 1)
+        T.run_schedule(layers, table, wl.S, wl.T, t0, t1 + 1, workspace=ws)
+        torch.cuda.synchronize()
+        stage = oracle.stage_of_step(t1, wl.S, wl.T)
+        for l, spec in enumerate(wl.layers):
+            X, W, sw, acc, y = host[l]
+            b = int(table[l, stage])
+            where = f"config {cfg} [{t0},{t1 + 1}) {spec.name} b={b}"
+            if spec.kind == "conv3x3":
+                pix = sorted(set([0, spec.Wd - 1, spec.Wd, spec.H * spec.Wd - 1]
+                                 + rng.integers(0, spec.H * spec.Wd, 6).tolist()))
+                pp = np.repeat(np.array(pix), spec.N)
+                cc = np.tile(np.arange(spec.N), len(pix))
+                ra, ry = oracle.conv3x3_entries(X, W, sx, sw, b, pp, cc)
+                ti = torch.as_tensor(pix)
+                check_outputs(acc.reshape(-1, spec.N)[ti], y.reshape(-1, spec.N)[ti],
+                              ra.reshape(len(pix), spec.N), ry.reshape(len(pix), spec.N), sx,
+                              sw, None, where)
+            else:
+                rows = sample_rows(spec.M, rng, 4)
+                rr = np.repeat(np.arange(len(rows)), spec.N)
+                cc = np.tile(np.arange(spec.N), len(rows))
+                ra, ry = oracle.masked_linear_entries(X[torch.as_tensor(rows)], W, sx, sw, b,
+                                                      rr, cc)
+                ti = torch.as_tensor(rows)
+                check_outputs(acc[ti], y[ti], ra.reshape(len(rows), spec.N),
+                              ry.reshape(len(rows), spec.N), sx, sw, None, where)
