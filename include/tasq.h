@@ -375,8 +375,13 @@ typedef struct tasq_layer {
  * the same weight source (bit planes with the BITPLANE variant, packed
  * buffers, or row-major W); otherwise it tiles every layer's GEMM, reading
  * the packed weights when every layer carries W_packed (W may then be NULL)
- * and the row-major W otherwise.  The whole table and every layer are
- * validated before anything is enqueued.
+ * and the row-major W otherwise.  With row-major weights, a layer whose one
+ * 256x256 output tile would cost more than a compute unit's even share of
+ * the step and which split-K would cut (a long K on few tiles, e.g. a 3x3
+ * conv over 32x32 pixels) is launched on its own each step, split-K over the
+ * partials room of the workspace, ahead of the grouped launch over the
+ * other layers.  The whole table and every layer are validated before
+ * anything is enqueued.
  */
 int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
                       int t_begin, int t_end, const tasq_opts *opts, void *stream);
@@ -386,7 +391,9 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
  * output tiles, or K too short).  A smaller workspace runs unsplit. */
 size_t tasq_workspace_bytes(int M, int N, int K);
 
-/* Workspace for the grouped schedule over these layers (host array). */
+/* Workspace for the grouped schedule over these layers (host array): the
+ * device layer list and bit table, plus the split-K partial sums of the
+ * largest layer that tasq_workspace_bytes would split (0 if none). */
 size_t tasq_schedule_workspace_bytes(const tasq_layer *layers, int L);
 
 /* Static description of a status code; never NULL. */

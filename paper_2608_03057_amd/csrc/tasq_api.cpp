@@ -222,6 +222,34 @@ void split_geometry(int K, int s, int &kchunk, int &splits)
     splits = (K + kchunk - 1) / kchunk;
 }
 
+// Split-K partials of the largest layer a schedule would split (0 when
+// none would): the schedule workspace keeps room for them after the device
+// layer list and the bit table.
+size_t max_split_bytes(const tasq_layer *layers, int L)
+{
+    unsigned long long mx = 0;
+    for (int l = 0; l < L; ++l) {
+        const tasq_layer &t = layers[l];
+        if (t.M <= 0 || t.N <= 0 || t.K <= 128)
+            continue;
+        const int s = auto_splits(t.M, t.N, t.K);
+        if (s < 2)
+            continue;
+        int kchunk, splits;
+        split_geometry(t.K, s, kchunk, splits);
+        const unsigned long long need = 4ULL * splits * (unsigned long long)t.M * t.N;
+        if (need < (1ULL << 31) && need > mx)
+            mx = need;
+    }
+    return (size_t)mx;
+}
+
+size_t schedule_partials_offset(int L)
+{
+    return round_up((size_t)L * kXcds * sizeof(LayerDesc), kWsAlign) +
+           round_up((size_t)L * 64, kWsAlign);
+}
+
 int pick_split_tile()
 {
     const int f = forced_tile();
@@ -746,11 +774,10 @@ size_t tasq_packed_weight_bytes(int N, int K)
 
 size_t tasq_schedule_workspace_bytes(const tasq_layer *layers, int L)
 {
-    (void)layers;
     if (L <= 0)
         return 0;
-    return round_up((size_t)L * kXcds * sizeof(LayerDesc), kWsAlign) +
-           round_up((size_t)L * 64, kWsAlign);
+    return schedule_partials_offset(L) + (layers ? round_up(max_split_bytes(layers, L), kWsAlign)
+                                                 : 0);
 }
 
 int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
@@ -817,8 +844,37 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         grouped = x_aligned(d) && (all_packed || (d.W && aligned16(d.W)));
     }
     if (all_skinny || grouped) {
-        bool any_conv = false;
         for (int l = 0; l < L; ++l)
+            descs[l].layer = l;
+        // A layer whose one 256x256 tile costs more than a compute unit's
+        // even share of the step, and that split-K can cut (a long K on few
+        // tiles: the 3x3 conv of the UNet block), is launched on its own
+        // each step, split-K over the partials room of the workspace, ahead
+        // of the grouped launch over the other layers; inside the grouped
+        // launch its tiles would set the step time and force small tiles on
+        // every layer (SDXL-Turbo-shaped block: 174.5 us per step grouped,
+        // 99.1 + 39.1 us split this way).
+        std::vector<LayerDesc> solo;
+        if (!all_skinny && !all_packed) {
+            double ops = 0;
+            for (const LayerDesc &d : descs)
+                ops += 2.0 * d.M * (double)d.N * d.K;
+            std::vector<LayerDesc> rest;
+            for (const LayerDesc &d : descs) {
+                const bool long_tile = 2.0 * 256 * 256 * (double)d.K > ops / kComputeUnits;
+                if (long_tile && auto_splits(d.M, d.N, d.K) > 1)
+                    solo.push_back(d);
+                else
+                    rest.push_back(d);
+            }
+            if (rest.empty())
+                solo.clear();
+            else if (!solo.empty())
+                descs.swap(rest);
+        }
+        const int LG = (int)descs.size();
+        bool any_conv = false;
+        for (int l = 0; l < LG; ++l)
             any_conv = any_conv || descs[l].kind == tasq::KIND_CONV3X3;
         tasq::TileShape ts = {32, 32, 128};
         hipError_t (*launch_step)(const LayerDesc *, int, int, const uint8_t *, int, int, bool,
@@ -839,25 +895,24 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
             ts = ops.shape;
             launch_step = ops.grouped;
             bool extras = false;
-            for (int l = 0; l < L; ++l)
+            for (int l = 0; l < LG; ++l)
                 extras = extras || descs[l].lr_T != nullptr || descs[l].wz != nullptr;
             if (!any_conv && !extras)
                 launch_persistent = ops.persistent;
             persistent_tile = tile;
         }
         long long total = 0;
-        for (int l = 0; l < L; ++l) {
+        for (int l = 0; l < LG; ++l) {
             LayerDesc &d = descs[l];
             d.tiles_m = (d.M + ts.bm - 1) / ts.bm;
             d.tiles_n = (d.N + ts.bn - 1) / ts.bn;
             d.tile_first = 0;
-            d.layer = l;
             d.tile_begin = (int)total;
             total += (long long)d.tiles_m * d.tiles_n;
             if (total > 0x7fffffffLL)
                 return TASQ_ERR_DIM;
         }
-        if (total == 0)
+        if (total == 0 && solo.empty())
             return TASQ_OK;
         if (!use_persistent(persistent_tile, total))
             launch_persistent = nullptr;
@@ -871,13 +926,13 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         std::vector<LayerDesc> segs;
         if (!all_skinny && xcd_imbalance(descs, total) > kImbalanceLimit) {
             try {
-                segs.reserve((size_t)L * kXcds);
+                segs.reserve((size_t)LG * kXcds);
             } catch (const std::bad_alloc &) {
                 return TASQ_ERR_HIP;
             }
             long long begin = 0;
             for (int r = 0; r < kXcds; ++r)
-                for (int l = 0; l < L; ++l) {
+                for (int l = 0; l < LG; ++l) {
                     const long long n = (long long)descs[l].tiles_m * descs[l].tiles_n;
                     const long long lo = n * r / kXcds, hi = n * (r + 1) / kXcds;
                     if (hi <= lo)
@@ -906,8 +961,18 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         if (hipMemcpyAsync(d_table, table.data(), (size_t)L * S, hipMemcpyHostToDevice, st) !=
             hipSuccess)
             return TASQ_ERR_HIP;
+        tasq_opts sopts = *opts;
+        sopts.workspace = ws + schedule_partials_offset(L);
+        sopts.workspace_bytes = opts->workspace_bytes - schedule_partials_offset(L);
         for (int t = t_begin; t < t_end; ++t) {
             const int s = tasq_stage_of_step(t, S, T);
+            for (LayerDesc d : solo) {
+                d.bits = b_table[(size_t)d.layer * S + s];
+                if (int rc = launch_layer(d, &sopts, st, true))
+                    return rc;
+            }
+            if (total == 0)
+                continue;
             const hipError_t e =
                 all_skinny ? tasq::launch_skinny_grouped(d_descs, nseg, (int)total, max_m, src,
                                                          d_table, S, s, st)

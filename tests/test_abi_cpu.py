@@ -312,3 +312,20 @@ def test_schedule_workspace_bytes_grows_with_layers():
     a = L.tasq_schedule_workspace_bytes((Layer * 1)(layer()), 1)
     b = L.tasq_schedule_workspace_bytes((Layer * 112)(*[layer()] * 112), 112)
     assert 0 < a <= b and a % 256 == 0 and b % 256 == 0
+
+
+def test_schedule_workspace_bytes_holds_split_partials():
+    """A schedule with a layer that split-K would cut (the UNet block's 3x3
+    conv: K = 11520 on 20 tiles of 256x256) reserves that layer's int32
+    partials after the layer list and the bit table; the 28-block DiT
+    schedule (K <= 4608) reserves none."""
+    lin = layer(M=4096, N=1920, K=640)
+    conv = layer(kind=_lib.KIND_CONV3X3, H=32, Wd=32, C=1280, M=1024, N=1280, K=11520)
+    base = L.tasq_schedule_workspace_bytes((Layer * 2)(lin, lin), 2)
+    with_conv = L.tasq_schedule_workspace_bytes((Layer * 2)(lin, conv), 2)
+    assert with_conv == base + L.tasq_workspace_bytes(1024, 1280, 11520)
+    assert L.tasq_workspace_bytes(1024, 1280, 11520) == 10 * 1024 * 1280 * 4
+    dit = [layer(M=8192, N=n, K=k) for k, n in [(1152, 3456), (1152, 1152), (1152, 4608),
+                                                (4608, 1152)]] * 28
+    assert L.tasq_schedule_workspace_bytes((Layer * 112)(*dit), 112) == \
+        L.tasq_schedule_workspace_bytes((Layer * 112)(*[layer()] * 112), 112)
