@@ -138,6 +138,51 @@ def time_schedule(layers, table, wl, ws, steps, warmup):
     return start.elapsed_time(end) / steps
 
 
+def measured_peaks(device, blocks=768, iters=40000, copy_reps=5):
+    """What the GPU sustains, measured here rather than taken from the
+    datasheet: the int8 matrix-instruction rate with no memory traffic
+    (libtasq_probe.so, eight independent v_mfma_i32_32x32x32_i8 chains per
+    wave, three workgroups of four waves per CU), the shader clock that rate
+    implies (the datasheet 5.0 POP/s is reached at 2.4 GHz), and the
+    bandwidth of a plain 1 GiB device-to-device copy (read + write bytes)."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2608_03057_amd", "libtasq_probe.so")
+    probe = ctypes.CDLL(path)
+    probe.tasq_probe_mfma_peak.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                           ctypes.c_void_p]
+    sink = torch.empty(blocks * 256, dtype=torch.int32, device=device)
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+    def run(n):
+        if probe.tasq_probe_mfma_peak(blocks, n, ctypes.c_void_p(sink.data_ptr()), stream):
+            raise RuntimeError("tasq_probe_mfma_peak failed")
+
+    run(100)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    run(iters)
+    b.record()
+    torch.cuda.synchronize()
+    ops = blocks * 4 * iters * probe.tasq_probe_mfma_chains() * 2.0 * 32 * 32 * 32
+    tops = ops / (a.elapsed_time(b) * 1e-3) / 1e12
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=device)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(copy_reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    copy = 2.0 * src.numel() * copy_reps / (a.elapsed_time(b) * 1e-3) / 1e9
+    del src, dst
+    return {"mfma_int8_TOPS": round(tops, 1), "mfma_frac_of_datasheet": round(tops / PEAK_INT8_TOPS, 4),
+            "implied_clock_GHz": round(2.4 * tops / PEAK_INT8_TOPS, 3),
+            "copy_GBps": round(copy, 1), "copy_frac_of_datasheet": round(copy / PEAK_HBM_GBS, 4),
+            "kernels": "k_mfma_peak (libtasq_probe.so); torch copy_ of 1 GiB"}
+
+
 def time_launches(layers, table, wl, ws, reps):
     """Average duration of one grouped launch (one denoising step), from
     events recorded around each launch on the launch stream."""
@@ -598,6 +643,14 @@ def main():
         roof["algorithmic_bytes"] = gemm_bytes(wl)
         roof["algorithmic_ops"] = ops_step
 
+    peaks = measured_peaks(dev)
+    if roof is not None:
+        # the same launch against what this GPU was measured to sustain
+        if roof["bound"] == "hbm":
+            roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks["copy_GBps"], 4)
+        else:
+            roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks["mfma_int8_TOPS"], 4)
+
     skinny = None
     if not args.no_skinny and not args.per_layer:
         log("timing the weight-streaming schedule at M=16")
@@ -641,6 +694,7 @@ def main():
         "mean_bits": round(float(table.float().mean()), 3),
         "accounting": accounting,
         "roofline": roof,
+        "measured_peaks": peaks,
         "skinny_schedule": skinny,
         "asymmetric_activations": act,
         "weight_quantizer": wq,

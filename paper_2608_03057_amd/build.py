@@ -1,4 +1,5 @@
-"""Builds libtasq.so (the C-ABI library) for gfx950 with hipcc, in-tree."""
+"""Builds libtasq.so (the C-ABI library) and libtasq_probe.so (the benchmark's
+measurement probe) for gfx950 with hipcc, in-tree."""
 from __future__ import annotations
 
 import os
@@ -11,6 +12,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtasq.so")
+# The benchmark's measurement probe, a library of its own (not the TASQ ABI).
+PROBE_LIB = os.path.join(HERE, "libtasq_probe.so")
+PROBE_SOURCES = ["probe.hip"]
 OBJDIR = os.path.join(ROOT, "_build")
 
 SOURCES = [
@@ -54,14 +58,20 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build() -> str:
-    os.makedirs(OBJDIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, out):
+    tmp = out + ".tmp"
     subprocess.check_call([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs,
                            "-o", tmp])
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+
+
+def build() -> str:
+    os.makedirs(OBJDIR, exist_ok=True)
+    srcs = SOURCES + PROBE_SOURCES
+    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = dict(zip(srcs, ex.map(_compile, srcs)))
+    _link([objs[s] for s in SOURCES], LIB)
+    _link([objs[s] for s in PROBE_SOURCES], PROBE_LIB)
     return LIB
 
 

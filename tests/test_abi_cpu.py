@@ -329,3 +329,23 @@ def test_schedule_workspace_bytes_holds_split_partials():
                                                 (4608, 1152)]] * 28
     assert L.tasq_schedule_workspace_bytes((Layer * 112)(*dit), 112) == \
         L.tasq_schedule_workspace_bytes((Layer * 112)(*[layer()] * 112), 112)
+
+
+def test_probe_library_exports_its_header_and_stays_out_of_the_abi():
+    """The benchmark's measurement probe is a library of its own: it exports
+    what include/tasq_probe.h declares, libtasq.so exports none of it, and
+    its argument checks fail before any launch."""
+    text = open(os.path.join(ROOT, "include", "tasq_probe.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    syms = sorted(set(re.findall(r"\b(tasq_\w+)\s*\(", text)))
+    assert syms == ["tasq_probe_mfma_chains", "tasq_probe_mfma_peak"]
+    probe = ctypes.CDLL(os.path.join(ROOT, "paper_2608_03057_amd", "libtasq_probe.so"))
+    for s in syms:
+        assert hasattr(probe, s), s
+        assert s not in _lib.EXPORTS and not hasattr(L, s), s
+    probe.tasq_probe_mfma_peak.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                           ctypes.c_void_p]
+    assert probe.tasq_probe_mfma_peak(0, 10, FAKE, None) == -1
+    assert probe.tasq_probe_mfma_peak(4, 0, FAKE, None) == -1
+    assert probe.tasq_probe_mfma_peak(4, 10, None, None) == -1
+    assert probe.tasq_probe_mfma_chains() == 8
