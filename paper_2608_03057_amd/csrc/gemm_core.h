@@ -362,13 +362,15 @@ struct Regs {
 // K tile t lives in LDS stage t % 2 while tile t+1 is written into the other
 // stage and tiles t+2 .. t+PF are in flight in the register ring.  Within
 // tile t, the LDS reads of sub-step kk+1 are in flight while the MFMAs of
-// sub-step kk issue.  The one barrier per K tile sits before the last
-// sub-step: by then every wave has read all of tile t's fragments and
-// written its share of tile t+1, so the last sub-step's MFMAs (operands
-// already in registers) cover the barrier and the reads of tile t+1's first
-// fragments.  Tile t+1 is stored from the ring half-way through tile t and
-// the ring slot is refilled right away, so a global load has PF whole K
-// tiles to land.
+// sub-step kk issue, one read after each MFMA (a run of reads can fill the
+// LDS queue, and a wave that waits to issue a read issues no MFMA either).
+// The one barrier per K tile sits before the last sub-step: by then every
+// wave has read all of tile t's fragments and written its share of tile
+// t+1, so the last sub-step's MFMAs (operands already in registers) cover
+// the barrier and the reads of tile t+1's first fragments.  Tile t+1 is
+// stored from the ring in the sub-step before the barrier (measured faster
+// than half-way through tile t) and the ring slot is refilled right away,
+// so a global load has PF whole K tiles to land.
 //
 // kloop is the loop proper: on entry tile 0 is in LDS stage 0 (visible to
 // every wave) and tiles 1 .. PF are in the ring; mainloop adds the prologue
@@ -385,7 +387,7 @@ __device__ __forceinline__ void kloop(const LayerDesc &d, uint32_t wmask, int m0
     const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
     constexpr int SA = C::BM * C::CPR, SB = C::BN * C::CPR;
     constexpr int KK = C::BK / 32;
-    constexpr int WRITE_KK = KK / 2 - 1;      // sub-step that stores tile t+1
+    constexpr int WRITE_KK = KK - 2;          // sub-step that stores tile t+1
     constexpr int NW = C::A_LOADS + C::B_LOADS;
 
     v4i fa[2][C::FM], fb[2][C::FN];
@@ -423,7 +425,6 @@ __device__ __forceinline__ void kloop(const LayerDesc &d, uint32_t wmask, int m0
                 for (int kk = 0; kk + 1 < KK; ++kk) {
                     read(stage, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
                     mfmas(fa[kk & 1], fb[kk & 1]);
-                    __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
                     if (kk == WRITE_KK) {
                         ring[u].store(smA + (stage ^ 1) * SA, smB + (stage ^ 1) * SB, wmask, tid);
                         if (t + 1 + C::PF < nk) {
@@ -433,18 +434,29 @@ __device__ __forceinline__ void kloop(const LayerDesc &d, uint32_t wmask, int m0
 #pragma unroll
                         for (int i = 0; i < C::FM * C::FN; ++i) {
                             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                            if (i < C::FM + C::FN)
+                                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
                             if (i < NW)
                                 __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
                         }
                     } else {
-                        __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
+#pragma unroll
+                        for (int i = 0; i < C::FM * C::FN; ++i) {
+                            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                            if (i < C::FM + C::FN)
+                                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                        }
                     }
                 }
                 __syncthreads();
                 read(stage ^ 1, 0, fa[0], fb[0]);
                 mfmas(fa[(KK - 1) & 1], fb[(KK - 1) & 1]);
-                __builtin_amdgcn_sched_group_barrier(0x100, C::FM + C::FN, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
+#pragma unroll
+                for (int i = 0; i < C::FM * C::FN; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    if (i < C::FM + C::FN)
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                }
                 stage ^= 1;
             }
         }
