@@ -55,8 +55,10 @@ __host__ __device__ inline size_t packed_weight_bytes(int N, int K)
 }
 
 // Accumulates all of K for tile (m0, n0).  Schedule as mainloop() in
-// gemm_core.h (barrier before the last sub-step, next activation tile
-// stored half-way through the current one, PF activation tiles in flight).
+// gemm_core.h (barrier before the last sub-step, one fragment read after
+// each MFMA, PF activation tiles in flight), except that the next
+// activation tile is stored half-way through the current one (storing it in
+// the sub-step before the barrier measured slower here).
 // The weight fragments live in one register buffer per sub-step: as soon as
 // the MFMAs of sub-step kk of tile t have taken their (masked) copy, the
 // fragment of sub-step kk of tile t+1 is loaded into the same registers, so
@@ -155,8 +157,12 @@ __device__ __forceinline__ void mainloop_packed(const LayerDesc &d, uint32_t wma
                     read(stage, kk + 1, fa[(kk + 1) & 1]);
                     mfmas(fa[kk & 1], kk);
                     loadB(t + 1, kk);
-                    __builtin_amdgcn_sched_group_barrier(0x100, C::FM, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
+#pragma unroll
+                    for (int i = 0; i < C::FM * C::FN; ++i) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                        if (i < C::FM)
+                            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    }
                     if (kk == WRITE_KK) {
                         ring[u].store(sm + (stage ^ 1) * SA, nullptr, wmask, tid);
                         if (t + 1 + PF < nk) {
@@ -169,8 +175,12 @@ __device__ __forceinline__ void mainloop_packed(const LayerDesc &d, uint32_t wma
                 read(stage ^ 1, 0, fa[0]);
                 mfmas(fa[(KK - 1) & 1], KK - 1);
                 loadB(t + 1, KK - 1);
-                __builtin_amdgcn_sched_group_barrier(0x100, C::FM, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
+#pragma unroll
+                for (int i = 0; i < C::FM * C::FN; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    if (i < C::FM)
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                }
                 stage ^= 1;
             }
         }
