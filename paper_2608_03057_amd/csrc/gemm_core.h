@@ -845,12 +845,12 @@ k_masked_gemm_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t 
 // contiguous run, unit x*span + j, + wgs, + 2 wgs, ... (the same units a
 // non-persistent launch would give that XCD, in the same order).  What it
 // gains over one workgroup per tile is overlap at the tile boundary: the
-// next tile's first K tiles are loaded into registers after the last read
-// of the epilogue and before its stores, so their latency is spent under
-// the stores, and the stores (write-only, not waited for) drain while the
-// next tile's K loop runs.  A vector-memory wait covers every older load
-// and store, so the next tile's loads are issued before the stores, not
-// after.
+// next tile's first K tile is loaded into registers between the two halves
+// of the current tile's stores, so its latency is spent under the second
+// half, and the stores (write-only, never waited for) drain while the next
+// tile starts.  A vector-memory wait covers every older load and store, so
+// those loads go out before the second half of the stores, not after all of
+// them.
 template <class C>
 __device__ __forceinline__ void unit_coords(const LayerDesc &d, int t, int &m0, int &n0)
 {
@@ -939,11 +939,11 @@ k_masked_gemm_persistent(const LayerDesc *__restrict__ descs, int L, int total,
             epilogue_write<C, true, false>(d, acc, ec, lds);
             break;
         }
-        // The last tile's stores come first only on this path, so that the
-        // registers of the next tile's first loads are dead in the K loop.
-        // The first half of the stores frees the registers that the next
-        // tile's first K tile is loaded into; the second half then covers
-        // the latency of those loads.
+        // Another tile follows: the first half of the stores frees
+        // accumulator registers, the next tile's first K tile is loaded,
+        // and the second half of the stores covers the latency of those
+        // loads.  (The ring slot they land in is dead after the K loop, so
+        // no register set is live around the tile loop.)
         constexpr int JH = C::FN / 2;
         const LayerDesc &dp = d;
         seg = find_segment(descs, L, u);
