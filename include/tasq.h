@@ -52,7 +52,7 @@ enum {
     TASQ_ERR_RANGE = -5,     /* bad S, T, t_begin, t_end, or L                      */
     TASQ_ERR_LAYOUT = -6,    /* requested variant needs a layout that is absent    */
     TASQ_ERR_WORKSPACE = -7, /* workspace missing or smaller than required         */
-    TASQ_ERR_HIP = -8,       /* a HIP runtime call or kernel launch failed          */
+    TASQ_ERR_HIP = -8,       /* a HIP call or launch failed, or host memory ran out */
     TASQ_ERR_KIND = -9,      /* unknown layer kind or variant                       */
     TASQ_ERR_ALIGN = -10     /* workspace not 256-byte aligned, or a packed weight
                                 not 16-byte aligned                                */

@@ -780,8 +780,8 @@ size_t tasq_schedule_workspace_bytes(const tasq_layer *layers, int L)
                                                  : 0);
 }
 
-int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
-                      int t_begin, int t_end, const tasq_opts *opts, void *stream)
+static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_table, int S,
+                             int T, int t_begin, int t_end, const tasq_opts *opts, void *stream)
 {
     if (L < 0)
         return TASQ_ERR_RANGE;
@@ -806,12 +806,7 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         return TASQ_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
 
-    std::vector<LayerDesc> descs;
-    try {
-        descs.resize(L);
-    } catch (const std::bad_alloc &) {
-        return TASQ_ERR_HIP;
-    }
+    std::vector<LayerDesc> descs(L);
     for (int l = 0; l < L; ++l)
         descs[l] = make_desc(layers[l], opts);
 
@@ -925,11 +920,7 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         // that each run holds about an eighth of every layer.
         std::vector<LayerDesc> segs;
         if (!all_skinny && xcd_imbalance(descs, total) > kImbalanceLimit) {
-            try {
-                segs.reserve((size_t)LG * kXcds);
-            } catch (const std::bad_alloc &) {
-                return TASQ_ERR_HIP;
-            }
+            segs.reserve((size_t)LG * kXcds);
             long long begin = 0;
             for (int r = 0; r < kXcds; ++r)
                 for (int l = 0; l < LG; ++l) {
@@ -995,6 +986,19 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
         }
     }
     return TASQ_OK;
+}
+
+// The host-side lists (layer descriptors, segments, the table copy) are
+// std::vectors: running out of host memory is returned as TASQ_ERR_HIP, not
+// thrown across the C ABI.
+int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
+                      int t_begin, int t_end, const tasq_opts *opts, void *stream)
+{
+    try {
+        return run_schedule_impl(layers, L, b_table, S, T, t_begin, t_end, opts, stream);
+    } catch (const std::bad_alloc &) {
+        return TASQ_ERR_HIP;
+    }
 }
 
 }  // extern "C"
