@@ -93,7 +93,9 @@ enum {
  *                   (TASQ_ERR_WORKSPACE otherwise).  The ranges' int32
  *                   partial sums are added in a fixed order, so every
  *                   output is identical to the unsplit one.  Negative:
- *                   TASQ_ERR_RANGE.  Schedules ignore it.
+ *                   TASQ_ERR_RANGE.  Schedules ignore it (a long-K layer
+ *                   that a schedule launches on its own uses the automatic
+ *                   split over the schedule workspace).
  *   W_planes        bit-plane copy of W as written by tasq_pack_planes; needed
  *                   by the BITPLANE variant (W may then be NULL).
  *   W_packed        W in the MFMA operand order as written by
@@ -140,7 +142,55 @@ enum {
  *   x_rowsums       device int32 [M] from tasq_row_sums of X; required with
  *                   w_zero.  Both 4-byte aligned (TASQ_ERR_ALIGN); linear
  *                   layers only (TASQ_ERR_LAYOUT on a conv).
+ * Tuning overrides, for sweeps and tests (0 everywhere = the library's own
+ * choice, which every other caller should keep):
+ *   tile            t + 1 forces staged-weight tile TASQ_TILE_* t (single
+ *                   calls, split-K and grouped schedule steps).
+ *   packed_tile     t + 1 forces packed-weight tile TASQ_PTILE_* t.
+ *   persistent      grouped schedule steps over linear layers without
+ *                   low-rank or weight-zero-point terms: 1 = one workgroup
+ *                   per output tile, 2 = the persistent launch (one
+ *                   workgroup per compute unit walking a run of tiles),
+ *                   whatever the tile and the tile count.
+ *   persistent_wgs  workgroups per XCD of the persistent launch (1..1024;
+ *                   0 = one per compute unit, 32).
+ *   persistent_parties  parts of each XCD's run of tiles walked side by side
+ *                   by the persistent launch (it must divide the workgroups
+ *                   per XCD, else 1 is used; 0 = 1).
+ *   Out of range: TASQ_ERR_RANGE.
+ * Measurement:
+ *   step_events     tasq_run_schedule only: NULL, or a host array of
+ *                   2 * (t_end - t_begin) hipEvent_t created by the caller;
+ *                   the library records step_events[2i] on the stream right
+ *                   before the kernels of step t_begin + i and
+ *                   step_events[2i + 1] right after them, so the pair times
+ *                   that step's launches alone (not the per-call upload of
+ *                   the layer list).  A failed record is TASQ_ERR_HIP.
  */
+
+/* Staged-weight tile configurations (tasq_opts.tile - 1): output tile,
+ * K bytes per step, waves per workgroup. */
+enum {
+    TASQ_TILE_256x256_K128_W8 = 0,
+    TASQ_TILE_256x256_K64_W8 = 1,
+    TASQ_TILE_128x128_K128_W4 = 2,
+    TASQ_TILE_64x64_K128_W4 = 3,
+    TASQ_TILE_256x128_K64_W4 = 4,
+    TASQ_TILE_128x256_K64_W4 = 5,
+    TASQ_TILE_COUNT = 6
+};
+
+/* Packed-weight tile configurations (tasq_opts.packed_tile - 1). */
+enum {
+    TASQ_PTILE_256x256_K128_W8 = 0,
+    TASQ_PTILE_256x256_K64_W8 = 1,
+    TASQ_PTILE_128x256_K128_W4 = 2,
+    TASQ_PTILE_128x256_K64_W4 = 3,
+    TASQ_PTILE_256x128_K64_W4 = 4,
+    TASQ_PTILE_128x128_K64_W4 = 5,
+    TASQ_PTILE_64x64_K128_W4 = 6,
+    TASQ_PTILE_COUNT = 7
+};
 typedef struct tasq_opts {
     int32_t variant;
     int32_t split_k;
@@ -155,6 +205,12 @@ typedef struct tasq_opts {
     int32_t lowrank_rank;
     const float *w_zero;
     const int32_t *x_rowsums;
+    int32_t tile;
+    int32_t packed_tile;
+    int32_t persistent;
+    int32_t persistent_wgs;
+    int32_t persistent_parties;
+    void **step_events;
 } tasq_opts;
 
 /*

@@ -49,6 +49,8 @@ def lib():
         p = ctypes.c_void_p
         i64 = ctypes.c_int64
         L.oracle_num_threads.restype = ctypes.c_int
+        L.oracle_set_num_threads.argtypes = [ctypes.c_int]
+        L.oracle_set_num_threads.restype = None
         L.oracle_mask.argtypes = [p, i64, ctypes.c_int, p]
         L.oracle_stage_of_step.argtypes = [ctypes.c_int] * 3
         L.oracle_masked_linear.argtypes = [p, p, ctypes.c_double, p, p, i64, i64, i64,
@@ -91,6 +93,11 @@ def _ptr(a):
 
 def num_threads() -> int:
     return lib().oracle_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads of the oracle's following calls."""
+    lib().oracle_set_num_threads(int(n))
 
 
 def mask(W, b: int) -> np.ndarray:

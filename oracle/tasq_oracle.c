@@ -51,6 +51,17 @@ int oracle_num_threads(void)
 #endif
 }
 
+/* Threads of the following calls (the CPU baseline times one and all). */
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* floor(w / 2^k) toward minus infinity, by integer division and correction. */
 static int64_t floor_div_pow2(int64_t w, int k)
 {

@@ -53,7 +53,16 @@ class Opts(ctypes.Structure):
                 ("act_params", ctypes.c_void_p), ("colsums", ctypes.c_void_p),
                 ("lowrank_T", ctypes.c_void_p), ("lowrank_up", ctypes.c_void_p),
                 ("lowrank_rank", ctypes.c_int32), ("w_zero", ctypes.c_void_p),
-                ("x_rowsums", ctypes.c_void_p)]
+                ("x_rowsums", ctypes.c_void_p), ("tile", ctypes.c_int32),
+                ("packed_tile", ctypes.c_int32), ("persistent", ctypes.c_int32),
+                ("persistent_wgs", ctypes.c_int32), ("persistent_parties", ctypes.c_int32),
+                ("step_events", ctypes.POINTER(ctypes.c_void_p))]
+
+
+# Tuning overrides of tasq_opts (sweeps and tests): staged and packed tile ids.
+TILE_COUNT = 6
+PTILE_COUNT = 7
+TUNING_FIELDS = ("tile", "packed_tile", "persistent", "persistent_wgs", "persistent_parties")
 
 
 class Cost(ctypes.Structure):

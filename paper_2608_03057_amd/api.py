@@ -38,8 +38,15 @@ def _need(t: Optional[torch.Tensor], dtype, shape, name):
 
 
 def _opts(variant, planes, workspace, split_k, packed=None, act=None, colsums=None,
-          lowrank=None, wzero=None) -> Opts:
+          lowrank=None, wzero=None, tune=None) -> Opts:
+    """``tune``: dict of tasq_opts tuning overrides (tile, packed_tile,
+    persistent, persistent_wgs, persistent_parties; values as the header
+    documents them, 0 = the library's choice)."""
     o = Opts()
+    for k, v in (tune or {}).items():
+        if k not in _lib.TUNING_FIELDS:
+            raise ValueError(f"unknown tuning field {k}")
+        setattr(o, k, int(v))
     o.variant = variant
     o.split_k = split_k
     o.W_planes = _ptr(planes)
@@ -220,8 +227,10 @@ def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: tor
                   planes: Optional[torch.Tensor] = None, packed: Optional[torch.Tensor] = None,
                   workspace: Optional[torch.Tensor] = None, split_k: int = 0,
                   act: Optional[torch.Tensor] = None, colsums: Optional[torch.Tensor] = None,
-                  lowrank=None, wzero=None):
+                  lowrank=None, wzero=None, tune: Optional[dict] = None):
     """(acc int32 [M, N] or None, y fp32 [M, N] or None) of the masked layer.
+    ``workspace`` (uint8, at least workspace_bytes(M, N, K) bytes) lets the
+    library cut a long K into ranges (split_k); none is allocated here.
     With ``act`` (params of quantize_activations) and ``colsums`` X holds
     asymmetric activation codes and sx is ignored.  ``lowrank`` = (T, up)
     adds the low-rank branch T up^T to y (T from lowrank_down, up bfloat16
@@ -240,12 +249,8 @@ def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: tor
         y = torch.empty((M, N), dtype=torch.float32, device=X.device)
     _need(acc, torch.int32, (M, N), "acc")
     _need(y, torch.float32, (M, N), "y")
-    if workspace is None and acc is None and M > 0 and N > 0:
-        wb = workspace_bytes(M, N, K)
-        if wb:
-            workspace = torch.empty(wb, dtype=torch.uint8, device=X.device)
     _need(colsums, torch.int32, (8, N), "colsums")
-    o = _opts(variant, planes, workspace, split_k, packed, act, colsums, lowrank, wzero)
+    o = _opts(variant, planes, workspace, split_k, packed, act, colsums, lowrank, wzero, tune)
     rc = _lib.lib().tasq_masked_linear(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias), M, N,
                                        K, int(b), _ptr(acc), _ptr(y), ctypes.byref(o), _stream())
     check(rc, "tasq_masked_linear")
@@ -255,8 +260,10 @@ def masked_linear(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: tor
 def masked_conv3x3(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: torch.Tensor,
                    b: int, bias: Optional[torch.Tensor] = None, *, want_acc: bool = True,
                    want_y: bool = True, acc=None, y=None, workspace=None, split_k: int = 0,
-                   packed: Optional[torch.Tensor] = None, variant: int = _lib.VARIANT_AUTO):
-    """3x3 / pad 1 conv, X NHWC [H, Wd, C], W [N, 3, 3, C] -> [H, Wd, N]."""
+                   packed: Optional[torch.Tensor] = None, variant: int = _lib.VARIANT_AUTO,
+                   tune: Optional[dict] = None):
+    """3x3 / pad 1 conv, X NHWC [H, Wd, C], W [N, 3, 3, C] -> [H, Wd, N].
+    ``workspace`` as in masked_linear (with M = H*Wd, K = 9*C)."""
     H, Wd, C = X.shape
     N = sw.shape[0]
     _need(X, torch.int8, (H, Wd, C), "X")
@@ -270,7 +277,7 @@ def masked_conv3x3(X: torch.Tensor, W: Optional[torch.Tensor], sx: float, sw: to
         y = torch.empty((H, Wd, N), dtype=torch.float32, device=X.device)
     _need(acc, torch.int32, (H, Wd, N), "acc")
     _need(y, torch.float32, (H, Wd, N), "y")
-    o = _opts(variant, None, workspace, split_k, packed)
+    o = _opts(variant, None, workspace, split_k, packed, tune=tune)
     rc = _lib.lib().tasq_masked_conv3x3(_ptr(X), _ptr(W), float(sx), _ptr(sw), _ptr(bias), H, Wd,
                                         C, N, int(b), _ptr(acc), _ptr(y), ctypes.byref(o),
                                         _stream())
@@ -342,14 +349,26 @@ def schedule_cost(layers, table, S: int, T: int, t_begin: int, t_end: int,
 
 def run_schedule(layers: Sequence[Layer], table: torch.Tensor, S: int, T: int, t_begin: int,
                  t_end: int, *, workspace: Optional[torch.Tensor] = None,
-                 variant: int = _lib.VARIANT_AUTO) -> None:
-    """Runs steps t_begin..t_end-1; ``table`` is a host uint8 [L, S] tensor."""
+                 variant: int = _lib.VARIANT_AUTO, split_k: int = 0,
+                 tune: Optional[dict] = None, step_events=None) -> None:
+    """Runs steps t_begin..t_end-1; ``table`` is a host uint8 [L, S] tensor.
+    ``step_events``: 2 * (t_end - t_begin) torch.cuda.Event objects, each
+    recorded once already (torch creates the event at its first record); the
+    library records pair i around the launches of step t_begin + i."""
     table = table.to(torch.uint8).contiguous().cpu()
     L = len(layers)
     if tuple(table.shape) != (L, S):
         raise ValueError(f"table must be [{L}, {S}]")
     arr = _layer_array(layers)
-    o = _opts(variant, None, workspace, 0)
+    o = _opts(variant, None, workspace, split_k, tune=tune)
+    if step_events is not None:
+        if len(step_events) != 2 * (t_end - t_begin):
+            raise ValueError("step_events needs 2 * (t_end - t_begin) events")
+        handles = [int(e.cuda_event) for e in step_events]
+        if not all(handles):
+            raise ValueError("record each step event once before passing it")
+        evarr = (ctypes.c_void_p * len(handles))(*handles)
+        o.step_events = ctypes.cast(evarr, ctypes.POINTER(ctypes.c_void_p))
     rc = _lib.lib().tasq_run_schedule(arr, L, table.data_ptr(), S, T, t_begin, t_end,
                                       ctypes.byref(o), _stream())
     check(rc, "tasq_run_schedule")

@@ -23,7 +23,7 @@ namespace tasq {
 namespace {
 
 // Order-preserving map of a finite float to uint32, so that min / max are
-// unsigned integer min / max (atomics on global memory).
+// unsigned integer min / max, whatever order the partial ranges are folded in.
 __device__ __forceinline__ uint32_t order_key(float f)
 {
     const uint32_t u = __float_as_uint(f);

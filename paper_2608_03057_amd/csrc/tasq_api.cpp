@@ -60,6 +60,8 @@ double xcd_imbalance(const std::vector<LayerDesc> &descs, long long G)
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+int variant_of_opts(const tasq_opts *o) { return o ? o->variant : TASQ_VARIANT_AUTO; }
+
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 int check_dims(long long M, long long N, long long K)
@@ -71,75 +73,63 @@ int check_dims(long long M, long long N, long long K)
     return TASQ_OK;
 }
 
-int check_variant(const tasq_opts *o, const int8_t *W)
+// The variant value, split_k and the alignment of the optional buffers.
+// Whether the layer has the weight copy its variant reads is checked per
+// layer (check_weights).
+int check_variant(const tasq_opts *o)
 {
-    const int v = o ? o->variant : TASQ_VARIANT_AUTO;
+    const int v = variant_of_opts(o);
     if (v != TASQ_VARIANT_AUTO && v != TASQ_VARIANT_MASKED_I8 && v != TASQ_VARIANT_BITPLANE &&
         v != TASQ_VARIANT_PACKED)
         return TASQ_ERR_KIND;
     if (o && o->split_k < 0)
         return TASQ_ERR_RANGE;
-    const bool planes = o && o->W_planes, packed = o && o->W_packed;
-    if (v == TASQ_VARIANT_BITPLANE && !planes)
-        return TASQ_ERR_LAYOUT;
-    if (v == TASQ_VARIANT_PACKED && !packed)
-        return TASQ_ERR_LAYOUT;
-    // The row-major weight is needed unless the chosen variant reads another
-    // copy: the planes (BITPLANE) or the packed buffer (PACKED, or AUTO when
-    // one is given).
-    const bool other = v == TASQ_VARIANT_BITPLANE ||
-                       (packed && (v == TASQ_VARIANT_PACKED || v == TASQ_VARIANT_AUTO));
-    if (!other && !W)
-        return TASQ_ERR_NULL;
-    if (packed && !aligned16(o->W_packed))
+    if (o && o->W_packed && !aligned16(o->W_packed))
         return TASQ_ERR_ALIGN;
     if (o && o->workspace && (reinterpret_cast<uintptr_t>(o->workspace) % kWsAlign) != 0)
         return TASQ_ERR_ALIGN;
     return TASQ_OK;
 }
 
-// TASQ_TILE=<id> / TASQ_PTILE=<id> force one tile configuration of the
-// staged / packed-weight kernels (tuning sweeps only).
-int forced(const char *name, int count)
+// Tuning overrides carried in tasq_opts (0 = the library's choice).
+int forced_tile(const tasq_opts *o) { return o && o->tile > 0 ? o->tile - 1 : -1; }
+
+int forced_ptile(const tasq_opts *o) { return o && o->packed_tile > 0 ? o->packed_tile - 1 : -1; }
+
+int check_tuning(const tasq_opts *o)
 {
-    const char *e = std::getenv(name);
-    if (!e || !*e)
-        return -1;
-    const int t = std::atoi(e);
-    return (t >= 0 && t < count) ? t : -1;
+    if (!o)
+        return TASQ_OK;
+    if (o->tile < 0 || o->tile > tasq::TILE_COUNT || o->packed_tile < 0 ||
+        o->packed_tile > tasq::PTILE_COUNT || o->persistent < 0 || o->persistent > 2 ||
+        o->persistent_wgs < 0 || o->persistent_wgs > 1024 || o->persistent_parties < 0 ||
+        o->persistent_parties > 1024)
+        return TASQ_ERR_RANGE;
+    return TASQ_OK;
 }
-
-int forced_tile() { return forced("TASQ_TILE", tasq::TILE_COUNT); }
-
-int forced_ptile() { return forced("TASQ_PTILE", tasq::PTILE_COUNT); }
 
 // The grouped step over linear layers without low-rank or weight-zero-point
 // terms runs as a persistent launch (one workgroup per compute unit, tile
 // boundaries overlapped) with the 256x256 tile once there are at least two
-// tiles per compute unit.  TASQ_PERSISTENT=0 / 1 forces it off / on whatever
-// the tile and the tile count, and TASQ_PERSISTENT_WGS=n sets the workgroups
-// per XCD (tuning sweeps and tests only).
-bool use_persistent(int tile, long long total)
+// tiles per compute unit, unless the caller forces it off or on.
+bool use_persistent(const tasq_opts *o, int tile, long long total)
 {
-    const int f = forced("TASQ_PERSISTENT", 2);
-    if (f >= 0)
-        return f == 1;
+    if (o && o->persistent)
+        return o->persistent == 2;
     return tile == tasq::TILE_256x256_K128_W8_PF1 && total >= 2LL * kComputeUnits;
 }
 
-int persistent_wgs_per_xcd()
+int persistent_wgs_per_xcd(const tasq_opts *o)
 {
-    const int f = forced("TASQ_PERSISTENT_WGS", 1025);
-    return f >= 1 ? f : kComputeUnits / kXcds;
+    return o && o->persistent_wgs > 0 ? o->persistent_wgs : kComputeUnits / kXcds;
 }
 
 // Parts of each XCD's run walked side by side by the persistent launch;
-// TASQ_PERSISTENT_PARTIES=n sets it (tuning sweeps and tests only).  Falls
-// back to 1 when n does not divide the workgroups per XCD.
-int persistent_parties(int wgs_per_xcd)
+// falls back to 1 when the requested count does not divide the workgroups
+// per XCD.
+int persistent_parties(const tasq_opts *o, int wgs_per_xcd)
 {
-    const int f = forced("TASQ_PERSISTENT_PARTIES", 1025);
-    const int p = f >= 1 ? f : 1;
+    const int p = o && o->persistent_parties > 0 ? o->persistent_parties : 1;
     return wgs_per_xcd % p == 0 ? p : 1;
 }
 
@@ -149,9 +139,9 @@ int persistent_parties(int wgs_per_xcd)
 // 256x256 tiles beats 2-3 waves of smaller ones from about there), the
 // 4-wave 128x256 tile (two workgroups per CU) while it gives 200 tiles, and
 // 64x64 tiles below that.
-int pick_packed_tile(long long M, long long N, long long K)
+int pick_packed_tile(const tasq_opts *o, long long M, long long N, long long K)
 {
-    const int f = forced_ptile();
+    const int f = forced_ptile(o);
     if (f >= 0)
         return f;
     const long long t256 = ((M + 255) / 256) * ((N + 255) / 256);
@@ -164,9 +154,9 @@ int pick_packed_tile(long long M, long long N, long long K)
 }
 
 // Packed-weight tile of the grouped per-step launch.
-int pick_packed_grouped_tile()
+int pick_packed_grouped_tile(const tasq_opts *o)
 {
-    const int f = forced_ptile();
+    const int f = forced_ptile(o);
     return f >= 0 ? f : tasq::PTILE_256x256_K128_W8;
 }
 
@@ -174,9 +164,9 @@ int pick_packed_grouped_tile()
 // tiles (8 waves, BK 128) from 140 tiles up, 128x128 tiles while they give
 // 200 tiles, 64x64 tiles below that so that more workgroups cover the 256
 // compute units.
-int pick_tile(long long M, long long N)
+int pick_tile(const tasq_opts *o, long long M, long long N)
 {
-    const int f = forced_tile();
+    const int f = forced_tile(o);
     if (f >= 0)
         return f;
     const long long t256 = ((M + 255) / 256) * ((N + 255) / 256);
@@ -250,9 +240,9 @@ size_t schedule_partials_offset(int L)
            round_up((size_t)L * 64, kWsAlign);
 }
 
-int pick_split_tile()
+int pick_split_tile(const tasq_opts *o)
 {
-    const int f = forced_tile();
+    const int f = forced_tile(o);
     return f >= 0 ? f : tasq::TILE_256x256_K128_W8_PF1;
 }
 
@@ -262,9 +252,9 @@ int pick_split_tile()
 // SDXL-Turbo block: K = 11520 against 0.5 GOP per CU), and 128x128 tiles cut
 // it by four (measured 0.230 -> 0.178 ms per step there, no change on the
 // DiT blocks, which keep 256x256).
-int pick_grouped_tile(const std::vector<LayerDesc> &descs)
+int pick_grouped_tile(const tasq_opts *o, const std::vector<LayerDesc> &descs)
 {
-    const int f = forced_tile();
+    const int f = forced_tile(o);
     if (f >= 0)
         return f;
     double total = 0, longest = 0;
@@ -278,14 +268,6 @@ int pick_grouped_tile(const std::vector<LayerDesc> &descs)
 }
 
 bool use_bitplane(const tasq_opts *o) { return o && o->variant == TASQ_VARIANT_BITPLANE; }
-
-// The packed-weight kernels run when the layer has a packed buffer and the
-// variant allows it (PACKED, or AUTO).
-bool use_packed(const LayerDesc &d, const tasq_opts *o)
-{
-    const int v = o ? o->variant : TASQ_VARIANT_AUTO;
-    return d.Wp && (v == TASQ_VARIANT_PACKED || v == TASQ_VARIANT_AUTO);
-}
 
 // The buffer-offset fast path also needs each input below 2 GiB.
 bool fits_buffers(const LayerDesc &d)
@@ -301,6 +283,12 @@ bool packed_fits(const LayerDesc &d)
     return tasq::packed_weight_bytes_host(d.N, d.K) < (1ULL << 31);
 }
 
+// The planes are addressed with 32-bit offsets by the weight-streaming kernel.
+bool planes_fit(const LayerDesc &d)
+{
+    return (long long)8 * ((d.K + 127) / 128) * d.N * 16 < (1LL << 31);
+}
+
 // Activation operand on the 16-byte buffer fast path.
 bool x_aligned(const LayerDesc &d)
 {
@@ -308,24 +296,75 @@ bool x_aligned(const LayerDesc &d)
     return inner % 16 == 0 && aligned16(d.X) && fits_buffers(d);
 }
 
-// Weight-streaming path for skinny activations: linear layers with M <= 64
-// and 16-byte activation rows, reading the planes (BITPLANE), the packed
-// buffer (when the variant allows it) or the aligned int8 rows.  Returns
-// false when none applies.
-bool skinny_source(const LayerDesc &d, const tasq_opts *o, tasq::SkinnyWeights &src)
+// A linear layer that the weight-streaming kernels take: few tokens and
+// 16-byte activation rows.
+bool skinny_shape(const LayerDesc &d)
 {
-    if (d.kind != tasq::KIND_LINEAR || d.M > tasq::kSkinnyMaxM || !x_aligned(d))
+    return d.kind == tasq::KIND_LINEAR && d.M <= tasq::kSkinnyMaxM && x_aligned(d);
+}
+
+// Which stored copy of the weight a layer reads.
+enum WeightSrc { SRC_NONE = 0, SRC_ROWS, SRC_PACKED, SRC_PLANES };
+
+// The variant names the copy; AUTO picks by shape from what is present.
+// With few tokens the layer is a weight stream whose time follows the
+// bytes read, so AUTO reads the top b planes there (App. G.2: only the
+// surviving planes are fetched).  Measured on the 112-layer PixArt-shaped
+// schedule at M = 16 (ms per denoising step, TASQ table of mean 4.94 bits /
+// static b = 8): planes 0.083 / 0.112, packed int8 0.105 / 0.105, int8 rows
+// 0.126 / 0.121.  The plane stream wins at every b below 8; at b = 8 it reads
+// as many bytes as the int8 copy and the packed stream is 6% faster, so
+// there AUTO prefers the packed copy when one is given.  For M in the
+// thousands the weights are a few percent of the traffic and rebuilding the
+// bytes from planes per output tile costs more than it saves, so AUTO takes
+// the packed copy, then the rows, and the bit-plane GEMM only when no other
+// copy is given.  any_below8: the layer runs at some b below 8 (its b for
+// a single call; any entry of its table row for a schedule).
+WeightSrc weight_source(const LayerDesc &d, const tasq_opts *o, bool any_below8)
+{
+    const bool rows = d.W != nullptr, packed = d.Wp != nullptr, planes = d.P != nullptr;
+    switch (variant_of_opts(o)) {
+    case TASQ_VARIANT_BITPLANE:
+        return planes && d.kind == tasq::KIND_LINEAR ? SRC_PLANES : SRC_NONE;
+    case TASQ_VARIANT_PACKED:
+        return packed ? SRC_PACKED : SRC_NONE;
+    case TASQ_VARIANT_MASKED_I8:
+        return rows ? SRC_ROWS : SRC_NONE;
+    default:
+        break;
+    }
+    const bool linear = d.kind == tasq::KIND_LINEAR;
+    if (planes && linear && skinny_shape(d) && planes_fit(d) && (any_below8 || !packed))
+        return SRC_PLANES;
+    if (packed)
+        return SRC_PACKED;
+    if (rows)
+        return SRC_ROWS;
+    if (planes && linear)
+        return SRC_PLANES;
+    return SRC_NONE;
+}
+
+// Weight-streaming path for skinny activations: linear layers with M <= 64
+// and 16-byte activation rows, reading the weight copy `src`.  Returns false
+// when that copy cannot be streamed.
+bool skinny_source(const LayerDesc &d, WeightSrc src, tasq::SkinnyWeights &out)
+{
+    if (!skinny_shape(d))
         return false;
-    if (use_bitplane(o)) {
-        src = tasq::SKINNY_PLANES;
-        return d.P && (long long)8 * ((d.K + 127) / 128) * d.N * 16 < (1LL << 31);
+    switch (src) {
+    case SRC_PLANES:
+        out = tasq::SKINNY_PLANES;
+        return planes_fit(d);
+    case SRC_PACKED:
+        out = tasq::SKINNY_PACKED;
+        return packed_fits(d);
+    case SRC_ROWS:
+        out = tasq::SKINNY_ROWS;
+        return aligned16(d.W);
+    default:
+        return false;
     }
-    if (use_packed(d, o) && packed_fits(d)) {
-        src = tasq::SKINNY_PACKED;
-        return true;
-    }
-    src = tasq::SKINNY_ROWS;
-    return d.W && aligned16(d.W);
 }
 
 int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream,
@@ -334,17 +373,18 @@ int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream,
     if (d.M == 0 || d.N == 0)
         return TASQ_OK;
     hipError_t e;
-    const bool want_planes = use_bitplane(o);
+    const WeightSrc wsrc = weight_source(d, o, d.bits < 8);
     tasq::SkinnyWeights src;
-    if (skinny_source(d, o, src)) {
+    if (skinny_source(d, wsrc, src)) {
         e = tasq::launch_skinny(d, src, stream);
         return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
     }
-    if (!want_planes && use_packed(d, o) && packed_fits(d)) {
-        e = tasq::packed_tile_ops(pick_packed_tile(d.M, d.N, d.K)).single(d, x_aligned(d), stream);
+    if (wsrc == SRC_PACKED && packed_fits(d)) {
+        e = tasq::packed_tile_ops(pick_packed_tile(o, d.M, d.N, d.K))
+                .single(d, x_aligned(d), stream);
         return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
     }
-    if (want_planes) {
+    if (wsrc == SRC_PLANES) {
         e = tasq::tile_ops(tasq::TILE_64x64_K128_W4_PF2).planes(
             d, (d.K % 16) == 0 && aligned16(d.X) && fits_buffers(d), stream);
     } else {
@@ -373,11 +413,11 @@ int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream,
         }
         if (splits > 1) {
             int32_t *part = static_cast<int32_t *>(o->workspace);
-            e = tasq::tile_ops(pick_split_tile()).split(d, part, splits, kchunk, stream);
+            e = tasq::tile_ops(pick_split_tile(o)).split(d, part, splits, kchunk, stream);
             if (e == hipSuccess)
                 e = tasq::launch_split_finish(d, part, splits, stream);
         } else {
-            e = tasq::tile_ops(pick_tile(d.M, d.N)).single(d, aligned, stream);
+            e = tasq::tile_ops(pick_tile(o, d.M, d.N)).single(d, aligned, stream);
         }
     }
     return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
@@ -417,6 +457,25 @@ LayerDesc make_desc(const tasq_layer &L, const tasq_opts *o)
     d.Wd = L.Wd;
     d.C = L.C;
     return d;
+}
+
+// The layer has the weight copy its variant reads: the planes (BITPLANE),
+// the packed buffer (PACKED), the rows (MASKED_I8), or under AUTO any copy
+// that serves the layer kind (the planes serve linear layers only).  The
+// named copy must be present even when the layer is empty.
+int check_weights(const tasq_layer &L, const tasq_opts &o, bool needs_w)
+{
+    const int v = o.variant;
+    if (v == TASQ_VARIANT_BITPLANE && !o.W_planes)
+        return TASQ_ERR_LAYOUT;
+    if (v == TASQ_VARIANT_PACKED && !o.W_packed)
+        return TASQ_ERR_LAYOUT;
+    if (!needs_w || v == TASQ_VARIANT_BITPLANE || v == TASQ_VARIANT_PACKED)
+        return TASQ_OK;
+    if (v == TASQ_VARIANT_MASKED_I8)
+        return L.W ? TASQ_OK : TASQ_ERR_NULL;
+    const bool planes_serve = o.W_planes && L.kind == TASQ_KIND_LINEAR;
+    return L.W || o.W_packed || planes_serve ? TASQ_OK : TASQ_ERR_NULL;
 }
 
 // Validation shared by single calls and schedule layers.
@@ -483,7 +542,9 @@ int validate_layer(const tasq_layer &L, const tasq_opts *o)
             return TASQ_ERR_DIM;
     }
     const bool needs_w = L.N > 0 && L.K > 0;
-    if (int rc = check_variant(&local, needs_w ? L.W : reinterpret_cast<const int8_t *>(1)))
+    if (int rc = check_variant(&local))
+        return rc;
+    if (int rc = check_weights(L, local, needs_w))
         return rc;
     if (L.kind == TASQ_KIND_CONV3X3) {
         if (L.H < 0 || L.Wd < 0 || L.C < 0 || L.N < 0)
@@ -576,6 +637,8 @@ int tasq_masked_linear(const int8_t *X, const int8_t *W, float sx, const float *
     L.bias = bias;
     L.acc = acc_out;
     L.y = y_out;
+    if (int rc = check_tuning(opts))
+        return rc;
     if (int rc = validate_layer(L, opts))
         return rc;
     if (b < 1 || b > 8)
@@ -612,6 +675,8 @@ int tasq_masked_conv3x3(const int8_t *X, const int8_t *W, float sx, const float 
     L.bias = bias;
     L.acc = acc_out;
     L.y = y_out;
+    if (int rc = check_tuning(opts))
+        return rc;
     if (int rc = validate_layer(L, opts))
         return rc;
     if (b < 1 || b > 8)
@@ -780,6 +845,16 @@ size_t tasq_schedule_workspace_bytes(const tasq_layer *layers, int L)
                                                  : 0);
 }
 
+// step_events[i] (caller-created hipEvent_t), when the caller asked for them.
+static int record_step_event(const tasq_opts *o, int i, hipStream_t st)
+{
+    if (!o || !o->step_events)
+        return TASQ_OK;
+    return hipEventRecord(static_cast<hipEvent_t>(o->step_events[i]), st) == hipSuccess
+               ? TASQ_OK
+               : TASQ_ERR_HIP;
+}
+
 static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_table, int S,
                              int T, int t_begin, int t_end, const tasq_opts *opts, void *stream)
 {
@@ -793,6 +868,8 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
         return TASQ_ERR_RANGE;
     if (opts && opts->workspace && (reinterpret_cast<uintptr_t>(opts->workspace) % kWsAlign))
         return TASQ_ERR_ALIGN;
+    if (int rc = check_tuning(opts))
+        return rc;
     for (int l = 0; l < L; ++l) {
         if (int rc = validate_layer(layers[l], opts))
             return rc;
@@ -821,22 +898,36 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
     // Otherwise each layer is launched on its own.
     const size_t need = tasq_schedule_workspace_bytes(layers, L);
     const bool have_ws = opts && opts->workspace && opts->workspace_bytes >= need;
+    // The weight copy each layer reads (AUTO: by shape, see weight_source),
+    // with "some b below 8" taken over the stages the steps touch.
+    const int s_first = tasq_stage_of_step(t_begin, S, T);
+    const int s_last = tasq_stage_of_step(t_end - 1, S, T);
+    std::vector<WeightSrc> wsrc(L);
+    for (int l = 0; l < L; ++l) {
+        bool below8 = false;
+        for (int s = s_first; s <= s_last; ++s)
+            below8 = below8 || b_table[(size_t)l * S + s] < 8;
+        wsrc[l] = weight_source(descs[l], opts, below8);
+    }
     tasq::SkinnyWeights src = tasq::SKINNY_ROWS;
     bool all_skinny = have_ws;
     int max_m = 0;
     for (int l = 0; all_skinny && l < L; ++l) {
         tasq::SkinnyWeights sl;
-        all_skinny = skinny_source(descs[l], opts, sl) && (l == 0 || sl == src);
+        all_skinny = skinny_source(descs[l], wsrc[l], sl) && (l == 0 || sl == src);
         src = sl;
         max_m = descs[l].M > max_m ? descs[l].M : max_m;
     }
-    bool all_packed = !use_bitplane(opts);
+    bool all_packed = true;
     for (int l = 0; l < L; ++l)
-        all_packed = all_packed && use_packed(descs[l], opts) && packed_fits(descs[l]);
-    bool grouped = have_ws && !use_bitplane(opts);
+        all_packed = all_packed && wsrc[l] == SRC_PACKED && packed_fits(descs[l]);
+    const int v = variant_of_opts(opts);
+    bool grouped = have_ws && v != TASQ_VARIANT_BITPLANE;
     for (int l = 0; grouped && l < L; ++l) {
         const LayerDesc &d = descs[l];
-        grouped = x_aligned(d) && (all_packed || (d.W && aligned16(d.W)));
+        const bool staged = v != TASQ_VARIANT_PACKED && wsrc[l] != SRC_PLANES && d.W &&
+                            aligned16(d.W);
+        grouped = x_aligned(d) && (all_packed || staged);
     }
     if (all_skinny || grouped) {
         for (int l = 0; l < L; ++l)
@@ -881,11 +972,11 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
             // one unit per 32 output channels, all tokens
             ts = {tasq::kSkinnyMaxM, 32, 128};
         } else if (all_packed) {
-            const tasq::PackedTileOps &ops = tasq::packed_tile_ops(pick_packed_grouped_tile());
+            const tasq::PackedTileOps &ops = tasq::packed_tile_ops(pick_packed_grouped_tile(opts));
             ts = ops.shape;
             launch_step = ops.grouped;
         } else {
-            const int tile = pick_grouped_tile(descs);
+            const int tile = pick_grouped_tile(opts, descs);
             const tasq::TileOps &ops = tasq::tile_ops(tile);
             ts = ops.shape;
             launch_step = ops.grouped;
@@ -909,10 +1000,10 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
         }
         if (total == 0 && solo.empty())
             return TASQ_OK;
-        if (!use_persistent(persistent_tile, total))
+        if (!use_persistent(opts, persistent_tile, total))
             launch_persistent = nullptr;
-        const int wgs_per_xcd = persistent_wgs_per_xcd();
-        const int parties = persistent_parties(wgs_per_xcd);
+        const int wgs_per_xcd = persistent_wgs_per_xcd(opts);
+        const int parties = persistent_parties(opts, wgs_per_xcd);
         // The GEMM kernels give each XCD one contiguous run of the work
         // units (for L2 locality), equal in count.  When the layers' tiles
         // differ in cost (K) and the layer order leaves one run much heavier
@@ -952,18 +1043,27 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
         if (hipMemcpyAsync(d_table, table.data(), (size_t)L * S, hipMemcpyHostToDevice, st) !=
             hipSuccess)
             return TASQ_ERR_HIP;
+        // Schedules ignore split_k: a layer launched on its own takes the
+        // automatic split over the partials room, which
+        // tasq_schedule_workspace_bytes reserved for it.
         tasq_opts sopts = *opts;
+        sopts.split_k = 0;
         sopts.workspace = ws + schedule_partials_offset(L);
         sopts.workspace_bytes = opts->workspace_bytes - schedule_partials_offset(L);
         for (int t = t_begin; t < t_end; ++t) {
             const int s = tasq_stage_of_step(t, S, T);
+            if (int rc = record_step_event(opts, 2 * (t - t_begin), st))
+                return rc;
             for (LayerDesc d : solo) {
                 d.bits = b_table[(size_t)d.layer * S + s];
                 if (int rc = launch_layer(d, &sopts, st, true))
                     return rc;
             }
-            if (total == 0)
+            if (total == 0) {
+                if (int rc = record_step_event(opts, 2 * (t - t_begin) + 1, st))
+                    return rc;
                 continue;
+            }
             const hipError_t e =
                 all_skinny ? tasq::launch_skinny_grouped(d_descs, nseg, (int)total, max_m, src,
                                                          d_table, S, s, st)
@@ -973,17 +1073,23 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
                     : launch_step(d_descs, nseg, (int)total, d_table, S, s, any_conv, st);
             if (e != hipSuccess)
                 return TASQ_ERR_HIP;
+            if (int rc = record_step_event(opts, 2 * (t - t_begin) + 1, st))
+                return rc;
         }
         return TASQ_OK;
     }
 
     for (int t = t_begin; t < t_end; ++t) {
         const int s = tasq_stage_of_step(t, S, T);
+        if (int rc = record_step_event(opts, 2 * (t - t_begin), st))
+            return rc;
         for (int l = 0; l < L; ++l) {
             descs[l].bits = b_table[(size_t)l * S + s];
             if (int rc = launch_layer(descs[l], opts, st))
                 return rc;
         }
+        if (int rc = record_step_event(opts, 2 * (t - t_begin) + 1, st))
+            return rc;
     }
     return TASQ_OK;
 }

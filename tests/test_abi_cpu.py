@@ -349,3 +349,69 @@ def test_probe_library_exports_its_header_and_stays_out_of_the_abi():
     assert probe.tasq_probe_mfma_peak(4, 0, FAKE, None) == -1
     assert probe.tasq_probe_mfma_peak(4, 10, None, None) == -1
     assert probe.tasq_probe_mfma_chains() == 8
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """The ctypes structs mirror tasq_opts and tasq_layer field by field: a C
+    program compiled against include/tasq.h prints each field's offset and
+    the struct sizes."""
+    structs = {"tasq_opts": Opts, "tasq_layer": Layer}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "tasq.h"', "int main(void){"]
+    for cname, py in structs.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in py._fields_:
+            lines.append(f'printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines.append("return 0;}")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    import subprocess
+    subprocess.check_call(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src),
+                           "-o", str(exe)])
+    got = subprocess.check_output([str(exe)]).decode().split("\n")
+    for line in filter(None, got):
+        cname, field, val = line.split()
+        py = structs[cname]
+        want = ctypes.sizeof(py) if field == "size" else getattr(py, field).offset
+        assert int(val) == want, (cname, field, int(val), want)
+
+
+@pytest.mark.parametrize("kw", [dict(tile=-1), dict(tile=_lib.TILE_COUNT + 1),
+                                dict(packed_tile=_lib.PTILE_COUNT + 1), dict(persistent=3),
+                                dict(persistent=-1), dict(persistent_wgs=1025),
+                                dict(persistent_parties=-2)])
+def test_tuning_overrides_out_of_range(kw):
+    assert lin(opts=opts(**kw)) == _lib.TASQ_ERR_RANGE
+    assert sched([layer()], [8, 7, 6, 5], 4, 20, 0, 0, opts(**kw)) == _lib.TASQ_ERR_RANGE
+
+
+def test_tuning_overrides_in_range_pass_validation():
+    for kw in (dict(tile=_lib.TILE_COUNT), dict(packed_tile=1), dict(persistent=2),
+               dict(persistent_wgs=1024, persistent_parties=4)):
+        assert lin(M=0, opts=opts(**kw)) == _lib.TASQ_OK
+        assert sched([layer()], [8, 7, 6, 5], 4, 20, 0, 0, opts(**kw)) == _lib.TASQ_OK
+
+
+def test_schedule_ignores_split_k():
+    """split_k is a single-call control: a schedule validates with any
+    non-negative value (a long-K layer it launches on its own takes the
+    automatic split), and rejects a negative one like every call."""
+    tbl = [8, 7, 6, 5, 4, 3, 2, 1]
+    conv = layer(kind=_lib.KIND_CONV3X3, H=32, Wd=32, C=1280, M=1024, N=1280, K=11520)
+    for sk in (1, 2, 7, 16, 1000):
+        assert sched([layer(), conv], tbl, 4, 20, 0, 0, opts(split_k=sk)) == _lib.TASQ_OK
+    assert sched([layer(), conv], tbl, 4, 20, 0, 0, opts(split_k=-1)) == _lib.TASQ_ERR_RANGE
+
+
+def test_auto_reads_planes_when_no_other_copy():
+    """Under AUTO a linear layer may carry only the bit planes; a conv may
+    not (the bit-plane kernels are linear-only)."""
+    o = opts(W_planes=FAKE)
+    assert lin(W=None, M=0, opts=o) == _lib.TASQ_OK
+    assert lin(W=None, b=0, opts=o) == _lib.TASQ_ERR_BITS
+    assert sched([layer(W=None, W_planes=FAKE)] * 2, [8, 7, 6, 5, 4, 3, 2, 1], 4, 20, 0, 0) \
+        == _lib.TASQ_OK
+    conv = layer(kind=_lib.KIND_CONV3X3, H=2, Wd=2, C=16, M=4, K=144, W=None, W_planes=FAKE)
+    assert sched([conv], [8, 7, 6, 5], 4, 20, 0, 0) == _lib.TASQ_ERR_NULL
+    assert lin(W=None, M=0, opts=opts(variant=_lib.VARIANT_MASKED_I8, W_planes=FAKE)) \
+        == _lib.TASQ_ERR_NULL

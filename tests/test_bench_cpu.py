@@ -39,3 +39,19 @@ def test_kernel_source_hash_is_stable_and_per_kernel():
     b = bench.kernel_source_sha256("k_gemm_packed_grouped")
     assert a == bench.kernel_source_sha256("k_masked_gemm_grouped")
     assert len(a) == 64 and a != b
+
+
+def test_cpu_baseline_reports_one_and_all_threads():
+    """The oracle timed on a tiny budget: median TOPS for one thread and for
+    all threads, the thread counts, and the host's CPU count and model."""
+    import oracle
+    wl = inputs.workload(4)
+    r = bench.cpu_baseline(wl, inputs.b_table(wl), run_s=0.2, runs=3)
+    assert r["kind"] == "oracle" and r["unit"] == "TOPS"
+    assert r["runs"]["single_thread"]["threads"] == 1
+    assert r["runs"]["all_threads"]["threads"] == r["cores"] == oracle.num_threads()
+    for k in ("single_thread", "all_threads"):
+        v = r["runs"][k]
+        assert len(v["TOPS_runs"]) == 3 and v["TOPS_median"] > 0
+    assert r["value"] == r["all_threads_TOPS"]
+    assert r["nproc"] >= 1

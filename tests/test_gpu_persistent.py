@@ -1,9 +1,8 @@
 """The persistent form of the grouped step (one workgroup per compute unit
 walking its XCD's run of tiles, the next tile's first loads issued before
-the current tile's stores), forced through the library's tuning hooks
-(TASQ_PERSISTENT=1, TASQ_PERSISTENT_WGS workgroups per XCD,
-TASQ_PERSISTENT_PARTIES parts of each XCD's run walked side by side,
-TASQ_TILE),
+the current tile's stores), forced through the library's tuning overrides
+(tasq_opts.persistent = 2, persistent_wgs workgroups per XCD,
+persistent_parties parts of each XCD's run walked side by side, tile),
 against the oracle on ragged linear layers, symmetric and asymmetric codes,
 with and without bias.  With one or three workgroups per XCD every
 workgroup runs many tiles of several layers, so each tile boundary (a new
@@ -62,18 +61,15 @@ def check_layer(h, b, where):
 
 @pytest.mark.parametrize("tile,wgs,parties", [(0, 1, 1), (0, 3, 1), (0, 32, 1), (2, 1, 1),
                                               (3, 5, 1), (0, 4, 2), (0, 6, 3), (2, 32, 4)])
-def test_persistent_schedule(tile, wgs, parties, monkeypatch):
-    monkeypatch.setenv("TASQ_PERSISTENT", "1")
-    monkeypatch.setenv("TASQ_PERSISTENT_WGS", str(wgs))
-    monkeypatch.setenv("TASQ_PERSISTENT_PARTIES", str(parties))
-    monkeypatch.setenv("TASQ_TILE", str(tile))
+def test_persistent_schedule(tile, wgs, parties):
+    tune = dict(persistent=2, persistent_wgs=wgs, persistent_parties=parties, tile=tile + 1)
     host, layers, keep = build(70 + tile, asym_layers=(1, 3))
     S, Tn = 4, 20
     rng = np.random.default_rng(71 + wgs)
     table = torch.as_tensor(rng.integers(1, 9, size=(len(host), S)), dtype=torch.uint8)
     ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
     for (t0, t1) in [(0, 20), (0, 1), (6, 7), (12, 16)]:
-        T.run_schedule(layers, table, S, Tn, t0, t1, workspace=ws)
+        T.run_schedule(layers, table, S, Tn, t0, t1, workspace=ws, tune=tune)
         torch.cuda.synchronize()
         stage = oracle.stage_of_step(t1 - 1, S, Tn)
         for i, h in enumerate(host):
@@ -82,7 +78,7 @@ def test_persistent_schedule(tile, wgs, parties, monkeypatch):
                               f"b={b}")
 
 
-def test_persistent_matches_grouped(monkeypatch):
+def test_persistent_matches_grouped():
     """The persistent step (forced on) and the non-persistent grouped launch
     (forced off) write identical outputs at the 256x256 tile."""
     M, N, K = 2048, 2304, 256
@@ -100,12 +96,12 @@ def test_persistent_matches_grouped(monkeypatch):
     ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
     results = {}
     for mode in ("1", "0"):
-        monkeypatch.setenv("TASQ_PERSISTENT", mode)
+        tune = dict(persistent=2 if mode == "1" else 1)
         for (t0, t1) in [(0, 1), (19, 20)]:
             for acc, y in outs:
                 acc.fill_(12345)
                 y.fill_(-7.0)
-            T.run_schedule(layers, table, 4, 20, t0, t1, workspace=ws)
+            T.run_schedule(layers, table, 4, 20, t0, t1, workspace=ws, tune=tune)
             torch.cuda.synchronize()
             results[(mode, t0)] = [(a.cpu().clone(), v.cpu().clone()) for a, v in outs]
     for t0 in (0, 19):

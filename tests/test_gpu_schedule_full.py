@@ -45,21 +45,30 @@ def check_layer(wl, l, W, sw, y, acc, b, rng, where):
                   ry.reshape(spec.M, len(cols)), sx, sw[tc], None, f"{where} cols")
 
 
-def test_config4_schedule_bench_launch_sampled():
+@pytest.fixture(scope="module")
+def cfg4():
+    """Config 4's 112 layers on the GPU, drawn as bench.py draws them."""
     wl = inputs.workload(4)
     table = inputs.b_table(wl)
-    L = len(wl.layers)
-    Ws, sws, keep, ys, layers = [], [], [], [], []
+    Ws, sws, keep = [], [], []
     for l, spec in enumerate(wl.layers):
         X = inputs.x_full(wl, l, device=DEV)
         W = inputs.w_full(wl, l)
         sw = inputs.sw_full(wl, l)
-        Wd, swd = W.to(DEV), sw.to(DEV)
-        y = torch.full((spec.M, spec.N), -7.0, dtype=torch.float32, device=DEV)
-        layers.append(T.make_layer(X, Wd, wl.sx, swd, None, None, y))
-        keep.append((X, Wd, swd))
+        keep.append((X, W.to(DEV), sw.to(DEV)))
         Ws.append(W)
         sws.append(sw)
+    return wl, table, Ws, sws, keep
+
+
+def test_config4_schedule_bench_launch_sampled(cfg4):
+    wl, table, Ws, sws, keep = cfg4
+    L = len(wl.layers)
+    ys, layers = [], []
+    for l, spec in enumerate(wl.layers):
+        X, Wd, swd = keep[l]
+        y = torch.full((spec.M, spec.N), -7.0, dtype=torch.float32, device=DEV)
+        layers.append(T.make_layer(X, Wd, wl.sx, swd, None, None, y))
         ys.append(y)
     ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
     rng = np.random.default_rng(44)
@@ -88,6 +97,45 @@ def test_config4_schedule_bench_launch_sampled():
         b = int(table[l, stage])
         check_layer(wl, l, Ws[l], sws[l], ys[l].cpu(), accs[l].cpu(), b, rng,
                     f"config 4 [{t},{t + 1}) layer {l} b={b} with int32")
+
+
+def test_config4_comparison_tables_and_packed_weights_sampled(cfg4):
+    """The benchmark's comparison schedules at full size: the static b = 8
+    table and the per-layer maximum over stages through the same grouped
+    launch, and the TASQ table with every layer holding only its packed
+    weight (bench.py --weights packed: the grouped packed-weight launch);
+    sampled outputs of every seventh layer after the last step."""
+    wl, table, Ws, sws, keep = cfg4
+    L = len(wl.layers)
+    t8 = torch.full_like(table, 8)
+    tmax = table.max(dim=1, keepdim=True).values.expand_as(table).contiguous()
+    ys = [torch.empty((s.M, s.N), dtype=torch.float32, device=DEV) for s in wl.layers]
+    layers = [T.make_layer(keep[l][0], keep[l][1], wl.sx, keep[l][2], None, None, ys[l])
+              for l in range(L)]
+    ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
+    rng = np.random.default_rng(45)
+    stage = oracle.stage_of_step(wl.T - 1, wl.S, wl.T)
+    for name, tab in (("static b=8", t8), ("static max over stages", tmax)):
+        for y in ys:
+            y.fill_(-7.0)
+        T.run_schedule(layers, tab, wl.S, wl.T, wl.T - 2, wl.T, workspace=ws)
+        torch.cuda.synchronize()
+        for l in range(0, L, 7):
+            b = int(tab[l, stage])
+            check_layer(wl, l, Ws[l], sws[l], ys[l].cpu(), None, b, rng,
+                        f"config 4 {name} layer {l} b={b}")
+    packs = [T.pack_weights(keep[l][1]) for l in range(L)]
+    layers = [T.make_layer(keep[l][0], None, wl.sx, keep[l][2], None, None, ys[l],
+                           packed=packs[l]) for l in range(L)]
+    ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
+    for y in ys:
+        y.fill_(-7.0)
+    T.run_schedule(layers, table, wl.S, wl.T, wl.T - 2, wl.T, workspace=ws)
+    torch.cuda.synchronize()
+    for l in range(3, L, 7):
+        b = int(table[l, stage])
+        check_layer(wl, l, Ws[l], sws[l], ys[l].cpu(), None, b, rng,
+                    f"config 4 packed weights layer {l} b={b}")
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3])

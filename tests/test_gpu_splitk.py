@@ -114,3 +114,47 @@ def test_forced_split_needs_workspace():
     small = workspace(1024)
     with pytest.raises(T.TasqError):
         T.masked_linear(X.to(DEV), W.to(DEV), SX, sw.to(DEV), 8, split_k=4, workspace=small)
+
+
+@pytest.mark.parametrize("split_k", [1, 7, 16])
+def test_schedule_ignores_split_k(split_k):
+    """A schedule whose 3x3 conv (the SDXL-Turbo one: 32x32 pixels, K =
+    11520 -> 1280) runs on its own, split-K over the schedule workspace,
+    ahead of the grouped launch of a linear layer: with split_k set in the
+    call's options the call returns TASQ_OK and writes the same bits as with
+    split_k = 0, and sampled pixels match the oracle (int32 bit-exact)."""
+    wl = inputs.workload(3)
+    conv_spec, lin_spec = wl.layers[8], wl.layers[4]
+    Xc = inputs.x_full(wl, 8)
+    Wc = inputs.w_full(wl, 8).reshape(conv_spec.N, 3, 3, conv_spec.C)
+    swc = inputs.sw_full(wl, 8)
+    Xl, Wl, swl = inputs.x_full(wl, 4), inputs.w_full(wl, 4), inputs.sw_full(wl, 4)
+    dev = [Xc.to(DEV), Wc.to(DEV), swc.to(DEV), Xl.to(DEV), Wl.to(DEV), swl.to(DEV)]
+    outs = [torch.empty((conv_spec.H, conv_spec.Wd, conv_spec.N), dtype=torch.int32, device=DEV),
+            torch.empty((conv_spec.H, conv_spec.Wd, conv_spec.N), dtype=torch.float32,
+                        device=DEV),
+            torch.empty((lin_spec.M, lin_spec.N), dtype=torch.int32, device=DEV),
+            torch.empty((lin_spec.M, lin_spec.N), dtype=torch.float32, device=DEV)]
+    layers = [T.make_layer(dev[0], dev[1], SX, dev[2], None, outs[0], outs[1]),
+              T.make_layer(dev[3], dev[4], SX, dev[5], None, outs[2], outs[3])]
+    table = torch.tensor([[6, 5, 7, 8], [4, 8, 6, 5]], dtype=torch.uint8)
+    ws = workspace(T.schedule_workspace_bytes(layers))
+    assert T.schedule_workspace_bytes(layers) > T.workspace_bytes(conv_spec.M, conv_spec.N,
+                                                                  conv_spec.K)
+    T.run_schedule(layers, table, 4, 4, 1, 2, workspace=ws)
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in outs]
+    for o in outs:
+        o.fill_(-3)
+    T.run_schedule(layers, table, 4, 4, 1, 2, workspace=ws, split_k=split_k)
+    torch.cuda.synchronize()
+    for o, r in zip(outs, ref):
+        assert torch.equal(o, r), f"split_k={split_k}"
+    pix = [0, 31, 32, 555, 1023]
+    pp = np.repeat(np.array(pix), conv_spec.N)
+    cc = np.tile(np.arange(conv_spec.N), len(pix))
+    ra, ry = oracle.conv3x3_entries(Xc, Wc, SX, swc, 5, pp, cc)
+    ti = torch.as_tensor(pix)
+    check_outputs(outs[0].reshape(-1, conv_spec.N)[ti], outs[1].reshape(-1, conv_spec.N)[ti],
+                  ra.reshape(len(pix), conv_spec.N), ry.reshape(len(pix), conv_spec.N), SX, swc,
+                  None, f"conv in schedule, split_k={split_k}")

@@ -1,5 +1,5 @@
-"""Every tile configuration, forced through the library's tuning hooks
-(TASQ_TILE for the staged kernels, TASQ_PTILE for the packed-weight ones),
+"""Every tile configuration, forced through the library's tuning overrides
+(tasq_opts.tile for the staged kernels, packed_tile for the packed-weight ones),
 against the oracle: a ragged linear layer with bias, the same layer with
 every optional epilogue term at once (asymmetric codes, low-rank branch,
 weight zero points: the LDS staging those terms use is sized per tile), a
@@ -27,23 +27,24 @@ def layer_case(seed, M=300, N=200, K=304):
     return X, W, sw, bias
 
 
-def run_layer(X, W, sw, bias, b, packed, **kw):
+def run_layer(X, W, sw, bias, b, packed, tune, **kw):
     Wd = W.to(DEV)
     wkw = dict(packed=T.pack_weights(Wd)) if packed else {}
     return T.masked_linear(X.to(DEV) if X.device.type == "cpu" else X, None if packed else Wd,
-                           SX, sw.to(DEV), b, None if bias is None else bias.to(DEV), **wkw, **kw)
+                           SX, sw.to(DEV), b, None if bias is None else bias.to(DEV), **wkw,
+                           tune=tune, **kw)
 
 
 @pytest.mark.parametrize("kind,tile", [("staged", t) for t in range(STAGED)] +
                          [("packed", t) for t in range(PACKED)])
-def test_forced_tile(kind, tile, monkeypatch):
-    monkeypatch.setenv("TASQ_TILE" if kind == "staged" else "TASQ_PTILE", str(tile))
+def test_forced_tile(kind, tile):
     packed = kind == "packed"
+    tune = {"packed_tile" if packed else "tile": tile + 1}
     where = f"{kind} tile {tile}"
     # plain layer, ragged in M, N and K
     X, W, sw, bias = layer_case(600 + tile)
     for b in (8, 5, 1):
-        acc, y = run_layer(X, W, sw, bias, b, packed)
+        acc, y = run_layer(X, W, sw, bias, b, packed, tune)
         torch.cuda.synchronize()
         ra, ry = oracle.masked_linear(X, W, SX, sw, b, bias)
         check_outputs(acc, y, ra, ry, SX, sw, bias, f"{where} b={b}")
@@ -62,7 +63,7 @@ def test_forced_tile(kind, tile, monkeypatch):
     cs = T.weight_colsums(Qd)
     wkw = dict(packed=T.pack_weights(Qd)) if packed else {}
     acc, y = T.masked_linear(q, None if packed else Qd, 0.0, swd, 6, act=params, colsums=cs,
-                             lowrank=(Tg, dev_bf16(U)), wzero=(zwd, rs), **wkw)
+                             lowrank=(Tg, dev_bf16(U)), wzero=(zwd, rs), tune=tune, **wkw)
     torch.cuda.synchronize()
     ra, ry = oracle.layer_dequant(Xc, Wc, rsw, 6, act=(ax, zx), zw=zw)
     _, lr64 = oracle.lowrank(x, D, U)
@@ -84,7 +85,7 @@ def test_forced_tile(kind, tile, monkeypatch):
     Wt = inputs.random_case(631 + tile, 1, Nc, 9 * C)[1].reshape(Nc, 3, 3, C)
     ckw = dict(packed=T.pack_weights(Wt.to(DEV))) if packed else {}
     acc, y = T.masked_conv3x3(Xi.to(DEV), None if packed else Wt.to(DEV), SX, swc.to(DEV), 4,
-                              biasc.to(DEV), **ckw)
+                              biasc.to(DEV), tune=tune, **ckw)
     torch.cuda.synchronize()
     ra, ry = oracle.conv3x3(Xi, Wt, SX, swc, 4, biasc)
     check_outputs(acc, y, ra, ry, SX, swc, biasc, f"{where} conv")
@@ -97,7 +98,7 @@ def test_forced_tile(kind, tile, monkeypatch):
     layers = [T.make_layer(d["X"], None if packed else d["W"], SX, d["sw"], d.get("bias"),
                            d["acc"], d["y"], packed=p) for d, p in zip(dev, packs)]
     ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
-    T.run_schedule(layers, table, S_, Tn, 3, 11, workspace=ws)
+    T.run_schedule(layers, table, S_, Tn, 3, 11, workspace=ws, tune=tune)
     torch.cuda.synchronize()
     ref = oracle.run_schedule(host, table.numpy(), S_, Tn, 3, 11, SX)
     for h, d, (ra, ry, b) in zip(host, dev, ref):
