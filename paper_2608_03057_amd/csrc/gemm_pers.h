@@ -142,6 +142,66 @@ struct PersOperands {
     }
 };
 
+// The epilogue's per-column factors (as epilogue_cols in gemm_core.h), in
+// two parts: the loads, issued early and read with buffer loads (a
+// generic-pointer load would also count as an LDS access and be waited for
+// with every other memory request in flight), and the arithmetic, done when
+// the epilogue needs it, so that the loads' latency is not waited for at
+// the point of issue.
+template <class C>
+struct ColLoads {
+    float sw[C::FN], bias[C::FN];
+    int cs[C::FN];
+    float alpha, zx;
+};
+
+template <class C>
+__device__ __forceinline__ void cols_request(const LayerDesc &d, int n0, int bits,
+                                             ColLoads<C> &cl)
+{
+    const int lane = threadIdx.x & 63;
+    const int wn = (threadIdx.x >> 6) % C::WAVES_N;
+    const uint32_t nb = (uint32_t)d.N * 4u;
+    const rsrc_t rsw = make_rsrc(d.sw, d.sw ? nb : 0u);
+    const rsrc_t rbias = make_rsrc(d.bias, d.bias ? nb : 0u);
+    const rsrc_t rcs = make_rsrc(d.colsums, d.act ? 8u * nb : 0u);
+    const rsrc_t ract = make_rsrc(d.act, d.act ? 8u : 0u);
+    cl.alpha = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ract, 0, 0, 0));
+    cl.zx = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ract, 4, 0, 0));
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+        const int n = n0 + wn * C::WTN + j * 32 + (lane & 31);
+        const bool nok = n < d.N;
+        const uint32_t on = nok ? (uint32_t)n * 4u : kOOB;
+        cl.sw[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsw, on, 0, 0));
+        cl.bias[j] =
+            __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rbias, on, 0, 0));
+        cl.cs[j] = (int)__builtin_amdgcn_raw_buffer_load_b32(
+            rcs, nok ? ((uint32_t)(bits - 1) * (uint32_t)d.N + (uint32_t)n) * 4u : kOOB, 0, 0);
+    }
+}
+
+template <class C>
+__device__ __forceinline__ void cols_finish(const LayerDesc &d, int m0, int n0,
+                                            const ColLoads<C> &cl, EpiCols<C> &ec)
+{
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+    const int mrow = m0 + wm * C::WTM + 4 * (lane >> 5);
+    const bool asym = d.act != nullptr;
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+        const int n = n0 + wn * C::WTN + j * 32 + (lane & 31);
+        const bool nok = n < d.N;
+        ec.scale[j] = (asym ? cl.alpha : d.sx) * cl.sw[j];
+        ec.bias[j] = cl.bias[j];
+        ec.corr[j] = asym ? (128.0f - cl.zx) * (float)cl.cs[j] : 0.0f;
+        ec.wsc[j] = 0.f;
+        ec.base[j] = nok ? ((uint32_t)mrow * (uint32_t)d.N + (uint32_t)n) * 4u : kOOB;
+    }
+}
+
 // One workgroup per compute unit walks its XCD's run of work units (as in
 // k_masked_gemm_persistent).  g counts K tiles across the walk: K tile t of
 // the current tile is global K tile g0 + t, in activation stage (g0+t) % 3
@@ -193,11 +253,11 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
     // exists (one past K reads zero weights, or activation bytes of other
     // rows into a stage no K tile of this tile reads), so that the count of
     // requests in flight is the same at every wait.
-    auto issue_first = [&](int g0) {
-        ops.issue_a(a_stage(g0), 0);
-        ops.load_b(ring[0], 0);
-        ops.issue_a(a_stage(g0 + 1), 1);
-        ops.load_b(ring[1], 1);
+    auto issue_first = [&](int g0, int t0) {
+        ops.issue_a(a_stage(g0), t0);
+        ops.load_b(ring[0], t0);
+        ops.issue_a(a_stage(g0 + 1), t0 + 1);
+        ops.load_b(ring[1], t0 + 1);
     };
 
     int seg = find_segment(descs, L, u);
@@ -209,7 +269,7 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
     {
         const LayerDesc &d0 = descs[seg];
         ops.init(d0, m0, n0, tid);
-        issue_first(0);
+        issue_first(0, 0);
     }
     for (;;) {
         const LayerDesc &d = descs[seg];
@@ -263,6 +323,9 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
         auto ktile = [&](auto slot_tag, int t) {
             constexpr int slot = decltype(slot_tag)::value;
             const int g = g0 + t;
+            // Activation K tile t+2 goes to the stage K tile t-1 used (every
+            // wave finished reading it before the last barrier).
+            ops.issue_a(a_stage(g + 2), t + 2);
 #pragma unroll
             for (int kk = 0; kk + 1 < KK; ++kk) {
                 read(g, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
@@ -270,10 +333,8 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
                 if (kk == WRITE_KK) {
                     // weight K tile t+1 to the other weight stage (read in
                     // K tile t-1, done before the last barrier), then the
-                    // slot is refilled with K tile t+3; activation K tile
-                    // t+2 goes to the stage K tile t-1 used.
+                    // slot is refilled with K tile t+3.
                     Ops::store_b(ring[slot], b_stage(g + 1), wmask);
-                    ops.issue_a(a_stage(g + 2), t + 2);
                     ops.load_b(ring[slot], t + 3);
                 }
 #pragma unroll
@@ -283,9 +344,10 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
                         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
                 }
             }
-            // Activation K tile t+1 landed (issued one K tile ago, or with
-            // the tile's first loads): after it come weight K tile t+2,
-            // activation K tile t+2 and weight K tile t+3, 12 requests.
+            // Activation K tile t+1 landed (issued at the start of K tile
+            // t-1, or with the tile's first loads): after it come weight K
+            // tile t+2, activation K tile t+2 and weight K tile t+3, 12
+            // requests.
             // Right after a tile boundary the previous tile's output stores
             // sit between them, well over the 63 requests a wave can have in
             // flight, so the hardware's own limit has already retired it.
@@ -312,7 +374,33 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
         }
         if (t + 1 < nk)
             ktile(std::integral_constant<int, 1>{}, t);
-        // Last K tile.
+        // Before the last K tile's matrix work (its operands are already in
+        // LDS): the epilogue's per-column factors are requested, and the
+        // next tile's coordinates found and its first two K tiles requested,
+        // so that all of these land under the last K tile's MFMAs.  The next
+        // tile's stages are free: activation stages (g0+nk) % 3 and
+        // (g0+nk+1) % 3 and weight stage (g0+nk) % 2 held K tiles nk-3 and
+        // nk-2 (or the previous tile's), whose reads every wave finished
+        // before the last barrier; the register slots hold only the requests
+        // past K.
+        ColLoads<C> cl;
+        cols_request<C>(d, n0, bits, cl);
+        const LayerDesc &dc = d;
+        const int mc = m0, nc = n0;
+        const int g1 = g0 + nk;
+        u += wgs;
+        const bool more = u < uend;
+        if (more) {
+            seg = find_segment(descs, L, u);
+            unit_coords<C>(descs[seg], u, m0, n0);
+            bits = bits_of(seg);
+            int t2 = tid;
+            asm volatile("" : "+v"(t2));
+            ops.init(descs[seg], m0, n0, t2);
+        }
+        // With no next tile the same requests go out past K (zeros into free
+        // stages and slots), so that the epilogue's waits see one count.
+        issue_first(g1, more ? 0 : nk);
         {
             const int g = g0 + nk - 1;
 #pragma unroll
@@ -325,34 +413,13 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
                 __builtin_amdgcn_sched_group_barrier(0x008, C::FM * C::FN, 0);
             }
         }
-
-        const char *lds = reinterpret_cast<const char *>(sm);
+        __builtin_amdgcn_sched_barrier(0);
         EpiCols<C> ec;
-        epilogue_cols<C>(d, m0, n0, bits, ec);
-        u += wgs;
-        if (u >= uend) {
-            epilogue_write<C, true, false>(d, acc, ec, lds);
+        cols_finish<C>(dc, mc, nc, cl, ec);
+        epilogue_write<C, true, false>(dc, acc, ec, reinterpret_cast<const char *>(sm));
+        __builtin_amdgcn_sched_barrier(0);
+        if (!more)
             break;
-        }
-        // The next tile's first two K tiles are requested before any store
-        // of this one.  Their stages are free: activation stages (g1) % 3 and
-        // (g1 + 1) % 3 and weight stage g1 % 2 held K tiles read before this
-        // tile's second-to-last barrier (or before its prologue barrier),
-        // and both register slots are empty.
-        const LayerDesc &dp = d;
-        const int g1 = g0 + nk;
-        seg = find_segment(descs, L, u);
-        unit_coords<C>(descs[seg], u, m0, n0);
-        bits = bits_of(seg);
-        {
-            int t2 = tid;
-            asm volatile("" : "+v"(t2));
-            ops.init(descs[seg], m0, n0, t2);
-        }
-        issue_first(g1);
-        __builtin_amdgcn_sched_barrier(0);
-        epilogue_write<C, true, false>(dp, acc, ec, lds);
-        __builtin_amdgcn_sched_barrier(0);
         g0 = g1;
         first = false;
     }
