@@ -442,6 +442,34 @@ typedef struct tasq_layer {
 int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
                       int t_begin, int t_end, const tasq_opts *opts, void *stream);
 
+/* Limits of tasq_run_schedule_noalloc: layers per call, and the bytes of
+ * the scratch array it keeps in each GPU's memory (the device layer list,
+ * room for 8 segments of 176 bytes per layer, and the bit table). */
+#define TASQ_STATIC_MAX_LAYERS 256
+#define TASQ_STATIC_SCRATCH_BYTES 376832
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * schedule as tasq_run_schedule, with the same arguments, validation and
+ * results, but the device-side layer list and bit table live in a scratch
+ * array of TASQ_STATIC_SCRATCH_BYTES that the library holds in each GPU's
+ * memory for the life of the process, instead of in opts->workspace (which
+ * is not used).  Nothing is allocated: no hipMalloc, hipFree or allocating
+ * library call; the first call on a device looks up that device's array
+ * address once.
+ *   L <= TASQ_STATIC_MAX_LAYERS, else TASQ_ERR_WORKSPACE (nothing enqueued).
+ *   A layer that a workspace schedule would cut with split-K (a long K on
+ *   few tiles) runs unsplit: same result, no partial sums to hold.
+ * Every call on one GPU shares that GPU's array, and a call overwrites it
+ * (stream-ordered) before its kernels read it: calls ordered on one stream
+ * are safe, calls that overlap on one GPU (other streams, other host
+ * threads) race on the array and must not be made.
+ */
+int tasq_run_schedule_noalloc(const tasq_layer *layers, int L, const uint8_t *b_table, int S,
+                              int T, int t_begin, int t_end, const tasq_opts *opts,
+                              void *stream);
+
 /* Workspace with which a single layer call (split_k = 0) cuts K into ranges:
  * splits * M * N * 4 bytes, or 0 when it would not split this shape (enough
  * output tiles, or K too short).  A smaller workspace runs unsplit. */

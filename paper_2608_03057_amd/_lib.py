@@ -26,6 +26,8 @@ TASQ_ERR_KIND = -9
 TASQ_ERR_ALIGN = -10
 TASQ_MAX_K = 131071
 TASQ_ACT_PARAMS_FLOATS = 1028
+TASQ_STATIC_MAX_LAYERS = 256
+TASQ_STATIC_SCRATCH_BYTES = 376832
 
 VARIANT_AUTO = 0
 VARIANT_MASKED_I8 = 1
@@ -41,7 +43,7 @@ EXPORTS = (
     "tasq_pack_weights", "tasq_packed_weight_bytes", "tasq_quantize_activations",
     "tasq_weight_colsums", "tasq_lowrank_down", "tasq_quantize_activations_lowrank",
     "tasq_quantize_weights", "tasq_row_sums", "tasq_schedule_cost",
-    "tasq_stage_of_step", "tasq_run_schedule",
+    "tasq_stage_of_step", "tasq_run_schedule", "tasq_run_schedule_noalloc",
     "tasq_workspace_bytes", "tasq_schedule_workspace_bytes", "tasq_status_string",
 )
 
@@ -132,6 +134,8 @@ def lib() -> ctypes.CDLL:
         L.tasq_run_schedule.argtypes = [ctypes.POINTER(Layer), i32, vp, i32, i32, i32, i32,
                                         ctypes.POINTER(Opts), vp]
         L.tasq_run_schedule.restype = i32
+        L.tasq_run_schedule_noalloc.argtypes = L.tasq_run_schedule.argtypes
+        L.tasq_run_schedule_noalloc.restype = i32
         L.tasq_workspace_bytes.argtypes = [i32, i32, i32]
         L.tasq_workspace_bytes.restype = ctypes.c_size_t
         L.tasq_schedule_workspace_bytes.argtypes = [ctypes.POINTER(Layer), i32]

@@ -372,3 +372,19 @@ def run_schedule(layers: Sequence[Layer], table: torch.Tensor, S: int, T: int, t
     rc = _lib.lib().tasq_run_schedule(arr, L, table.data_ptr(), S, T, t_begin, t_end,
                                       ctypes.byref(o), _stream())
     check(rc, "tasq_run_schedule")
+
+
+def run_schedule_noalloc(layers: Sequence[Layer], table: torch.Tensor, S: int, T: int,
+                         t_begin: int, t_end: int, *, variant: int = _lib.VARIANT_AUTO,
+                         tune: Optional[dict] = None) -> None:
+    """run_schedule with the layer list in the library's per-GPU scratch array
+    (tasq_run_schedule_noalloc): no workspace, nothing allocated."""
+    table = table.to(torch.uint8).contiguous().cpu()
+    L = len(layers)
+    if tuple(table.shape) != (L, S):
+        raise ValueError(f"table must be [{L}, {S}]")
+    arr = _layer_array(layers)
+    o = _opts(variant, None, None, 0, tune=tune)
+    rc = _lib.lib().tasq_run_schedule_noalloc(arr, L, table.data_ptr(), S, T, t_begin, t_end,
+                                              ctypes.byref(o), _stream())
+    check(rc, "tasq_run_schedule_noalloc")

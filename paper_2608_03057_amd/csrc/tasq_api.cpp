@@ -7,6 +7,7 @@
 
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -58,7 +59,7 @@ double xcd_imbalance(const std::vector<LayerDesc> &descs, long long G)
     return total > 0 ? mx / (total / kXcds) : 1.0;
 }
 
-size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+constexpr size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 int variant_of_opts(const tasq_opts *o) { return o ? o->variant : TASQ_VARIANT_AUTO; }
 
@@ -234,7 +235,7 @@ size_t max_split_bytes(const tasq_layer *layers, int L)
     return (size_t)mx;
 }
 
-size_t schedule_partials_offset(int L)
+constexpr size_t schedule_partials_offset(int L)
 {
     return round_up((size_t)L * kXcds * sizeof(LayerDesc), kWsAlign) +
            round_up((size_t)L * 64, kWsAlign);
@@ -571,6 +572,47 @@ int validate_layer(const tasq_layer &L, const tasq_opts *o)
 }
 
 
+// Device-side layer list and bit table of tasq_run_schedule_noalloc: one
+// copy per GPU the library runs on, held until the process ends.  Host code
+// never uses the name itself (a host-side stand-in, not a device address):
+// static_scratch() looks the address up once per device with that device
+// current, and only that pointer reaches kernels and copies.
+constexpr size_t kStaticScratchBytes = schedule_partials_offset(TASQ_STATIC_MAX_LAYERS);
+static_assert(kStaticScratchBytes == TASQ_STATIC_SCRATCH_BYTES,
+              "TASQ_STATIC_SCRATCH_BYTES must match the layer-list layout");
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+// Device address of this stream's GPU's scratch array.
+int static_scratch(hipStream_t stream, void **out)
+{
+    int cur = 0, dev = 0;
+    if (hipGetDevice(&cur) != hipSuccess)
+        return TASQ_ERR_HIP;
+    dev = cur;
+    if (stream && hipStreamGetDevice(stream, &dev) != hipSuccess)
+        return TASQ_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices)
+        return TASQ_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        if (dev != cur && hipSetDevice(dev) != hipSuccess)
+            return TASQ_ERR_HIP;
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (dev != cur && hipSetDevice(cur) != hipSuccess)
+            return TASQ_ERR_HIP;
+        if (e != hipSuccess || !p)
+            return TASQ_ERR_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return TASQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -585,7 +627,8 @@ const char *tasq_status_string(int status)
     case TASQ_ERR_OVERFLOW: return "K too large for exact int32 accumulation";
     case TASQ_ERR_RANGE: return "bad stage/step range or count";
     case TASQ_ERR_LAYOUT: return "requested variant needs a weight layout that is absent";
-    case TASQ_ERR_WORKSPACE: return "workspace missing or too small";
+    case TASQ_ERR_WORKSPACE:
+        return "workspace missing or too small (noalloc schedule: more layers than its scratch holds)";
     case TASQ_ERR_HIP: return "HIP runtime or launch failure";
     case TASQ_ERR_KIND: return "unknown layer kind or variant";
     case TASQ_ERR_ALIGN: return "workspace not 256-byte aligned or packed weight not 16-byte aligned";
@@ -855,8 +898,12 @@ static int record_step_event(const tasq_opts *o, int i, hipStream_t st)
                : TASQ_ERR_HIP;
 }
 
+// static_ws: the per-device scratch array (tasq_run_schedule_noalloc) in
+// place of the caller's workspace; it holds the layer list and the table
+// only, so layers that a workspace schedule would split-K run unsplit.
 static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_table, int S,
-                             int T, int t_begin, int t_end, const tasq_opts *opts, void *stream)
+                             int T, int t_begin, int t_end, const tasq_opts *opts, void *stream,
+                             bool use_static)
 {
     if (L < 0)
         return TASQ_ERR_RANGE;
@@ -879,9 +926,16 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
                 return TASQ_ERR_BITS;
         }
     }
+    if (use_static && L > TASQ_STATIC_MAX_LAYERS)
+        return TASQ_ERR_WORKSPACE;
     if (L == 0 || t_begin == t_end)
         return TASQ_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
+    void *static_ws = nullptr;
+    if (use_static) {
+        if (int rc = static_scratch(st, &static_ws))
+            return rc;
+    }
 
     std::vector<LayerDesc> descs(L);
     for (int l = 0; l < L; ++l)
@@ -896,8 +950,12 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
     //  - packed-weight GEMM, when every layer has a packed weight;
     //  - staged GEMM, when every layer has its aligned row-major weight.
     // Otherwise each layer is launched on its own.
-    const size_t need = tasq_schedule_workspace_bytes(layers, L);
-    const bool have_ws = opts && opts->workspace && opts->workspace_bytes >= need;
+    const size_t need = use_static ? schedule_partials_offset(L)
+                                   : tasq_schedule_workspace_bytes(layers, L);
+    char *const ws = use_static ? static_cast<char *>(static_ws)
+                                : static_cast<char *>(opts ? opts->workspace : nullptr);
+    const size_t ws_bytes = use_static ? kStaticScratchBytes : (opts ? opts->workspace_bytes : 0);
+    const bool have_ws = ws && ws_bytes >= need;
     // The weight copy each layer reads (AUTO: by shape, see weight_source),
     // with "some b below 8" taken over the stages the steps touch.
     const int s_first = tasq_stage_of_step(t_begin, S, T);
@@ -1029,7 +1087,6 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
             segs = descs;
         }
         const int nseg = (int)segs.size();
-        char *ws = static_cast<char *>(opts->workspace);
         LayerDesc *d_descs = reinterpret_cast<LayerDesc *>(ws);
         uint8_t *d_table = reinterpret_cast<uint8_t *>(
             ws + round_up((size_t)L * kXcds * sizeof(LayerDesc), kWsAlign));
@@ -1046,10 +1103,11 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
         // Schedules ignore split_k: a layer launched on its own takes the
         // automatic split over the partials room, which
         // tasq_schedule_workspace_bytes reserved for it.
-        tasq_opts sopts = *opts;
+        tasq_opts sopts = opts ? *opts : tasq_opts{};
         sopts.split_k = 0;
-        sopts.workspace = ws + schedule_partials_offset(L);
-        sopts.workspace_bytes = opts->workspace_bytes - schedule_partials_offset(L);
+        sopts.step_events = nullptr;
+        sopts.workspace = use_static ? nullptr : ws + schedule_partials_offset(L);
+        sopts.workspace_bytes = use_static ? 0 : ws_bytes - schedule_partials_offset(L);
         for (int t = t_begin; t < t_end; ++t) {
             const int s = tasq_stage_of_step(t, S, T);
             if (int rc = record_step_event(opts, 2 * (t - t_begin), st))
@@ -1101,7 +1159,17 @@ int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, i
                       int t_begin, int t_end, const tasq_opts *opts, void *stream)
 {
     try {
-        return run_schedule_impl(layers, L, b_table, S, T, t_begin, t_end, opts, stream);
+        return run_schedule_impl(layers, L, b_table, S, T, t_begin, t_end, opts, stream, false);
+    } catch (const std::bad_alloc &) {
+        return TASQ_ERR_HIP;
+    }
+}
+
+int tasq_run_schedule_noalloc(const tasq_layer *layers, int L, const uint8_t *b_table, int S,
+                              int T, int t_begin, int t_end, const tasq_opts *opts, void *stream)
+{
+    try {
+        return run_schedule_impl(layers, L, b_table, S, T, t_begin, t_end, opts, stream, true);
     } catch (const std::bad_alloc &) {
         return TASQ_ERR_HIP;
     }

@@ -415,3 +415,18 @@ def test_auto_reads_planes_when_no_other_copy():
     assert sched([conv], [8, 7, 6, 5], 4, 20, 0, 0) == _lib.TASQ_ERR_NULL
     assert lin(W=None, M=0, opts=opts(variant=_lib.VARIANT_MASKED_I8, W_planes=FAKE)) \
         == _lib.TASQ_ERR_NULL
+
+
+def test_noalloc_schedule_rejects_before_touching_a_device():
+    """tasq_run_schedule_noalloc validates like tasq_run_schedule and rejects
+    more layers than its scratch array holds, before any HIP call."""
+    def na(layers, table, S, T, t0, t1):
+        arr = (Layer * len(layers))(*layers)
+        tab = (ctypes.c_uint8 * max(1, len(table)))(*table)
+        return L.tasq_run_schedule_noalloc(arr, len(layers), tab, S, T, t0, t1, None, None)
+    L_max = _lib.TASQ_STATIC_MAX_LAYERS
+    assert na([layer()] * (L_max + 1), [8] * (L_max + 1), 1, 1, 0, 1) == _lib.TASQ_ERR_WORKSPACE
+    assert na([layer()] * 2, [8, 7, 6, 5, 4, 3, 2, 0], 4, 20, 0, 1) == _lib.TASQ_ERR_BITS
+    assert na([layer()] * 2, [8] * 8, 4, 20, 3, 2) == _lib.TASQ_ERR_RANGE
+    assert na([layer()] * 2, [8] * 8, 4, 20, 5, 5) == _lib.TASQ_OK
+    assert _lib.TASQ_STATIC_SCRATCH_BYTES == 376832
