@@ -42,7 +42,7 @@ def log(msg):
 # Sources the grouped kernel of each weight layout is built from: recorded
 # counter readings stay valid while none of these files changes.
 KERNEL_SOURCES = {
-    "k_masked_gemm_persistent": ["gemm_core.h", "tasq_internal.h",
+    "k_masked_gemm_persistent": ["gemm_core.h", "gemm_pers.h", "tasq_internal.h",
                                  "tile_256x256_k128_w8_pf1.hip", "tasq_api.cpp"],
     "k_masked_gemm_grouped": ["gemm_core.h", "tasq_internal.h", "tile_256x256_k128_w8_pf1.hip",
                               "tasq_api.cpp"],
