@@ -439,14 +439,16 @@ def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
     """The asymmetric-activation form of the same schedule: each layer's input
     arrives as fp32 (seeded normal draws with a few large channels), is
     quantized per tensor on the GPU, and the grouped launch dequantises with
-    the zero-point term.  Per denoising step: the 112 quantizer calls, then
-    one grouped launch.  Timed twice: without and with a rank-`rank` 16-bit
-    low-rank branch on every layer (SVDQuant-initialised models), where the
-    quantizer also writes the down projection and the grouped launch adds the
-    up projection.  Returns milliseconds per denoising step for the
-    quantizer, the grouped launch and both, and the quantizer's HBM roofline
-    (algorithmic bytes: 4 read + 1 written per element, plus 4 per element of
-    the projection with the branch)."""
+    the zero-point term.  Per denoising step: one batched quantizer call over
+    the 112 inputs, then one grouped launch.  Timed three ways: plain (with
+    the same quantization as one call per tensor timed beside it), with a
+    rank-`rank` 16-bit low-rank branch on every layer (SVDQuant-initialised
+    models), where the quantizer also writes the down projection (one call
+    per tensor) and the grouped launch adds the up projection, and with
+    weight zero points (row sums of the codes).  Returns milliseconds per
+    denoising step for the quantizer, the grouped launch and both, and the
+    quantizer's HBM roofline (algorithmic bytes: 4 read + 1 written per
+    element, plus 4 per element of the projection with the branch)."""
     xs, codes, Ts, plain, lowrank, wzero, hold = [], [], [], [], [], [], []
     rsums = []
     params = torch.empty((len(wl.layers), T.TASQ_ACT_PARAMS_FLOATS), dtype=torch.float32,
@@ -480,13 +482,21 @@ def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
                                   wzero=(zw, rs)))
     torch.cuda.synchronize()
 
+    xlist = [x for x, _ in xs]
+    plist = [params[l] for l in range(len(xs))]
+
     def quantize_all(kind):
-        for l, (x, down) in enumerate(xs):
-            if kind == "lowrank":
+        if kind == "lowrank":
+            for l, (x, down) in enumerate(xs):
                 T.quantize_activations_lowrank(x, down, out=codes[l], params=params[l], T=Ts[l])
-            else:
+            return
+        if kind == "single":
+            for l, x in enumerate(xlist):
                 T.quantize_activations(x, out=codes[l], params=params[l])
-            if kind == "wzero":
+            return
+        T.quantize_activations_batch(xlist, codes, plist)
+        if kind == "wzero":
+            for l in range(len(xs)):
                 T.row_sums(codes[l], out=rsums[l])
 
     ev = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
@@ -519,15 +529,28 @@ def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
         if kind == "wzero":            # the row sums read the codes once more
             alg += elems + 4.0 * sum(float(s.M) for s in wl.layers)
         ach = alg / (qm * 1e-3) / 1e9
+        if kind == "plain":
+            # the same quantization as one pair of launches per tensor
+            quantize_all("single")
+            torch.cuda.synchronize()
+            s0, s1 = ev(), ev()
+            s0.record()
+            for _ in range(reps * 4):
+                quantize_all("single")
+            s1.record()
+            torch.cuda.synchronize()
+            single_ms = s0.elapsed_time(s1) / (reps * 4)
         out[name] = {
             "ms_per_denoising_step": round(a0.elapsed_time(a1) / reps / wl.T, 4),
             "quantize_ms": round(qm, 4), "grouped_launch_ms": round(gm, 4),
             "quantizer_roofline": {
                 "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(ach / PEAK_HBM_GBS, 4), "algorithmic_bytes": alg,
-                "kernels": {"plain": "k_act_range, k_act_quantize per layer",
+                "kernels": {"plain": "k_act_batch (all layers in ceil(L / 8) + 1 launches)",
                             "lowrank": "k_lowrank_down<true>, k_act_quantize per layer",
-                            "wzero": "k_act_range, k_act_quantize, k_row_sums per layer"}[kind]}}
+                            "wzero": "k_act_batch, then k_row_sums per layer"}[kind]}}
+        if kind == "plain":
+            out[name]["quantize_ms_per_tensor_calls"] = round(single_ms, 4)
     return out
 
 

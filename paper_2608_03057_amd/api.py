@@ -139,6 +139,35 @@ def quantize_activations(x: torch.Tensor, out: Optional[torch.Tensor] = None,
     return out, params
 
 
+def quantize_activations_batch(xs, outs=None, params=None):
+    """quantize_activations over a list of fp32 tensors in few launches
+    (App. A.1.2): returns the lists of codes and params, each entry equal to
+    what quantize_activations gives for that tensor.  Every tensor needs its
+    own params buffer."""
+    xs = list(xs)
+    n = len(xs)
+    outs = list(outs) if outs is not None else [None] * n
+    params = list(params) if params is not None else [None] * n
+    if len(outs) != n or len(params) != n:
+        raise ValueError("xs, outs and params differ in length")
+    jobs = (_lib.ActJob * max(n, 1))()
+    for j, x in enumerate(xs):
+        M = x.shape[0] if x.dim() else 1
+        K = x.numel() // M if M else 0
+        _need(x, torch.float32, tuple(x.shape), "x")
+        if outs[j] is None:
+            outs[j] = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+        if params[j] is None:
+            params[j] = torch.empty(_lib.TASQ_ACT_PARAMS_FLOATS, dtype=torch.float32,
+                                    device=x.device)
+        _need(outs[j], torch.int8, tuple(x.shape), "out")
+        _need(params[j], torch.float32, (_lib.TASQ_ACT_PARAMS_FLOATS,), "params")
+        jobs[j] = _lib.ActJob(_ptr(x), M, K, _ptr(outs[j]), _ptr(params[j]))
+    check(_lib.lib().tasq_quantize_activations_batch(jobs, n, _stream()),
+          "tasq_quantize_activations_batch")
+    return outs, params
+
+
 def quantize_weights(W: torch.Tensor):
     """(codes int8 [N, ...], alpha, z, sw fp32 [N]) of fp32 weights W
     [N, ...]: the per-channel 8-bit quantizer of App. A.1.1; z is the

@@ -15,7 +15,10 @@
 //
 // Two launches: per-workgroup ranges into the params buffer's partial slots,
 // then a pass in which every workgroup folds those partials and writes its
-// share of the codes.  No atomics and no buffer to clear beforehand.
+// share of the codes.  No atomics and no buffer to clear beforehand.  The
+// batched form runs the passes of many tensors in few launches.
+#include <vector>
+
 #include "tasq_internal.h"
 
 namespace tasq {
@@ -36,19 +39,19 @@ __device__ __forceinline__ float order_value(uint32_t k)
     return __uint_as_float(u);
 }
 
-// Per-workgroup range of x as order keys: workgroup g writes its minimum
-// key to part[2g] and its maximum key to part[2g + 1] (no atomics: the
-// quantizer folds the partial ranges).  The first 4*n4 elements are read as
-// float4 (n4 = 0 when x is not 16-byte aligned), four loads in flight per
+// Per-workgroup range of x as order keys: workgroup g of G writes its
+// minimum key to part[2g] and its maximum key to part[2g + 1] (no atomics:
+// the quantizer folds the partial ranges).  The first 4*n4 elements are read
+// as float4 (n4 = 0 when x is not 16-byte aligned), four loads in flight per
 // thread.
-__global__ void __launch_bounds__(256) k_act_range(const float *__restrict__ x, long long n,
-                                                   long long n4, uint32_t *__restrict__ part)
+__device__ __forceinline__ void act_range(const float *__restrict__ x, long long n, long long n4,
+                                          uint32_t *__restrict__ part, int g, int G)
 {
     __shared__ uint32_t smin[4], smax[4];
     float mn = __builtin_huge_valf(), mx = -__builtin_huge_valf();
-    const long long stride = (long long)gridDim.x * blockDim.x;
+    const long long stride = (long long)G * blockDim.x;
     const float4 *x4 = reinterpret_cast<const float4 *>(x);
-    long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    long long i = (long long)g * blockDim.x + threadIdx.x;
     for (; i + 3 * stride < n4; i += 4 * stride) {
         float4 v[4];
 #pragma unroll
@@ -65,8 +68,7 @@ __global__ void __launch_bounds__(256) k_act_range(const float *__restrict__ x, 
         mn = fminf(fminf(mn, v.x), fminf(v.y, fminf(v.z, v.w)));
         mx = fmaxf(fmaxf(mx, v.x), fmaxf(v.y, fmaxf(v.z, v.w)));
     }
-    for (long long t = (n4 << 2) + (long long)blockIdx.x * blockDim.x + threadIdx.x; t < n;
-         t += stride) {
+    for (long long t = (n4 << 2) + (long long)g * blockDim.x + threadIdx.x; t < n; t += stride) {
         mn = fminf(mn, x[t]);
         mx = fmaxf(mx, x[t]);
     }
@@ -88,9 +90,15 @@ __global__ void __launch_bounds__(256) k_act_range(const float *__restrict__ x, 
             kmn = min(kmn, smin[w]);
             kmx = max(kmx, smax[w]);
         }
-        part[2 * blockIdx.x] = kmn;
-        part[2 * blockIdx.x + 1] = kmx;
+        part[2 * g] = kmn;
+        part[2 * g + 1] = kmx;
     }
+}
+
+__global__ void __launch_bounds__(256) k_act_range(const float *__restrict__ x, long long n,
+                                                   long long n4, uint32_t *__restrict__ part)
+{
+    act_range(x, n, n4, part, blockIdx.x, gridDim.x);
 }
 
 __device__ __forceinline__ void scale_of(uint32_t kmn, uint32_t kmx, float &alpha, float &z)
@@ -112,13 +120,13 @@ __device__ __forceinline__ int8_t code_of(float x, float alpha, float z)
     return (int8_t)((int)r - 128);
 }
 
-// Every workgroup folds the G partial ranges (a few KB, cache resident) into
-// alpha and z, then writes the codes of its share; workgroup 0 also
-// publishes alpha and z.  n4 as in k_act_range, with q 4-byte aligned
+// Every workgroup (g of Q) folds the G partial ranges (a few KB, cache
+// resident) into alpha and z, then writes the codes of its share; workgroup
+// 0 also publishes alpha and z.  n4 as in act_range, with q 4-byte aligned
 // whenever n4 > 0.
-__global__ void __launch_bounds__(256) k_act_quantize(const float *__restrict__ x, long long n,
-                                                      long long n4, int8_t *__restrict__ q,
-                                                      float *params, int G)
+__device__ __forceinline__ void act_quantize(const float *__restrict__ x, long long n,
+                                             long long n4, int8_t *__restrict__ q, float *params,
+                                             int G, int g, int Q)
 {
     __shared__ uint32_t smin[4], smax[4];
     const uint32_t *part = reinterpret_cast<const uint32_t *>(params + kActHeader);
@@ -141,21 +149,72 @@ __global__ void __launch_bounds__(256) k_act_quantize(const float *__restrict__ 
     kmx = max(max(smax[0], smax[1]), max(smax[2], smax[3]));
     float alpha, z;
     scale_of(kmn, kmx, alpha, z);
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
+    if (g == 0 && threadIdx.x == 0) {
         params[0] = alpha;
         params[1] = z;
     }
-    const long long stride = (long long)gridDim.x * blockDim.x;
+    const long long stride = (long long)Q * blockDim.x;
     const float4 *x4 = reinterpret_cast<const float4 *>(x);
     char4 *q4 = reinterpret_cast<char4 *>(q);
-    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    long long i = (long long)g * blockDim.x + threadIdx.x;
+    for (; i + 3 * stride < n4; i += 4 * stride) {
+        float4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            v[u] = x4[i + u * stride];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            q4[i + u * stride] = make_char4(code_of(v[u].x, alpha, z), code_of(v[u].y, alpha, z),
+                                            code_of(v[u].z, alpha, z), code_of(v[u].w, alpha, z));
+    }
+    for (; i < n4; i += stride) {
         const float4 v = x4[i];
         q4[i] = make_char4(code_of(v.x, alpha, z), code_of(v.y, alpha, z), code_of(v.z, alpha, z),
                            code_of(v.w, alpha, z));
     }
-    for (long long i = (n4 << 2) + (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += stride)
+    for (long long i = (n4 << 2) + (long long)g * blockDim.x + threadIdx.x; i < n; i += stride)
         q[i] = code_of(x[i], alpha, z);
+}
+
+__global__ void __launch_bounds__(256) k_act_quantize(const float *__restrict__ x, long long n,
+                                                      long long n4, int8_t *__restrict__ q,
+                                                      float *params, int G)
+{
+    act_quantize(x, n, n4, q, params, G, blockIdx.x, gridDim.x);
+}
+
+// Many tensors in one launch: each task is one tensor's range pass or its
+// code pass, run by a contiguous run of the launch's workgroups exactly as
+// the single-tensor kernels run it, so the codes and scales are those of the
+// single-tensor calls.  The task list travels in the kernel arguments.
+struct ActTask {
+    const float *x;
+    int8_t *q;
+    float *params;
+    long long n, n4;
+    int first;      // first workgroup of the task in the launch
+    int wgs;        // its workgroups
+    int parts;      // workgroups (partial ranges) of the tensor's range pass
+    int quant;      // 0: range pass, 1: code pass
+};
+constexpr int kActBatchTasks = 16;
+struct ActLaunch {
+    ActTask t[kActBatchTasks];
+    int ntasks;
+};
+
+__global__ void __launch_bounds__(256) k_act_batch(const ActLaunch L)
+{
+    int i = 0;
+    while (i + 1 < L.ntasks && (int)blockIdx.x >= L.t[i + 1].first)
+        ++i;
+    const ActTask &t = L.t[i];
+    const int g = (int)blockIdx.x - t.first;
+    if (t.quant)
+        act_quantize(t.x, t.n, t.n4, t.q, t.params, t.parts, g, t.wgs);
+    else
+        act_range(t.x, t.n, t.n4, reinterpret_cast<uint32_t *>(t.params + kActHeader), g,
+                  t.parts);
 }
 
 // ------------------------------------------------- low-rank down projection
@@ -366,6 +425,71 @@ hipError_t launch_quantize_activations(const float *x, long long n, int8_t *q, f
     hipLaunchKernelGGL(k_act_quantize, dim3(grid_for(items, 256, 1024)), dim3(256), 0, stream, x,
                        n, n4, q, params, G);
     return hipGetLastError();
+}
+
+// Groups of consecutive tensors (at most half a launch's tasks, and about
+// 128 MB of x unless a single tensor is larger) run their code pass in the
+// launch after their range pass, beside the next group's range pass:
+// ceil(n / group) + 1 launches instead of 2 n, and each x is read the second
+// time while it is still in the last-level cache.
+hipError_t launch_quantize_activations_batch(const ActJob *jobs, int n, hipStream_t stream)
+{
+    constexpr long long kGroupBytes = 128LL << 20;
+    constexpr int kGroupTasks = kActBatchTasks / 2;
+    struct Prep {
+        ActTask range, quant;
+    };
+    std::vector<Prep> prep;
+    prep.reserve((size_t)n);
+    for (int j = 0; j < n; ++j) {
+        const ActJob &a = jobs[j];
+        const long long cnt = (long long)a.M * a.K;
+        if (cnt == 0)
+            continue;
+        const bool vec = (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 &&
+                         (reinterpret_cast<uintptr_t>(a.q) & 3) == 0;
+        const long long n4 = vec ? cnt >> 2 : 0;
+        const long long items = vec ? (cnt + 3) / 4 : cnt;
+        const int G = grid_for(items, 256 * 4, kActPartials);
+        ActTask r = {a.x, a.q, a.params, cnt, n4, 0, G, G, 0};
+        ActTask q = r;
+        q.wgs = grid_for(items, 256, 1024);
+        q.quant = 1;
+        prep.push_back({r, q});
+    }
+    // group boundaries
+    std::vector<int> bounds{0};
+    long long bytes = 0;
+    for (int j = 0; j < (int)prep.size(); ++j) {
+        const long long b = prep[j].range.n * 4;
+        const int in_group = j - bounds.back();
+        if (in_group > 0 && (in_group == kGroupTasks || bytes + b > kGroupBytes)) {
+            bounds.push_back(j);
+            bytes = 0;
+        }
+        bytes += b;
+    }
+    bounds.push_back((int)prep.size());
+    const int ng = (int)bounds.size() - 1;
+    for (int k = 0; k <= ng && !prep.empty(); ++k) {
+        ActLaunch L = {};
+        int wg = 0;
+        auto add = [&](ActTask t) {
+            t.first = wg;
+            wg += t.wgs;
+            L.t[L.ntasks++] = t;
+        };
+        if (k > 0)
+            for (int j = bounds[k - 1]; j < bounds[k]; ++j)
+                add(prep[j].quant);
+        if (k < ng)
+            for (int j = bounds[k]; j < bounds[k + 1]; ++j)
+                add(prep[j].range);
+        hipLaunchKernelGGL(k_act_batch, dim3(wg), dim3(256), 0, stream, L);
+        if (hipError_t e = hipGetLastError(); e != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_lowrank_down(const float *x, int M, int K, const uint16_t *D, int r, float *T,

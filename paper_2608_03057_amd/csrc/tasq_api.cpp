@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -625,7 +626,7 @@ const char *tasq_status_string(int status)
     case TASQ_ERR_DIM: return "bad dimension";
     case TASQ_ERR_BITS: return "effective bits outside [1, 8]";
     case TASQ_ERR_OVERFLOW: return "K too large for exact int32 accumulation";
-    case TASQ_ERR_RANGE: return "bad stage/step range or count";
+    case TASQ_ERR_RANGE: return "bad stage/step range or count, or a buffer shared by two jobs";
     case TASQ_ERR_LAYOUT: return "requested variant needs a weight layout that is absent";
     case TASQ_ERR_WORKSPACE:
         return "workspace missing or too small (noalloc schedule: more layers than its scratch holds)";
@@ -771,6 +772,39 @@ int tasq_quantize_activations(const float *x, int M, int K, int8_t *X_out, float
         return TASQ_ERR_ALIGN;
     hipError_t e = tasq::launch_quantize_activations(x, n, X_out, act_params,
                                                      static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}
+
+int tasq_quantize_activations_batch(const tasq_act_job *jobs, int n, void *stream)
+{
+    if (n < 0)
+        return TASQ_ERR_RANGE;
+    if (n == 0)
+        return TASQ_OK;
+    if (!jobs)
+        return TASQ_ERR_NULL;
+    std::vector<tasq::ActJob> js;
+    std::vector<const float *> bufs;
+    js.reserve((size_t)n);
+    bufs.reserve((size_t)n);
+    for (int j = 0; j < n; ++j) {
+        const tasq_act_job &a = jobs[j];
+        if (a.M < 0 || a.K < 0)
+            return TASQ_ERR_DIM;
+        if ((long long)a.M * a.K == 0)
+            continue;
+        if (!a.x || !a.X_out || !a.act_params)
+            return TASQ_ERR_NULL;
+        if ((reinterpret_cast<uintptr_t>(a.x) & 3) || (reinterpret_cast<uintptr_t>(a.act_params) & 3))
+            return TASQ_ERR_ALIGN;
+        js.push_back({a.x, a.M, a.K, a.X_out, a.act_params});
+        bufs.push_back(a.act_params);
+    }
+    std::sort(bufs.begin(), bufs.end());
+    if (std::adjacent_find(bufs.begin(), bufs.end()) != bufs.end())
+        return TASQ_ERR_RANGE;
+    hipError_t e = tasq::launch_quantize_activations_batch(js.data(), (int)js.size(),
+                                                           static_cast<hipStream_t>(stream));
     return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
 }
 

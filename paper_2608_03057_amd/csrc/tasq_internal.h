@@ -139,6 +139,14 @@ hipError_t launch_quantize_activations_lowrank(const float *x, int M, int K, int
                                                hipStream_t stream);
 hipError_t launch_quantize_activations(const float *x, long long n, int8_t *q, float *params,
                                        hipStream_t stream);
+// One tensor of a batched activation quantization.
+struct ActJob {
+    const float *x;
+    int M, K;
+    int8_t *q;
+    float *params;
+};
+hipError_t launch_quantize_activations_batch(const ActJob *jobs, int n, hipStream_t stream);
 hipError_t launch_weight_colsums(const int8_t *W, int N, int K, int32_t *colsums,
                                  hipStream_t stream);
 

@@ -171,6 +171,34 @@ def test_quantize_activations_rejects():
     assert q(None, 0, 4, None, None, None) == _lib.TASQ_OK          # empty: nothing enqueued
 
 
+def test_quantize_activations_batch_rejects():
+    """Every job is validated before anything is enqueued; a bad job anywhere
+    in the list fails the whole call."""
+    f = L.tasq_quantize_activations_batch
+
+    def jobs(*js):
+        arr = (_lib.ActJob * len(js))()
+        for i, j in enumerate(js):
+            arr[i] = _lib.ActJob(*j)
+        return arr
+    good = (FAKE, 4, 4, FAKE, FAKE)
+    other = (FAKE, 4, 4, FAKE, FAKE + 4096)
+    assert f(None, 0, None) == _lib.TASQ_OK                           # nothing to do
+    assert f(None, 2, None) == _lib.TASQ_ERR_NULL
+    assert f(jobs(good), -1, None) == _lib.TASQ_ERR_RANGE
+    assert f(jobs(good, (None, 4, 4, FAKE, FAKE + 8192)), 2, None) == _lib.TASQ_ERR_NULL
+    assert f(jobs(good, (FAKE, 4, 4, None, FAKE + 8192)), 2, None) == _lib.TASQ_ERR_NULL
+    assert f(jobs(good, (FAKE, 4, 4, FAKE, None)), 2, None) == _lib.TASQ_ERR_NULL
+    assert f(jobs(good, (FAKE, -1, 4, FAKE, FAKE + 8192)), 2, None) == _lib.TASQ_ERR_DIM
+    assert f(jobs(good, (FAKE, 4, -3, FAKE, FAKE + 8192)), 2, None) == _lib.TASQ_ERR_DIM
+    assert f(jobs(good, (FAKE + 2, 4, 4, FAKE, FAKE + 8192)), 2, None) == _lib.TASQ_ERR_ALIGN
+    assert f(jobs(good, (FAKE, 4, 4, FAKE, FAKE + 8194)), 2, None) == _lib.TASQ_ERR_ALIGN
+    # two jobs sharing one act_params buffer
+    assert f(jobs(good, other, (FAKE, 8, 8, FAKE, FAKE)), 3, None) == _lib.TASQ_ERR_RANGE
+    # empty jobs are skipped, whatever their pointers
+    assert f(jobs((None, 0, 4, None, None), (None, 5, 0, None, None)), 2, None) == _lib.TASQ_OK
+
+
 def test_lowrank_down_rejects():
     f = L.tasq_lowrank_down
     assert f(FAKE, 4, 4, FAKE, 24, FAKE, None) == _lib.TASQ_ERR_DIM
@@ -355,7 +383,7 @@ def test_struct_layouts_match_header(tmp_path):
     """The ctypes structs mirror tasq_opts and tasq_layer field by field: a C
     program compiled against include/tasq.h prints each field's offset and
     the struct sizes."""
-    structs = {"tasq_opts": Opts, "tasq_layer": Layer}
+    structs = {"tasq_opts": Opts, "tasq_layer": Layer, "tasq_act_job": _lib.ActJob}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "tasq.h"', "int main(void){"]
     for cname, py in structs.items():
         lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')

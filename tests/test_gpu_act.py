@@ -94,6 +94,68 @@ def test_quantizer_unaligned_and_repeated():
         assert np.array_equal((q.cpu().numpy().astype(np.int16) + 128).astype(np.uint8), Q)
 
 
+def check_codes_vs_oracle(x_cpu, q, params, where):
+    alpha, z, Q = oracle.act_quant(x_cpu)
+    p = params.cpu().numpy()
+    assert np.float32(p[0]).tobytes() == np.float32(alpha).tobytes(), (where, p[0], alpha)
+    assert np.float32(p[1]).tobytes() == np.float32(z).tobytes(), (where, p[1], z)
+    got = (q.cpu().numpy().astype(np.int16) + 128).astype(np.uint8).reshape(-1)
+    bad = np.argwhere(got != Q.reshape(-1))
+    assert bad.size == 0, f"{where}: {len(bad)} code mismatches, first {bad[:3].tolist()}"
+
+
+def test_quantizer_batch_matches_single_and_oracle():
+    """The batched quantizer over 21 tensors (three groups of launches):
+    ragged shapes, an unaligned view (element-wise path), empty tensors in
+    the list and one tensor of more than a million elements; every tensor's
+    codes, alpha and z against the oracle and bit-identical to the
+    single-tensor call."""
+    shapes = [(1, 1), (7, 13), (33, 257), (5, 1001), (256, 1152), (1, 3), (64, 64), (0, 5),
+              (3, 0), (129, 577), (2, 2), (300, 70), (1, 4099), (17, 17), (900, 1152), (8, 8),
+              (1000, 1030), (4, 4), (11, 1), (1, 11), (45, 45)]
+    xs_cpu, xs = [], []
+    for i, (M, K) in enumerate(shapes):
+        x = inputs.activations_f32(500 + i, torch.arange(M), K, "skewed" if i % 2 else "outlier")
+        xs_cpu.append(x)
+        xs.append(x.to(DEV))
+    flat = inputs.activations_f32(77, torch.arange(9), 333, "skewed").reshape(-1).to(DEV)
+    xs_cpu.append(flat[1:].cpu())
+    xs.append(flat[1:])                  # 4 bytes into its storage: element-wise path
+    outs, params = T.quantize_activations_batch(xs)
+    torch.cuda.synchronize()
+    for i, (x, q, p) in enumerate(zip(xs, outs, params)):
+        if x.numel() == 0:
+            continue
+        q1, p1 = T.quantize_activations(x)
+        torch.cuda.synchronize()
+        assert torch.equal(q, q1), f"tensor {i}: codes differ from the single call"
+        assert torch.equal(p[:2], p1[:2]), f"tensor {i}: params differ from the single call"
+        check_codes_vs_oracle(xs_cpu[i], q, p, f"tensor {i} {tuple(x.shape)}")
+
+
+def test_quantizer_batch_full_size_step():
+    """The inputs of one block of the 28-block schedule (M = 8192; K = 1152,
+    1152, 1152, 4608) in one batched call, twice in a row into the same
+    buffers: every tensor against the oracle and bit-identical to the single
+    call."""
+    Ks = [1152, 1152, 1152, 4608]
+    xs = [inputs.activations_f32(900 + i, torch.arange(8192), K, "skewed") for i, K in enumerate(Ks)]
+    xd = [x.to(DEV) for x in xs]
+    outs = [torch.empty(x.shape, dtype=torch.int8, device=DEV) for x in xs]
+    params = [torch.empty(T.TASQ_ACT_PARAMS_FLOATS, dtype=torch.float32, device=DEV)
+              for _ in xs]
+    for rep in range(2):
+        T.quantize_activations_batch(xd, outs, params)
+        torch.cuda.synchronize()
+        for i, x in enumerate(xd):
+            q1, p1 = T.quantize_activations(x)
+            torch.cuda.synchronize()
+            assert torch.equal(outs[i], q1), f"rep {rep} tensor {i}"
+            assert torch.equal(params[i][:2], p1[:2]), f"rep {rep} tensor {i}"
+            if rep == 0:
+                check_codes_vs_oracle(xs[i], outs[i], params[i], f"tensor {i} K={Ks[i]}")
+
+
 # -------------------------------------------------------------- channel sums
 
 @pytest.mark.parametrize("N,K", [(1, 1), (5, 31), (64, 128), (1152, 1152), (70, 9 * 48),
