@@ -334,9 +334,9 @@ def shape_sweep(device, reps=50, warmup=10):
     outside the events).  Per shape: median / p10 / p90 microseconds at b = 8
     and at the lowest b of the layer's table row, the roofline of the shape
     (2MNK ops against the dense int8 MFMA peak, M*K + N*K + 4*M*N bytes
-    against HBM), the packed-weight kernel's median, and, as external
-    context only, the vendor int8 GEMM (hipBLASLt through torch._int_mm,
-    int32 output, b = 8)."""
+    against HBM), the packed-weight kernel's median, the median under AUTO
+    with both int8 copies given, and, as external context only, the vendor
+    int8 GEMM (hipBLASLt through torch._int_mm, int32 output, b = 8)."""
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=device)
     ev = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
 
@@ -383,15 +383,21 @@ def shape_sweep(device, reps=50, warmup=10):
                                                         workspace=ws)
                     fp = lambda b=bits: T.masked_conv3x3(X, None, wl.sx, sw, b, packed=P,
                                                          want_acc=False, y=yb)
+                    fa = lambda b=bits: T.masked_conv3x3(X, W, wl.sx, sw, b, packed=P,
+                                                         want_acc=False, y=yb, workspace=ws)
                 else:
                     f = lambda b=bits: T.masked_linear(X, W, wl.sx, sw, b, want_acc=False, y=yb,
                                                        workspace=ws)
                     fp = lambda b=bits: T.masked_linear(X, None, wl.sx, sw, b, packed=P,
                                                         want_acc=False, y=yb)
+                    fa = lambda b=bits: T.masked_linear(X, W, wl.sx, sw, b, packed=P,
+                                                        want_acc=False, y=yb, workspace=ws)
                 med, p10, p90 = timed(f)
                 row[f"b{bits}_us"] = {"median": round(med, 2), "p10": round(p10, 2),
                                       "p90": round(p90, 2)}
                 row[f"b{bits}_packed_us_median"] = round(timed(fp)[0], 2)
+                # AUTO with both int8 copies given (it picks one by shape)
+                row[f"b{bits}_auto_us_median"] = round(timed(fa)[0], 2)
             ops = 2.0 * spec.M * spec.N * spec.K
             byts = float(spec.M * (spec.C if conv else spec.K) + spec.N * spec.K
                          + 4 * spec.M * spec.N)

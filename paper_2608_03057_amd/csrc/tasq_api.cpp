@@ -319,10 +319,22 @@ enum WeightSrc { SRC_NONE = 0, SRC_ROWS, SRC_PACKED, SRC_PLANES };
 // there AUTO prefers the packed copy when one is given.  For M in the
 // thousands the weights are a few percent of the traffic and rebuilding the
 // bytes from planes per output tile costs more than it saves, so AUTO takes
-// the packed copy, then the rows, and the bit-plane GEMM only when no other
-// copy is given.  any_below8: the layer runs at some b below 8 (its b for
-// a single call; any entry of its table row for a schedule).
-WeightSrc weight_source(const LayerDesc &d, const tasq_opts *o, bool any_below8)
+// the int8 copies, and the bit-plane GEMM only when no other copy is given.
+// Between the two int8 copies (both given):
+//   * a single layer takes the packed copy when it has more than one
+//     256x256 tile per two compute units, the rows otherwise.  Measured per
+//     layer (us, b = 8, cold cache, rows / packed): PixArt QKV 8192x1152x3456
+//     (448 tiles) 60.4 / 57.0, MLP-up (576) 82.6 / 78.0, MLP-down (160)
+//     72.5 / 71.0, SANA GLU-up (704) 145.4 / 133.4; SDXL-Turbo A-QKV (128)
+//     17.8 / 18.4, B-QKV (60) 17.9 / 21.6, B-ff-down (20) 30.6 / 33.9, the
+//     3x3 conv (20) 69.4 / 71.5, 256x1152x1152 (5) 10.6 / 12.1;
+//   * a schedule takes the rows, whose grouped step runs as the persistent
+//     launch: 4.23 ms per denoising step of the 28-block PixArt-shaped
+//     schedule against 4.59 ms for the grouped packed-weight launch.
+// any_below8: the layer runs at some b below 8 (its b for a single call; any
+// entry of its table row for a schedule).
+WeightSrc weight_source(const LayerDesc &d, const tasq_opts *o, bool any_below8,
+                        bool in_schedule)
 {
     const bool rows = d.W != nullptr, packed = d.Wp != nullptr, planes = d.P != nullptr;
     switch (variant_of_opts(o)) {
@@ -338,6 +350,12 @@ WeightSrc weight_source(const LayerDesc &d, const tasq_opts *o, bool any_below8)
     const bool linear = d.kind == tasq::KIND_LINEAR;
     if (planes && linear && skinny_shape(d) && planes_fit(d) && (any_below8 || !packed))
         return SRC_PLANES;
+    if (packed && rows && !skinny_shape(d)) {
+        if (in_schedule)
+            return aligned16(d.W) ? SRC_ROWS : SRC_PACKED;
+        const long long tiles = (long long)((d.M + 255) / 256) * ((d.N + 255) / 256);
+        return tiles > kComputeUnits / 2 ? SRC_PACKED : SRC_ROWS;
+    }
     if (packed)
         return SRC_PACKED;
     if (rows)
@@ -375,7 +393,7 @@ int launch_layer(const LayerDesc &d, const tasq_opts *o, hipStream_t stream,
     if (d.M == 0 || d.N == 0)
         return TASQ_OK;
     hipError_t e;
-    const WeightSrc wsrc = weight_source(d, o, d.bits < 8);
+    const WeightSrc wsrc = weight_source(d, o, d.bits < 8, false);
     tasq::SkinnyWeights src;
     if (skinny_source(d, wsrc, src)) {
         e = tasq::launch_skinny(d, src, stream);
@@ -999,7 +1017,7 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
         bool below8 = false;
         for (int s = s_first; s <= s_last; ++s)
             below8 = below8 || b_table[(size_t)l * S + s] < 8;
-        wsrc[l] = weight_source(descs[l], opts, below8);
+        wsrc[l] = weight_source(descs[l], opts, below8, true);
     }
     tasq::SkinnyWeights src = tasq::SKINNY_ROWS;
     bool all_skinny = have_ws;

@@ -118,8 +118,10 @@ def test_auto_picks_weight_copy_per_shape(M):
         cases = [
             # (copies given, weight AUTO must read)
             (dict(W=rows_d, planes=planes_d), W_planes if skinny else W_rows),
+            # rows and packed: a stream takes the packed copy; a layer of at
+            # most 128 256x256 tiles (this one has 32 at M = 8192) the rows
             (dict(W=rows_d, planes=planes_d, packed=packed_d),
-             W_planes if skinny and b < 8 else W_packed),
+             (W_planes if b < 8 else W_packed) if skinny else W_rows),
             (dict(W=None, planes=planes_d), W_planes),
             (dict(W=None, planes=planes_d, packed=packed_d),
              W_planes if skinny and b < 8 else W_packed),
@@ -131,6 +133,31 @@ def test_auto_picks_weight_copy_per_shape(M):
             ra, ry = oracle.masked_linear(X, want, SX, sw, b)
             check_outputs(acc, y, ra, ry, SX, sw, None,
                           f"M={M} b={b} copies={sorted(copies) + (['W'] if W is not None else [])}")
+
+
+def test_auto_large_layer_reads_packed_copy():
+    """A single layer of more than 128 256x256 tiles (4096 x 4352: 272) under
+    AUTO with both int8 copies given reads the packed copy; the same weights
+    in a grouped schedule read the rows (the persistent step).  Sampled rows
+    against the oracle."""
+    M, N, K = 4096, 4352, 256
+    (W_rows, W_packed, _), sw = three_weights(760, N, K)
+    X = inputs.random_case(761, M, N, K)[0]
+    Xd, swd = X.to(DEV), sw.to(DEV)
+    rows_d, packed_d = W_rows.to(DEV), T.pack_weights(W_packed.to(DEV))
+    rows = slice(2000, 2064)
+    acc, y = T.masked_linear(Xd, rows_d, SX, swd, 6, packed=packed_d)
+    torch.cuda.synchronize()
+    ra, ry = oracle.masked_linear(X[rows], W_packed, SX, sw, 6)
+    check_outputs(acc[rows], y[rows], ra, ry, SX, sw, None, "single layer, AUTO, packed copy")
+    acc.fill_(0)
+    y.fill_(0)
+    layer = T.make_layer(Xd, rows_d, SX, swd, None, acc, y, packed=packed_d)
+    ws = torch.empty(T.schedule_workspace_bytes([layer]), dtype=torch.uint8, device=DEV)
+    T.run_schedule([layer], torch.tensor([[6]], dtype=torch.uint8), 1, 1, 0, 1, workspace=ws)
+    torch.cuda.synchronize()
+    ra, ry = oracle.masked_linear(X[rows], W_rows, SX, sw, 6)
+    check_outputs(acc[rows], y[rows], ra, ry, SX, sw, None, "schedule, AUTO, rows")
 
 
 def test_auto_schedule_streams_planes():
