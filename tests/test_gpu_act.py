@@ -105,7 +105,7 @@ def check_codes_vs_oracle(x_cpu, q, params, where):
 
 
 def test_quantizer_batch_matches_single_and_oracle():
-    """The batched quantizer over 21 tensors (three groups of launches):
+    """The batched quantizer over 22 tensors (three groups of launches):
     ragged shapes, an unaligned view (element-wise path), empty tensors in
     the list and one tensor of more than a million elements; every tensor's
     codes, alpha and z against the oracle and bit-identical to the
