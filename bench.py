@@ -761,7 +761,7 @@ def main():
             ach = ops_step / (launch_ms * 1e-3) / 1e12
             roof = dict(bound="mfma", achieved=round(ach, 1), peak=PEAK_INT8_TOPS, unit="TOP/s",
                         frac=round(ach / PEAK_INT8_TOPS, 4), traffic=recorded_traffic(kname))
-        roof["kernel"] = f"{kname} (one launch = one denoising step, 112 GEMMs)"
+        roof["kernel"] = (f"{kname}_ds" if kname == "k_masked_gemm_persistent" else kname) + " (one launch = one denoising step, 112 GEMMs)"
         roof["launch_ms"] = round(launch_ms, 4)
         roof["launch_ms_event_pairs"] = round(launch_pairs_ms, 4)
         roof["mfma_frac"] = round(ops_step / (launch_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)
