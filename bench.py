@@ -552,7 +552,7 @@ def act_schedule(wl, table, keep, ws, device, reps=2, rank=32):
             "quantizer_roofline": {
                 "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(ach / PEAK_HBM_GBS, 4), "algorithmic_bytes": alg,
-                "kernels": {"plain": "k_act_batch (all layers in ceil(L / 8) + 1 launches)",
+                "kernels": {"plain": "k_act_batch (one launch per group of tensors, plus one)",
                             "lowrank": "k_lowrank_down<true>, k_act_quantize per layer",
                             "wzero": "k_act_batch, then k_row_sums per layer"}[kind]}}
         if kind == "plain":

@@ -333,7 +333,8 @@ typedef struct tasq_act_job {
 /*
  * The quantizer of tasq_quantize_activations (App. A.1.2, Eqs. act_quant
  * and act_scale) over n tensors, e.g. the inputs of every layer of one
- * denoising step, in about n / 8 + 1 launches instead of 2 n (the range
+ * denoising step, in one launch per group of up to 8 tensors (and 128 MB of
+ * x) plus one, instead of 2 n launches (the range
  * pass of each group of tensors shares a launch with the code pass of the
  * group before).  Every job's codes, alpha and z equal those of a
  * tasq_quantize_activations call on it.
