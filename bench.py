@@ -46,16 +46,16 @@ KERNEL_SOURCES = {
                                  "tile_256x256_k128_w8_pf1.hip", "tasq_api.cpp"],
     "k_masked_gemm_grouped": ["gemm_core.h", "tasq_internal.h", "tile_256x256_k128_w8_pf1.hip",
                               "tasq_api.cpp"],
-    "k_gemm_packed_grouped": ["gemm_core.h", "gemm_packed.h", "tasq_internal.h",
-                              "ptile_256x256_k128_w8.hip", "tasq_api.cpp"],
+    "k_gemm_packed_persistent": ["gemm_core.h", "gemm_packed.h", "gemm_pers.h",
+                                 "gemm_pers_packed.h", "tasq_internal.h",
+                                 "ptile_256x256_k128_w8.hip", "tasq_api.cpp"],
 }
 
 
 def step_kernel(weights: str) -> str:
     """The kernel of one denoising step of the 28-block schedule: the
-    persistent grouped launch for row-major weights, the grouped
-    packed-weight launch otherwise."""
-    return "k_gemm_packed_grouped" if weights == "packed" else "k_masked_gemm_persistent"
+    persistent grouped launch of the weight layout."""
+    return "k_gemm_packed_persistent" if weights == "packed" else "k_masked_gemm_persistent"
 
 
 def kernel_source_sha256(kernel: str = "k_masked_gemm_persistent") -> str:

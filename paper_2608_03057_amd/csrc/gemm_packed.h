@@ -283,7 +283,7 @@ hipError_t launch_packed_grouped(const LayerDesc *d_descs, int L, int total_tile
     {                                                                                         \
         static const PackedTileOps ops = {{CFG::BM, CFG::BN, CFG::BK},                        \
                                           &launch_packed_single<CFG>,                         \
-                                          &launch_packed_grouped<CFG>};                       \
+                                          &launch_packed_grouped<CFG>, nullptr};              \
         return ops;                                                                           \
     }
 

@@ -114,11 +114,11 @@ int check_tuning(const tasq_opts *o)
 // terms runs as a persistent launch (one workgroup per compute unit, tile
 // boundaries overlapped) with the 256x256 tile once there are at least two
 // tiles per compute unit, unless the caller forces it off or on.
-bool use_persistent(const tasq_opts *o, int tile, long long total)
+bool use_persistent(const tasq_opts *o, bool big_tile, long long total)
 {
     if (o && o->persistent)
         return o->persistent == 2;
-    return tile == tasq::TILE_256x256_K128_W8_PF1 && total >= 2LL * kComputeUnits;
+    return big_tile && total >= 2LL * kComputeUnits;
 }
 
 int persistent_wgs_per_xcd(const tasq_opts *o)
@@ -1077,25 +1077,29 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
                                   hipStream_t) = nullptr;
         hipError_t (*launch_persistent)(const LayerDesc *, int, int, const uint8_t *, int, int,
                                         int, int, hipStream_t) = nullptr;
-        int persistent_tile = -1;
+        bool big_tile = false;      // the 256x256 tile, which AUTO runs persistent
+        bool extras = false;
+        for (int l = 0; l < LG; ++l)
+            extras = extras || descs[l].lr_T != nullptr || descs[l].wz != nullptr;
         if (all_skinny) {
             // one unit per 32 output channels, all tokens
             ts = {tasq::kSkinnyMaxM, 32, 128};
         } else if (all_packed) {
-            const tasq::PackedTileOps &ops = tasq::packed_tile_ops(pick_packed_grouped_tile(opts));
+            const int ptile = pick_packed_grouped_tile(opts);
+            const tasq::PackedTileOps &ops = tasq::packed_tile_ops(ptile);
             ts = ops.shape;
             launch_step = ops.grouped;
+            if (!any_conv && !extras)
+                launch_persistent = ops.persistent;
+            big_tile = ptile == tasq::PTILE_256x256_K128_W8;
         } else {
             const int tile = pick_grouped_tile(opts, descs);
             const tasq::TileOps &ops = tasq::tile_ops(tile);
             ts = ops.shape;
             launch_step = ops.grouped;
-            bool extras = false;
-            for (int l = 0; l < LG; ++l)
-                extras = extras || descs[l].lr_T != nullptr || descs[l].wz != nullptr;
             if (!any_conv && !extras)
                 launch_persistent = ops.persistent;
-            persistent_tile = tile;
+            big_tile = tile == tasq::TILE_256x256_K128_W8_PF1;
         }
         long long total = 0;
         for (int l = 0; l < LG; ++l) {
@@ -1110,7 +1114,7 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
         }
         if (total == 0 && solo.empty())
             return TASQ_OK;
-        if (!use_persistent(opts, persistent_tile, total))
+        if (!use_persistent(opts, big_tile, total))
             launch_persistent = nullptr;
         const int wgs_per_xcd = persistent_wgs_per_xcd(opts);
         const int parties = persistent_parties(opts, wgs_per_xcd);

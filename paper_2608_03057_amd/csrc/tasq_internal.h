@@ -95,6 +95,11 @@ struct PackedTileOps {
     hipError_t (*grouped)(const LayerDesc *d_descs, int L, int total_tiles,
                           const uint8_t *d_table, int S, int stage, bool any_conv,
                           hipStream_t stream);
+    // Persistent grouped step (linear layers, no low-rank or weight-zero-
+    // point terms), or null for tiles without one.
+    hipError_t (*persistent)(const LayerDesc *d_descs, int L, int total_tiles,
+                             const uint8_t *d_table, int S, int stage, int wgs_per_xcd,
+                             int parties, hipStream_t stream);
 };
 
 enum PackedTileId : int {

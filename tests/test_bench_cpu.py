@@ -36,7 +36,7 @@ def test_multi_gpu_request_exits_with_message():
 
 def test_kernel_source_hash_is_stable_and_per_kernel():
     a = bench.kernel_source_sha256("k_masked_gemm_grouped")
-    b = bench.kernel_source_sha256("k_gemm_packed_grouped")
+    b = bench.kernel_source_sha256("k_gemm_packed_persistent")
     assert a == bench.kernel_source_sha256("k_masked_gemm_grouped")
     assert len(a) == 64 and a != b
 

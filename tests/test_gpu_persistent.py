@@ -114,3 +114,33 @@ def test_persistent_matches_grouped():
     ra, ry = oracle.masked_linear(X[rows], W, SX, sw, 8, bias)
     check_outputs(results[("1", 0)][0][0][rows], results[("1", 0)][0][1][rows], ra, ry, SX, sw,
                   bias, "persistent 2048x2304x256 rows 1000..1099 b=8")
+
+
+@pytest.mark.parametrize("wgs,parties", [(1, 1), (3, 1), (32, 1), (6, 3), (32, 4)])
+def test_persistent_packed_schedule(wgs, parties):
+    """The persistent step on packed weights (the weights streamed from the
+    packed layout into registers, the activation K tiles requested three
+    ahead across tile boundaries), forced with few workgroups per XCD so that
+    every workgroup's request positions cross many tiles and layers."""
+    tune = dict(persistent=2, persistent_wgs=wgs, persistent_parties=parties, packed_tile=1)
+    host, layers, keep = build(170 + wgs, asym_layers=(1, 3))
+    packed = []
+    for h, ly in zip(host, layers):
+        P = T.pack_weights(h["W"].to(DEV))
+        packed.append(P)
+        ly.W = None
+        ly.W_packed = P.data_ptr()
+    S, Tn = 4, 20
+    rng = np.random.default_rng(171 + wgs)
+    table = torch.as_tensor(rng.integers(1, 9, size=(len(host), S)), dtype=torch.uint8)
+    ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
+    for (t0, t1) in [(0, 20), (0, 1), (6, 7), (12, 16)]:
+        for h in host:
+            h["acc"].fill_(12345)
+            h["y"].fill_(-7.0)
+        T.run_schedule(layers, table, S, Tn, t0, t1, workspace=ws, tune=tune)
+        torch.cuda.synchronize()
+        stage = oracle.stage_of_step(t1 - 1, S, Tn)
+        for i, h in enumerate(host):
+            b = int(table[i, stage])
+            check_layer(h, b, f"packed wgs {wgs} parties {parties} [{t0},{t1}) layer {i} b={b}")
