@@ -116,3 +116,36 @@ def test_noalloc_rejects_too_many_layers_and_enqueues_nothing():
     assert e.value.status == _lib.TASQ_ERR_WORKSPACE
     torch.cuda.synchronize()
     assert bool((dev[0]["na"][0] == 12345).all()) and bool((dev[0]["na"][1] == -7.0).all())
+
+
+@pytest.mark.parametrize("packed", [False, True])
+def test_noalloc_persistent_step_matches(packed):
+    """The persistent grouped step (forced on, 3 workgroups per XCD so that
+    each walks many tiles) through both entry points, on row-major and on
+    packed weights: the same bits."""
+    shapes = [(520, 260, 1152), (300, 200, 304), (1024, 1152, 1152)]
+    host, dev = build(shapes, 47 + packed, ("ws", "na"))
+    keep = []
+    lw, ln = layers_of(dev, "ws"), layers_of(dev, "na")
+    if packed:
+        for d, a, b in zip(dev, lw, ln):
+            P = T.pack_weights(d["W"])
+            keep.append(P)
+            for ly in (a, b):
+                ly.W = None
+                ly.W_packed = P.data_ptr()
+    S, Tn = 4, 20
+    table = torch.as_tensor(np.random.default_rng(48).integers(1, 9, size=(len(shapes), S)),
+                            dtype=torch.uint8)
+    tune = dict(persistent=2, persistent_wgs=3)
+    ws = torch.empty(T.schedule_workspace_bytes(lw), dtype=torch.uint8, device=DEV)
+    T.run_schedule(lw, table, S, Tn, 0, Tn, workspace=ws, tune=tune)
+    T.run_schedule_noalloc(ln, table, S, Tn, 0, Tn, tune=tune)
+    torch.cuda.synchronize()
+    for i, d in enumerate(dev):
+        assert torch.equal(d["ws"][0], d["na"][0]), f"packed={packed} layer {i}"
+        assert torch.equal(d["ws"][1].view(torch.int32), d["na"][1].view(torch.int32)), i
+    ref = oracle.run_schedule(host, table.numpy(), S, Tn, 0, Tn, SX)
+    for h, d, (ra, ry, b) in zip(host, dev, ref):
+        check_outputs(d["na"][0], d["na"][1], ra, ry, SX, h["sw"], h.get("bias"),
+                      f"packed={packed} b={b}")
