@@ -711,7 +711,8 @@ def main():
         wl = inputs.workload(4)
         keep = [(None, inputs.w_full(wl, l).to("cuda"), inputs.sw_full(wl, l).to("cuda"), None)
                 for l in range(len(wl.layers))]
-        print(json.dumps(skinny_schedule(wl, inputs.b_table(wl), keep, "cuda")), flush=True)
+        print(json.dumps(skinny_schedule(wl, inputs.b_table(wl), keep, "cuda", M=args.tokens or 16)),
+              flush=True)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the path shards by "

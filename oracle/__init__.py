@@ -216,14 +216,16 @@ def conv3x3_entries(X, Wt, sx, sw, b, pix, cols, bias=None):
 
 
 def pack_planes(W) -> np.ndarray:
-    """uint32 [8 x ceil(K/128) x N x 4] bit planes, most significant plane
-    first (q = 7 - p).  Element j of a row, r = j % 128, with s = r // 32,
-    h = (r % 32) // 16, i = (r % 16) // 4, c = r % 4, lands in word
-    2*h + s // 2 of block j // 128 at bit (8*c + 4*(s % 2) + i + p) % 32."""
+    """uint32 [ceil(N/32), 8, ceil(K/128), 16, 4, 2] bit planes: index
+    (nb, q, kb, r, w, f) is word w of channel n = 32*nb + 16*f + r in block kb
+    of plane p = 7 - q (most significant first).  Element j of a row,
+    e = j % 128, with s = e // 32, h = (e % 32) // 16, i = (e % 16) // 4,
+    c = e % 4, lands in word 2*h + s // 2 of block j // 128 at bit
+    (8*c + 4*(s % 2) + i + p) % 32."""
     W = _np(W, np.int8)
     N, K = W.shape
-    KB = (K + 127) // 128
-    planes = np.empty((8, KB, N, 4), np.uint32)
+    NB, KB = (N + 31) // 32, (K + 127) // 128
+    planes = np.empty((NB, 8, KB, 16, 4, 2), np.uint32)
     lib().oracle_pack_planes(_ptr(W), N, K, _ptr(planes))
     return planes
 

@@ -259,32 +259,36 @@ int oracle_conv3x3_entries(const int8_t *X, const int8_t *Wt, double sx, const f
 /*
  * Bit planes of the stored two's-complement weight (App. G.2: plane p is bit
  * p of the code, p = 0 the least significant).  Layout, in uint32 words:
- *   planes[q][kb][n][w],  q = 7 - p (most significant plane first, so the
- *   top b planes are one contiguous prefix), kb = j / 128.
- * Element j of row n, with r = j % 128, is sub-step s = r / 32, half
- * h = (r % 32) / 16, group i = (r % 16) / 4 and byte c = r % 4 of its
+ *   planes[nb][q][kb][r][w][f],  n = 32 nb + 16 f + r (r < 16),
+ *   q = 7 - p (most significant plane first, so the top b planes of a
+ *   32-channel block are one contiguous run), kb = j / 128.
+ * Element j of row n, with e = j % 128, is sub-step s = e / 32, half
+ * h = (e % 32) / 16, group i = (e % 16) / 4 and byte c = e % 4 of its
  * 16-element half; it goes to word w = 2 h + s / 2, at bit
  *   (8 c + g + p) mod 32,  g = 4 (s % 2) + i.
  * (A word holds one half's 16 elements of two sub-steps; plane p's word is
- * the plain byte-sliced word rotated left by p bits.)  KB = ceil(K / 128);
- * bits past K are zero.  A storage layout of the same bits, not arithmetic.
+ * the plain byte-sliced word rotated left by p bits.)  NB = ceil(N / 32),
+ * KB = ceil(K / 128); bits of channels past N and of codes past K are zero.
+ * A storage layout of the same bits, not arithmetic.
  */
 int oracle_pack_planes(const int8_t *W, int64_t N, int64_t K, uint32_t *planes)
 {
-    int64_t KB = (K + 127) / 128;
-    for (int64_t i = 0; i < 8 * KB * N * 4; ++i)
+    int64_t KB = (K + 127) / 128, NB = (N + 31) / 32;
+    for (int64_t i = 0; i < NB * 8 * KB * 128; ++i)
         planes[i] = 0;
     for (int q = 0; q < 8; ++q) {
         int p = 7 - q;
-        for (int64_t n = 0; n < N; ++n)
+        for (int64_t n = 0; n < N; ++n) {
+            int64_t nb = n / 32, f = (n % 32) / 16, r = n % 16;
             for (int64_t j = 0; j < K; ++j) {
                 uint32_t bit = ((uint32_t)(uint8_t)W[n * K + j] >> p) & 1u;
-                int r = (int)(j % 128);
-                int s = r / 32, h = (r % 32) / 16, i = (r % 16) / 4, c = r % 4;
+                int e = (int)(j % 128);
+                int s = e / 32, h = (e % 32) / 16, i = (e % 16) / 4, c = e % 4;
                 int w = 2 * h + s / 2, g = 4 * (s % 2) + i;
-                int64_t word = ((q * KB + j / 128) * N + n) * 4 + w;
+                int64_t word = (((nb * 8 + q) * KB + j / 128) * 16 + r) * 8 + 2 * w + f;
                 planes[word] |= bit << ((8 * c + g + p) % 32);
             }
+        }
     }
     return ORACLE_OK;
 }

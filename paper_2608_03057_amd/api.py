@@ -92,10 +92,12 @@ def workspace_bytes(M: int, N: int, K: int) -> int:
 
 
 def pack_planes(W: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """uint32 planes [8, ceil(K/128), N, 4] (as int32 storage) of int8 W [N, K]."""
+    """uint32 planes (as int32 storage) of int8 W [N, K], shaped
+    [ceil(N/32), 8, ceil(K/128), 16, 4, 2]: (32-channel block, plane, K block,
+    channel within a half, word, half), the layout of tasq_pack_planes."""
     N, K = W.shape
     _need(W, torch.int8, (N, K), "W")
-    shape = (8, (K + 127) // 128, N, 4)
+    shape = ((N + 31) // 32, 8, (K + 127) // 128, 16, 4, 2)
     if out is None:
         out = torch.empty(shape, dtype=torch.int32, device=W.device)
     _need(out, torch.int32, shape, "planes")

@@ -185,19 +185,29 @@ __device__ __forceinline__ uint32_t plane_place(uint32_t merged, int g)
     return __builtin_amdgcn_alignbit(merged, merged, (uint32_t)g);
 }
 
+// Bytes of the bit-plane buffer of an [N][K] weight (tasq_pack_planes): 8
+// planes x 32 * ceil(N/32) channels x ceil(K/128) blocks x 16 bytes.
+__host__ __device__ inline size_t planes_bytes(int N, int K)
+{
+    return (size_t)8 * (size_t)((N + 31) / 32) * 32 * (size_t)((K + 127) / 128) * 16;
+}
+
 // Chunk (row n, kbyte..kbyte+15, kbyte a multiple of 16) of W_b rebuilt from
 // the top b bit planes (App. G.2: the b-bit operand is the top b planes of
 // the stored buffer; the dropped planes are never read).  Plane q holds bit
-// 7 - q of each code; the result is the two's-complement byte of W_b.
+// 7 - q of each code; the result is the two's-complement byte of W_b.  Word
+// w of channel n = 32 nb + 16 f + r in block kb of plane q is word
+// ((nb * 8 + q) * KB + kb) * 128 + 8 r + 2 w + f.
 __device__ __forceinline__ v4i load_planes(const uint32_t *P, int N, int K, int b, int n,
                                            int kbyte)
 {
     if (n >= N || kbyte >= K)
         return zero4();
     const int KB = (K + 127) >> 7;
-    const size_t plane_stride = (size_t)KB * (size_t)N * 4;
+    const size_t plane_stride = (size_t)KB * 128;
     const int s = (kbyte & 127) >> 5, h = (kbyte >> 4) & 1;
-    const uint32_t *base = P + ((size_t)(kbyte >> 7) * N + n) * 4 + 2 * h + (s >> 1);
+    const uint32_t *base = P + ((size_t)(n >> 5) * 8 * KB + (size_t)(kbyte >> 7)) * 128 +
+                           8 * (n & 15) + 2 * (2 * h + (s >> 1)) + ((n >> 4) & 1);
     const int g0 = 4 * (s & 1);
     uint32_t d0 = 0, d1 = 0, d2 = 0, d3 = 0;
     for (int q = 0; q < b; ++q) {

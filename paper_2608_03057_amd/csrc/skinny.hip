@@ -4,16 +4,16 @@
 // arithmetic per byte, so its time is the weight stream.  Three sources of
 // the weight operand:
 //   * int8 rows [N][K], masked with one v_and_b32 per 4 weights;
-//   * the packed buffer (tasq_pack_weights): each 32 x 32 fragment is one
-//     contiguous 1 KB, so a wave's weight loads are fully coalesced;
+//   * the packed buffer (tasq_pack_weights), 1 KB per 32 x 32 fragment;
 //   * bit planes, reading only the top b planes (App. G.2; the dropped
 //     planes are never fetched): b/8 byte per weight, rebuilt into the
 //     two's-complement bytes of W_b in registers (one AND-OR per plane and
 //     one rotate per 4 weights, from the rotated plane words).
-// A workgroup owns 32 output channels; its 8 waves take interleaved
-// 128-byte K blocks and compute acc^T = W_b X^T with v_mfma_i32_32x32x32_i8
-// (A = 32 weight rows, B = up to 32 activation rows per m-tile).  The waves'
-// exact int32 partial sums are added through LDS in a fixed order and the
+// A workgroup owns 32 output channels; its 8 waves take interleaved 128-byte
+// K blocks and compute acc^T = W_b X^T with v_mfma_i32_16x16x64_i8, 16
+// channels x 16 tokens x 64 K per instruction (A = weight rows, B = one tile
+// of up to 16 activation rows; MT tiles cover M <= 16 MT).  The waves' exact
+// int32 partial sums are added through LDS in a fixed order and the
 // workgroup writes acc and y = acc * sx * sw[n] + bias[n] itself: one launch,
 // no atomics, no workspace.  The grouped form covers every layer of a
 // denoising step in one launch, its b taken from the (layer, stage) table.
@@ -25,72 +25,93 @@ namespace tasq {
 namespace {
 
 constexpr int SK_WAVES = 8;
-constexpr int SK_KBLK = 128;          // K bytes per block (four 32-wide MFMA steps)
+constexpr int SK_KBLK = 128;          // K bytes per block (two 64-wide MFMA steps)
 constexpr int SK_PAD = 65;            // LDS row pitch (ints) of the reduction buffer
 
 enum SkinnySource : int { SRC_ROWS = 0, SRC_PACKED = 1, SRC_PLANES = 2 };
 
-// Weight stream of output channels 32*nb .. 32*nb+31 of layer d at b bits:
-// each wave's int32 partial sums go to red, SK_WAVES * MT * 16 rows of
-// SK_PAD ints.  BP is b as a compile-time count for the plane source (one
-// copy of the loop per b, so the plane loop has no branches), 0 otherwise.
+// Weight stream of output channels 32*nb .. 32*nb+31 of layer d at b bits,
+// MT 16-token tiles: each wave's int32 partial sums go to red.  BP is b as a
+// compile-time count for the plane source (one copy of the loop per b, so
+// the plane loop has no branches), 0 otherwise.
+//
+// Operand order.  Lane l feeds row r = l % 16 of both operands (a channel of
+// the A operand, a token of the B operand) with 16 consecutive K bytes; a
+// wave takes both 16-channel halves f of the block (channels n0 + 16 f + r).
+// Any assignment of a block's K bytes to (lane group, step) gives the same
+// sums when both operands follow it; lane group j = l / 16 takes bytes
+// kj + 32 t at step t = 0, 1, kj = 64 (j & 1) + 16 (j >> 1).  These are
+// exactly the codes of plane word j of the block (groups 0-3 of the word:
+// t = 0, groups 4-7: t = 1), and the plane layout stores word j of channels
+// n0 + r and n0 + 16 + r side by side, so a lane reads both halves' word
+// with one 8-byte load per plane: a wave reads 512 contiguous bytes per
+// plane and block, and a workgroup's top b planes are one contiguous run.
+// Register v of accumulator (f, mt) of lane l is channel n0 + 16 f +
+// 4 (l / 16) + v, token 16 mt + l % 16.
 template <int SRC, int MT, int BP>
 __device__ __forceinline__ void skinny_stream(const LayerDesc &d, int b, int nb, int *red)
 {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int h = lane >> 5, r = lane & 31;
+    const int r = lane & 15, j = lane >> 4;
     const int n0 = nb * 32;
-    const int n = n0 + r;
     const int nkb = (d.K + SK_KBLK - 1) / SK_KBLK;
+    const uint32_t kj = 64u * (uint32_t)(j & 1) + 16u * (uint32_t)(j >> 1);
 
     const rsrc_t rX = make_rsrc(d.X, (uint32_t)d.M * (uint32_t)d.K);
     uint32_t offX[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-        const int m = 32 * mt + r;
-        offX[mt] = m < d.M ? (uint32_t)m * (uint32_t)d.K + 16 * h : kOOB;
+        const int m = 16 * mt + r;
+        offX[mt] = m < d.M ? (uint32_t)m * (uint32_t)d.K + kj : kOOB;
     }
     const int msk = (int)keep_mask_dword(b);
 
-    v16i acc[MT];
+    v4i acc[2][MT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-        acc[mt] = v16i{};
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            acc[f][mt] = zero4();
 
     rsrc_t rW;
-    uint32_t offW;
+    uint32_t offW[2];
     uint32_t plane_stride = 0;
     if constexpr (SRC == SRC_PLANES) {
-        // words planes[q][kb][n][2h], [2h + 1]: this lane half's 16 weights
-        // of sub-steps 0, 1 and of 2, 3
-        plane_stride = (uint32_t)nkb * (uint32_t)d.N * 16u;
-        rW = make_rsrc(d.P, 8u * plane_stride);
-        offW = n < d.N ? (uint32_t)n * 16u + 8u * (uint32_t)h : kOOB;
+        // words planes[nb][q][kb][r][j][0..1]
+        plane_stride = (uint32_t)nkb * 512u;
+        rW = make_rsrc(d.P, (uint32_t)planes_bytes(d.N, d.K));
+        offW[0] = (uint32_t)nb * 8u * plane_stride + (uint32_t)(4 * r + j) * 8u;
+        offW[1] = 0;
     } else if constexpr (SRC == SRC_PACKED) {
-        // unit (nb, 4*kb + s), this lane's 16 bytes
-        const int NB = (d.N + 31) / 32;
+        // unit (nb, 4 kb + 2 (j & 1) + t), row 16 f + r of lane half j >> 1
         rW = make_rsrc(d.Wp, (uint32_t)packed_weight_bytes(d.N, d.K));
-        offW = nb < NB ? (uint32_t)nb * (uint32_t)(4 * nkb) * 1024u + (uint32_t)lane * 16u : kOOB;
+        const uint32_t o = (uint32_t)nb * (uint32_t)(4 * nkb) * 1024u + 2048u * (uint32_t)(j & 1) +
+                           (uint32_t)(32 * (j >> 1) + r) * 16u;
+        offW[0] = o;
+        offW[1] = o + 256u;
     } else {
         rW = make_rsrc(d.W, (uint32_t)d.N * (uint32_t)d.K);
-        offW = n < d.N ? (uint32_t)n * (uint32_t)d.K + 16 * h : kOOB;
+#pragma unroll
+        for (int f = 0; f < 2; ++f) {
+            const int n = n0 + 16 * f + r;
+            offW[f] = n < d.N ? (uint32_t)n * (uint32_t)d.K + kj : kOOB;
+        }
     }
 
     // One K block's operands: every load of the block is issued before any
-    // is used.  Latency is covered by the other waves of the CU rather than
-    // by a second buffer, which would halve the waves that fit.  Planes: one
-    // 8-byte load per plane (a wave reads 32 rows x 16 contiguous bytes).
+    // is used.  Latency is covered by the other waves of the CU (8 per SIMD
+    // with one token tile) rather than by a second buffer.
     struct Block {
-        v4i w[4];
         v2i pw[8];
-        v4i x[4][MT];
+        v4i w[2][2];
+        v4i x[2][MT];
     };
     auto load = [&](int kb, Block &bl) {
         const uint32_t k0 = (uint32_t)kb * SK_KBLK;
         if constexpr (SRC == SRC_PLANES) {
-            const uint32_t base = offW + (uint32_t)kb * (uint32_t)d.N * 16u;
+            const uint32_t base = offW[0] + (uint32_t)kb * 512u;
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
                 bl.pw[q] = v2i{0, 0};
@@ -99,58 +120,62 @@ __device__ __forceinline__ void skinny_stream(const LayerDesc &d, int b, int nb,
             }
         } else {
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                if constexpr (SRC == SRC_PACKED)
-                    bl.w[s] = ld16(rW, offW + (uint32_t)(4 * kb + s) * 1024u);
-                else
-                    bl.w[s] = ld16(rW, offW + k0 + 32 * s);
-            }
+            for (int f = 0; f < 2; ++f)
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    if constexpr (SRC == SRC_PACKED)
+                        bl.w[f][t] = ld16(rW, offW[f] + (uint32_t)(4 * kb + t) * 1024u);
+                    else
+                        bl.w[f][t] = ld16(rW, offW[f] + k0 + 32u * t);
+                }
         }
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
-                bl.x[s][mt] = ld16(rX, offX[mt] + k0 + 32 * s);
+                bl.x[t][mt] = ld16(rX, offX[mt] + k0 + 32u * t);
     };
-    // Sub-step s of a block: weight fragment rebuilt (planes) or masked
+    // Step t, half f: the weight fragment is rebuilt (planes) or masked
     // (int8) and consumed at once, so only one fragment is live.
     auto compute = [&](int kb, const Block &bl) {
         const uint32_t k0 = (uint32_t)kb * SK_KBLK;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            v4i wq = zero4();
-            if constexpr (SRC == SRC_PLANES) {
-                // groups 4(s % 2) .. +3 of word s / 2 of each plane
-                uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
-                const int g0 = 4 * (s & 1);
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    if (q < BP) {
-                        const uint32_t w = (uint32_t)(s < 2 ? bl.pw[q].x : bl.pw[q].y);
-                        const int p = 7 - q;
-                        m0 = plane_bits(w, g0 + 0, p, m0);
-                        m1 = plane_bits(w, g0 + 1, p, m1);
-                        m2 = plane_bits(w, g0 + 2, p, m2);
-                        m3 = plane_bits(w, g0 + 3, p, m3);
+            for (int f = 0; f < 2; ++f) {
+                v4i wq = zero4();
+                if constexpr (SRC == SRC_PLANES) {
+                    uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
+                    const int g0 = 4 * t;
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        if (q < BP) {
+                            const uint32_t w = (uint32_t)(f == 0 ? bl.pw[q].x : bl.pw[q].y);
+                            const int p = 7 - q;
+                            m0 = plane_bits(w, g0 + 0, p, m0);
+                            m1 = plane_bits(w, g0 + 1, p, m1);
+                            m2 = plane_bits(w, g0 + 2, p, m2);
+                            m3 = plane_bits(w, g0 + 3, p, m3);
+                        }
                     }
+                    wq = v4i{(int)plane_place(m0, g0 + 0), (int)plane_place(m1, g0 + 1),
+                             (int)plane_place(m2, g0 + 2), (int)plane_place(m3, g0 + 3)};
+                } else {
+                    wq = bl.w[f][t];
+                    wq.x &= msk;
+                    wq.y &= msk;
+                    wq.z &= msk;
+                    wq.w &= msk;
+                    // Columns past K: zero the weights (row-major loads there
+                    // may hold the next row; packed and plane layouts are zero).
+                    if (SRC == SRC_ROWS && k0 + kj + 32u * t >= (uint32_t)d.K)
+                        wq = zero4();
                 }
-                wq = v4i{(int)plane_place(m0, g0 + 0), (int)plane_place(m1, g0 + 1),
-                         (int)plane_place(m2, g0 + 2), (int)plane_place(m3, g0 + 3)};
-            } else {
-                wq = bl.w[s];
-                wq.x &= msk;
-                wq.y &= msk;
-                wq.z &= msk;
-                wq.w &= msk;
-                // Columns past K: zero the weights (row-major loads there may
-                // hold the next row; packed and plane layouts are zero).
-                if (SRC == SRC_ROWS && k0 + 32 * s + 16 * h >= (uint32_t)d.K)
-                    wq = zero4();
-            }
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                acc[mt] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wq, bl.x[s][mt], acc[mt], 0, 0, 0);
-        }
+                for (int mt = 0; mt < MT; ++mt)
+                    acc[f][mt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wq, bl.x[t][mt],
+                                                                         acc[f][mt], 0, 0, 0);
+            }
     };
 
     for (int kb = wave; kb < nkb; kb += SK_WAVES) {
@@ -159,13 +184,25 @@ __device__ __forceinline__ void skinny_stream(const LayerDesc &d, int b, int nb,
         compute(kb, bl);
     }
 
-    // Each wave's partial block: register v of lane l is channel
-    // 8*(v/4) + 4*(l/32) + v%4, token l%32.
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int f = 0; f < 2; ++f)
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-            red[((wave * MT + mt) * 16 + v) * SK_PAD + lane] = acc[mt][v];
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                red[(((wave * 2 + f) * MT + mt) * 4 + v) * SK_PAD + lane] = acc[f][mt][v];
+}
+
+// Ints of a workgroup's reduction buffer.
+template <int MT>
+constexpr int skinny_red_ints() { return SK_WAVES * 2 * MT * 4 * SK_PAD; }
+
+// Index in red of wave w's partial sum of token row, channel n0 + col.
+template <int MT>
+__device__ __forceinline__ int skinny_red_index(int w, int row, int col)
+{
+    const int f = col >> 4, c = col & 15;
+    return (((w * 2 + f) * MT + (row >> 4)) * 4 + (c & 3)) * SK_PAD + 16 * (c >> 2) + (row & 15);
 }
 
 // Output channels 32*nb .. 32*nb+31 of layer d at b bits: the weight stream,
@@ -196,8 +233,6 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
     // cover one 128-byte output row segment.
     const int col = tid & 31;
     const int nn = n0 + col;
-    const int vv = 4 * (col >> 3) + (col & 3);
-    const int lh = 32 * ((col & 7) >> 2);
     float scale = 0.f, bias = 0.f, corr = 0.f;
     if (nn < d.N && d.y) {
         if (d.act) {
@@ -210,16 +245,14 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
             bias = d.bias[nn];
     }
 #pragma unroll
-    for (int i = 0; i < 2 * MT; ++i) {
+    for (int i = 0; i < MT; ++i) {
         const int row = (tid >> 5) + 16 * i;
         if (row >= d.M || nn >= d.N)
             continue;
-        const int mt = row >> 5;
-        const int ln = (row & 31) + lh;
         int sum = 0;
 #pragma unroll
         for (int w = 0; w < SK_WAVES; ++w)
-            sum += red[((w * MT + mt) * 16 + vv) * SK_PAD + ln];
+            sum += red[skinny_red_index<MT>(w, row, col)];
         const size_t o = (size_t)row * (size_t)d.N + (size_t)nn;
         if (d.acc)
             d.acc[o] = sum;
@@ -245,17 +278,18 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
     }
 }
 
-// Occupancy: with one 32-token block (MT = 1) the streaming loop fits 80
-// VGPRs, i.e. 6 waves per SIMD (three 8-wave workgroups per CU); the
-// epilogue's optional terms must not push it past that.
+// Occupancy: with one token tile the streaming loop fits 64 VGPRs, 8 waves
+// per SIMD (four 8-wave workgroups per CU); each further tile adds 16
+// accumulator and activation registers.  The epilogue's optional terms must
+// not push a form past its count.
 template <int MT>
-constexpr int skinny_waves_per_eu() { return MT == 1 ? 6 : 4; }
+constexpr int skinny_waves_per_eu() { return MT == 1 ? 8 : MT == 2 ? 6 : MT == 3 ? 5 : 4; }
 
 template <int SRC, int MT>
 __global__ void __launch_bounds__(SK_WAVES * 64)
 __attribute__((amdgpu_waves_per_eu(skinny_waves_per_eu<MT>()))) k_skinny(LayerDesc d)
 {
-    __shared__ int red[SK_WAVES * MT * 16 * SK_PAD];
+    __shared__ int red[skinny_red_ints<MT>()];
     skinny_block<SRC, MT>(d, d.bits, blockIdx.x, red);
 }
 
@@ -266,7 +300,7 @@ __global__ void __launch_bounds__(SK_WAVES * 64)
 __attribute__((amdgpu_waves_per_eu(skinny_waves_per_eu<MT>())))
 k_skinny_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *table, int S, int stage)
 {
-    __shared__ int red[SK_WAVES * MT * 16 * SK_PAD];
+    __shared__ int red[skinny_red_ints<MT>()];
     const int t = blockIdx.x;
     int lo = 0, hi = L - 1;
     while (lo < hi) {
@@ -280,28 +314,51 @@ k_skinny_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *tabl
     skinny_block<SRC, MT>(d, table[d.layer * S + stage], t - d.tile_begin + d.tile_first, red);
 }
 
+// Token tiles of 16 rows for M rows (M <= 64).
+template <int SRC, template <int, int> class Launch, typename... Args>
+hipError_t dispatch_tiles(int m, Args... args)
+{
+    if (m > 48)
+        return Launch<SRC, 4>::run(args...);
+    if (m > 32)
+        return Launch<SRC, 3>::run(args...);
+    if (m > 16)
+        return Launch<SRC, 2>::run(args...);
+    return Launch<SRC, 1>::run(args...);
+}
+
+template <int SRC, int MT>
+struct LaunchSingle {
+    static hipError_t run(const LayerDesc &d, hipStream_t stream)
+    {
+        const unsigned grid = (unsigned)((d.N + 31) / 32);
+        hipLaunchKernelGGL((k_skinny<SRC, MT>), dim3(grid), dim3(SK_WAVES * 64), 0, stream, d);
+        return hipGetLastError();
+    }
+};
+
+template <int SRC, int MT>
+struct LaunchGrouped {
+    static hipError_t run(const LayerDesc *d_descs, int L, int total, const uint8_t *d_table,
+                          int S, int stage, hipStream_t stream)
+    {
+        hipLaunchKernelGGL((k_skinny_grouped<SRC, MT>), dim3((unsigned)total),
+                           dim3(SK_WAVES * 64), 0, stream, d_descs, L, d_table, S, stage);
+        return hipGetLastError();
+    }
+};
+
 template <int SRC>
 hipError_t launch_single_src(const LayerDesc &d, hipStream_t stream)
 {
-    const unsigned grid = (unsigned)((d.N + 31) / 32);
-    if (d.M > 32)
-        hipLaunchKernelGGL((k_skinny<SRC, 2>), dim3(grid), dim3(SK_WAVES * 64), 0, stream, d);
-    else
-        hipLaunchKernelGGL((k_skinny<SRC, 1>), dim3(grid), dim3(SK_WAVES * 64), 0, stream, d);
-    return hipGetLastError();
+    return dispatch_tiles<SRC, LaunchSingle>(d.M, d, stream);
 }
 
 template <int SRC>
 hipError_t launch_grouped_src(const LayerDesc *d_descs, int L, int total, int max_m,
                               const uint8_t *d_table, int S, int stage, hipStream_t stream)
 {
-    if (max_m > 32)
-        hipLaunchKernelGGL((k_skinny_grouped<SRC, 2>), dim3((unsigned)total), dim3(SK_WAVES * 64),
-                           0, stream, d_descs, L, d_table, S, stage);
-    else
-        hipLaunchKernelGGL((k_skinny_grouped<SRC, 1>), dim3((unsigned)total), dim3(SK_WAVES * 64),
-                           0, stream, d_descs, L, d_table, S, stage);
-    return hipGetLastError();
+    return dispatch_tiles<SRC, LaunchGrouped>(max_m, d_descs, L, total, d_table, S, stage, stream);
 }
 
 }  // namespace

@@ -288,7 +288,7 @@ bool packed_fits(const LayerDesc &d)
 // The planes are addressed with 32-bit offsets by the weight-streaming kernel.
 bool planes_fit(const LayerDesc &d)
 {
-    return (long long)8 * ((d.K + 127) / 128) * d.N * 16 < (1LL << 31);
+    return tasq::planes_bytes_host(d.N, d.K) < (1ULL << 31);
 }
 
 // Activation operand on the 16-byte buffer fast path.
@@ -664,9 +664,7 @@ int tasq_stage_of_step(int t, int S, int T)
 
 size_t tasq_planes_bytes(int N, int K)
 {
-    if (N < 0 || K < 0)
-        return 0;
-    return (size_t)8 * (size_t)((K + 127) / 128) * (size_t)N * 16;
+    return (size_t)tasq::planes_bytes_host(N, K);
 }
 
 size_t tasq_workspace_bytes(int M, int N, int K)

@@ -123,6 +123,15 @@ inline unsigned long long packed_weight_bytes_host(long long N, long long K)
            128ULL;
 }
 
+// Bytes of the bit-plane buffer: 8 * 32 * ceil(N/32) * ceil(K/128) * 16.
+inline unsigned long long planes_bytes_host(long long N, long long K)
+{
+    if (N <= 0 || K <= 0)
+        return 0;
+    return 8ULL * (unsigned long long)((N + 31) / 32) * 32ULL *
+           (unsigned long long)((K + 127) / 128) * 16ULL;
+}
+
 // Asymmetric 8-bit activation quantizer and the channel sums of the masked
 // weight (act_quant.hip).  params: device float[kActHeader + 2 * kActPartials],
 // [0] alpha, [1] z on completion, [kActHeader..] partial ranges.

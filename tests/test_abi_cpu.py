@@ -48,9 +48,12 @@ def test_stage_of_step_range(t, S, T):
 
 
 def test_planes_bytes():
+    # 8 planes x 32 * ceil(N/32) channels x ceil(K/128) blocks x 16 bytes
     assert L.tasq_planes_bytes(1152, 1152) == 8 * 9 * 1152 * 16
-    assert L.tasq_planes_bytes(3, 1) == 8 * 1 * 3 * 16
-    assert L.tasq_planes_bytes(3, 129) == 8 * 2 * 3 * 16
+    assert L.tasq_planes_bytes(3, 1) == 8 * 1 * 32 * 16
+    assert L.tasq_planes_bytes(3, 129) == 8 * 2 * 32 * 16
+    assert L.tasq_planes_bytes(33, 128) == 8 * 1 * 64 * 16
+    assert L.tasq_planes_bytes(0, 128) == 0 and L.tasq_planes_bytes(5, 0) == 0
 
 
 def lin(**kw):

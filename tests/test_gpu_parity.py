@@ -305,12 +305,26 @@ def test_skinny_weight_streaming(case, source):
                       f"skinny y-only {M}x{N}x{K} {source} b={b}")
 
 
+SKINNY_SCHEDULES = {
+    # four 16-token tiles (largest M 64)
+    "m64": [(16, 1152, 1152), (16, 3456, 1152), (64, 130, 528), (33, 257, 1152),
+            (1, 37, 1152)],
+    # one 16-token tile (largest M 16): ragged N, K = 1040 and 144 (a partial
+    # last 128-wide block), a layer whose K blocks outnumber the waves
+    "m16": [(16, 1152, 1152), (5, 300, 1040), (1, 37, 1152), (16, 1152, 4608),
+            (9, 77, 144), (2, 3456, 1152)],
+    # two tiles (largest M 32) and three (largest M 40)
+    "m32": [(32, 300, 1040), (17, 1152, 1152), (1, 37, 144)],
+    "m40": [(40, 130, 528), (16, 1152, 1152), (33, 77, 1040)],
+}
+
+
+@pytest.mark.parametrize("group", sorted(SKINNY_SCHEDULES))
 @pytest.mark.parametrize("source", ["rows", "packed", "planes"])
-def test_skinny_schedule_grouped(source):
+def test_skinny_schedule_grouped(source, group):
     """A schedule of skinny layers (M <= 64) runs one weight-streaming launch
     per step; every step range matches the oracle's literal step loop."""
-    shapes = [(16, 1152, 1152), (16, 3456, 1152), (64, 130, 528), (33, 257, 1152),
-              (1, 37, 1152)]
+    shapes = SKINNY_SCHEDULES[group]
     host, dev = [], []
     for i, (M, N, K) in enumerate(shapes):
         X, W, sw, bias = inputs.random_case(700 + i, M, N, K)

@@ -260,11 +260,19 @@ def test_conv_entries_match_full():
 
 # ---------------------------------------------------------------- bit planes
 
-def unpack(planes, K):
+def words_by_channel(planes, N):
+    """[nb, q, kb, r, w, f] plane words as [q, kb, n, w], n = 32*nb + 16*f + r."""
+    NB, Q, KB, R, Wn, F = planes.shape
+    assert (R, Wn, F) == (16, 4, 2)
+    return planes.transpose(1, 2, 0, 5, 3, 4).reshape(Q, KB, NB * 32, 4)[:, :, :N, :]
+
+
+def unpack(planes, N, K):
     """Bit plane q (q = 7 - p) back to a {0,1} int64 array [8 x N x K].
-    Element j: r = j % 128 is sub-step r // 32, half (r % 32) // 16, group
-    (r % 16) // 4, byte r % 4; word 2*half + sub-step // 2, and plane p's bit
+    Element j: e = j % 128 is sub-step e // 32, half (e % 32) // 16, group
+    (e % 16) // 4, byte e % 4; word 2*half + sub-step // 2, and plane p's bit
     at (8*byte + 4*(sub-step % 2) + group + p) mod 32."""
+    planes = words_by_channel(planes, N)
     Q, KB, N, _ = planes.shape
     j = np.arange(K)
     r = j % 128
@@ -281,40 +289,53 @@ def unpack(planes, K):
 
 
 def test_planes_bit_position_worked_example():
-    """Positions worked out by hand from the layout definition:
-    element 0 = 1 (sub-step 0, half 0, group 0, byte 0) sets bit
-    (0 + 0 + p=0) = 0 of word 0 of plane p = 0 (q = 7);
-    element 5 = -128 (group 1, byte 1) sets bit (8 + 1 + 7) = 16 of word 0
-    of the sign plane (q = 0);
-    element 63 = -128 (sub-step 1, half 1, group 3, byte 3: word 2*1 + 0 = 2)
-    sets bit (24 + 4 + 3 + 7) mod 32 = 6 of word 2 of the sign plane;
-    element 100 = 2 (sub-step 3, half 0, group 1, byte 0: word 1) sets bit
-    (0 + 4 + 1 + 1) = 6 of word 1 of plane p = 1 (q = 6)."""
-    W = np.zeros((1, 128), np.int8)
+    """Positions worked out by hand from the layout definition, as
+    (nb, q, kb, r, w, f) and as the flat word index
+    (((nb*8 + q)*KB + kb)*16 + r)*8 + 2*w + f, here KB = 1:
+    element (0, 0) = 1 (sub-step 0, half 0, group 0, byte 0) sets bit
+    (0 + 0 + p=0) = 0 of word (0, 7, 0, 0, 0, 0), flat 7*128 = 896;
+    element (0, 5) = -128 (group 1, byte 1) sets bit (8 + 1 + 7) = 16 of
+    word (0, 0, 0, 0, 0, 0) of the sign plane, flat 0;
+    element (0, 63) = -128 (sub-step 1, half 1, group 3, byte 3: word
+    2*1 + 0 = 2) sets bit (24 + 4 + 3 + 7) mod 32 = 6 of word (0, 0, 0, 0, 2, 0),
+    flat 4;
+    element (0, 100) = 2 (sub-step 3, half 0, group 1, byte 0: word 1) sets
+    bit (0 + 4 + 1 + 1) = 6 of word (0, 6, 0, 0, 1, 0) of plane p = 1, flat
+    6*128 + 2 = 770;
+    element (17, 0) = -128 (channel 17: nb 0, f 1, r 1) sets bit 7 of word
+    (0, 0, 0, 1, 0, 1), flat 8 + 1 = 9;
+    element (33, 127) = 1 (channel 33: nb 1, f 0, r 1; sub-step 3, half 1,
+    group 3, byte 3: word 3) sets bit (24 + 4 + 3 + 0) = 31 of word
+    (1, 7, 0, 1, 3, 0), flat (15*16 + 1)*8 + 6 = 1934."""
+    W = np.zeros((40, 128), np.int8)
     W[0, 0] = 1
     W[0, 5] = -128
     W[0, 63] = -128
     W[0, 100] = 2
+    W[17, 0] = -128
+    W[33, 127] = 1
     planes = oracle.pack_planes(W)
-    assert int(planes[7, 0, 0, 0]) == 1 << 0
-    assert int(planes[0, 0, 0, 0]) == 1 << 16
-    assert int(planes[0, 0, 0, 2]) == 1 << 6
-    assert int(planes[6, 0, 0, 1]) == 1 << 6
-    assert not planes[0, 0, 0, 1] and not planes[0, 0, 0, 3]
-    assert not planes[1:6].any()
-    assert not planes[6, 0, 0, [0, 2, 3]].any() and not planes[7, 0, 0, 1:].any()
+    assert planes.shape == (2, 8, 1, 16, 4, 2)
+    expect = {896: 1 << 0, 0: 1 << 16, 4: 1 << 6, 770: 1 << 6, 9: 1 << 7, 1934: 1 << 31}
+    flat = planes.reshape(-1)
+    for idx, v in expect.items():
+        assert int(flat[idx]) == v, idx
+    assert np.count_nonzero(flat) == len(expect)
+    assert planes[0, 7, 0, 0, 0, 0] == 1 and planes[1, 7, 0, 1, 3, 0] == 1 << 31
+    assert planes[0, 0, 0, 1, 0, 1] == 1 << 7 and planes[0, 6, 0, 0, 1, 0] == 1 << 6
 
 
-@pytest.mark.parametrize("N,K", [(1, 1), (5, 31), (7, 32), (3, 100), (4, 300)])
+@pytest.mark.parametrize("N,K", [(1, 1), (5, 31), (7, 32), (3, 100), (4, 300), (40, 200)])
 def test_planes_round_trip(N, K):
     W = rand_i8((N, K))
     W[0, 0] = -128
     planes = oracle.pack_planes(W)
-    assert planes.shape == (8, (K + 127) // 128, N, 4)
-    bits = unpack(planes, K)
+    assert planes.shape == ((N + 31) // 32, 8, (K + 127) // 128, 16, 4, 2)
+    bits = unpack(planes, N, K)
     coef = np.array([-128] + [1 << p for p in range(6, -1, -1)])   # q = 0 is the sign plane
     np.testing.assert_array_equal(np.tensordot(coef, bits, 1), W.astype(np.int64))
-    # every bit past K is zero: the total popcount equals that of the K elements
+    # every bit past K and past N is zero: the total popcount equals that of
+    # the N x K elements
     total = sum(bin(int(v)).count("1") for v in planes.reshape(-1))
     assert total == int(bits.sum())
 
@@ -359,7 +380,7 @@ def test_bit_plane_identity(b):
     only the top b planes)."""
     M, N, K = 6, 9, 70
     X, W = rand_i8((M, K)), rand_i8((N, K))
-    bits = unpack(oracle.pack_planes(W), K)
+    bits = unpack(oracle.pack_planes(W), N, K)
     total = np.zeros((M, N), np.int64)
     for q in range(b):
         p = 7 - q
