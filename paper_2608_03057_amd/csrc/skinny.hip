@@ -9,14 +9,18 @@
 //     planes are never fetched): b/8 byte per weight, rebuilt into the
 //     two's-complement bytes of W_b in registers (one AND-OR per plane and
 //     one rotate per 4 weights, from the rotated plane words).
-// A workgroup owns 32 output channels; its 8 waves take interleaved 128-byte
+// A workgroup owns 32 output channels; its W waves take interleaved 128-byte
 // K blocks and compute acc^T = W_b X^T with v_mfma_i32_16x16x64_i8, 16
 // channels x 16 tokens x 64 K per instruction (A = weight rows, B = one tile
 // of up to 16 activation rows; MT tiles cover M <= 16 MT).  The waves' exact
 // int32 partial sums are added through LDS in a fixed order and the
 // workgroup writes acc and y = acc * sx * sw[n] + bias[n] itself: one launch,
 // no atomics, no workspace.  The grouped form covers every layer of a
-// denoising step in one launch, its b taken from the (layer, stage) table.
+// denoising step in one launch, its b taken from the (layer, stage) table,
+// with W = 4 waves per workgroup: nine or 36 K blocks (1152- and 4608-deep
+// layers) keep every wave busy to the end, where 8 waves leave 7 of them
+// idle through the second of a 1152-deep layer's two rounds.  A single
+// layer, with few workgroups, keeps W = 8 for more loads in flight.
 #include "gemm_core.h"
 #include "gemm_packed.h"
 
@@ -24,7 +28,8 @@ namespace tasq {
 
 namespace {
 
-constexpr int SK_WAVES = 8;
+constexpr int SK_WAVES_SINGLE = 8;    // waves per workgroup, one layer per launch
+constexpr int SK_WAVES_GROUPED = 4;   // waves per workgroup, a schedule step per launch
 constexpr int SK_KBLK = 128;          // K bytes per block (two 64-wide MFMA steps)
 constexpr int SK_PAD = 65;            // LDS row pitch (ints) of the reduction buffer
 
@@ -48,7 +53,7 @@ enum SkinnySource : int { SRC_ROWS = 0, SRC_PACKED = 1, SRC_PLANES = 2 };
 // plane and block, and a workgroup's top b planes are one contiguous run.
 // Register v of accumulator (f, mt) of lane l is channel n0 + 16 f +
 // 4 (l / 16) + v, token 16 mt + l % 16.
-template <int SRC, int MT, int BP>
+template <int SRC, int MT, int BP, int W>
 __device__ __forceinline__ void skinny_stream(const LayerDesc &d, int b, int nb, int *red)
 {
     const int tid = threadIdx.x;
@@ -178,7 +183,7 @@ __device__ __forceinline__ void skinny_stream(const LayerDesc &d, int b, int nb,
             }
     };
 
-    for (int kb = wave; kb < nkb; kb += SK_WAVES) {
+    for (int kb = wave; kb < nkb; kb += W) {
         Block bl;
         load(kb, bl);
         compute(kb, bl);
@@ -194,8 +199,8 @@ __device__ __forceinline__ void skinny_stream(const LayerDesc &d, int b, int nb,
 }
 
 // Ints of a workgroup's reduction buffer.
-template <int MT>
-constexpr int skinny_red_ints() { return SK_WAVES * 2 * MT * 4 * SK_PAD; }
+template <int MT, int W>
+constexpr int skinny_red_ints() { return W * 2 * MT * 4 * SK_PAD; }
 
 // Index in red of wave w's partial sum of token row, channel n0 + col.
 template <int MT>
@@ -207,30 +212,31 @@ __device__ __forceinline__ int skinny_red_index(int w, int row, int col)
 
 // Output channels 32*nb .. 32*nb+31 of layer d at b bits: the weight stream,
 // then the fixed-order reduction of the waves' partials and the epilogue.
-template <int SRC, int MT>
+template <int SRC, int MT, int W>
 __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, int *red)
 {
     if constexpr (SRC == SRC_PLANES) {
         switch (b) {
-        case 1: skinny_stream<SRC, MT, 1>(d, b, nb, red); break;
-        case 2: skinny_stream<SRC, MT, 2>(d, b, nb, red); break;
-        case 3: skinny_stream<SRC, MT, 3>(d, b, nb, red); break;
-        case 4: skinny_stream<SRC, MT, 4>(d, b, nb, red); break;
-        case 5: skinny_stream<SRC, MT, 5>(d, b, nb, red); break;
-        case 6: skinny_stream<SRC, MT, 6>(d, b, nb, red); break;
-        case 7: skinny_stream<SRC, MT, 7>(d, b, nb, red); break;
-        default: skinny_stream<SRC, MT, 8>(d, b, nb, red); break;
+        case 1: skinny_stream<SRC, MT, 1, W>(d, b, nb, red); break;
+        case 2: skinny_stream<SRC, MT, 2, W>(d, b, nb, red); break;
+        case 3: skinny_stream<SRC, MT, 3, W>(d, b, nb, red); break;
+        case 4: skinny_stream<SRC, MT, 4, W>(d, b, nb, red); break;
+        case 5: skinny_stream<SRC, MT, 5, W>(d, b, nb, red); break;
+        case 6: skinny_stream<SRC, MT, 6, W>(d, b, nb, red); break;
+        case 7: skinny_stream<SRC, MT, 7, W>(d, b, nb, red); break;
+        default: skinny_stream<SRC, MT, 8, W>(d, b, nb, red); break;
         }
     } else {
-        skinny_stream<SRC, MT, 0>(d, b, nb, red);
+        skinny_stream<SRC, MT, 0, W>(d, b, nb, red);
     }
     __syncthreads();
 
     const int tid = threadIdx.x;
     const int n0 = nb * 32;
 
-    // Thread t writes channel n0 + t%32 of tokens t/32 + 16*i: 32 threads
+    // Thread t writes channel n0 + t%32 of tokens t/32 + RP*i: 32 threads
     // cover one 128-byte output row segment.
+    constexpr int RP = 2 * W;               // rows per pass
     const int col = tid & 31;
     const int nn = n0 + col;
     float scale = 0.f, bias = 0.f, corr = 0.f;
@@ -245,13 +251,13 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
             bias = d.bias[nn];
     }
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-        const int row = (tid >> 5) + 16 * i;
+    for (int i = 0; i < (16 * MT + RP - 1) / RP; ++i) {
+        const int row = (tid >> 5) + RP * i;
         if (row >= d.M || nn >= d.N)
             continue;
         int sum = 0;
 #pragma unroll
-        for (int w = 0; w < SK_WAVES; ++w)
+        for (int w = 0; w < W; ++w)
             sum += red[skinny_red_index<MT>(w, row, col)];
         const size_t o = (size_t)row * (size_t)d.N + (size_t)nn;
         if (d.acc)
@@ -279,28 +285,29 @@ __device__ __forceinline__ void skinny_block(const LayerDesc &d, int b, int nb, 
 }
 
 // Occupancy: with one token tile the streaming loop fits 64 VGPRs, 8 waves
-// per SIMD (four 8-wave workgroups per CU); each further tile adds 16
+// per SIMD (32 waves per CU: four 8-wave or eight 4-wave workgroups); each
+// further tile adds 16
 // accumulator and activation registers.  The epilogue's optional terms must
 // not push a form past its count.
 template <int MT>
 constexpr int skinny_waves_per_eu() { return MT == 1 ? 8 : MT == 2 ? 6 : MT == 3 ? 5 : 4; }
 
 template <int SRC, int MT>
-__global__ void __launch_bounds__(SK_WAVES * 64)
+__global__ void __launch_bounds__(SK_WAVES_SINGLE * 64)
 __attribute__((amdgpu_waves_per_eu(skinny_waves_per_eu<MT>()))) k_skinny(LayerDesc d)
 {
-    __shared__ int red[skinny_red_ints<MT>()];
-    skinny_block<SRC, MT>(d, d.bits, blockIdx.x, red);
+    __shared__ int red[skinny_red_ints<MT, SK_WAVES_SINGLE>()];
+    skinny_block<SRC, MT, SK_WAVES_SINGLE>(d, d.bits, blockIdx.x, red);
 }
 
 // One launch per denoising step over every layer's 32-channel blocks;
 // d.tile_begin is the layer's first block.
 template <int SRC, int MT>
-__global__ void __launch_bounds__(SK_WAVES * 64)
+__global__ void __launch_bounds__(SK_WAVES_GROUPED * 64)
 __attribute__((amdgpu_waves_per_eu(skinny_waves_per_eu<MT>())))
 k_skinny_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *table, int S, int stage)
 {
-    __shared__ int red[skinny_red_ints<MT>()];
+    __shared__ int red[skinny_red_ints<MT, SK_WAVES_GROUPED>()];
     const int t = blockIdx.x;
     int lo = 0, hi = L - 1;
     while (lo < hi) {
@@ -311,7 +318,8 @@ k_skinny_grouped(const LayerDesc *__restrict__ descs, int L, const uint8_t *tabl
             hi = mid - 1;
     }
     const LayerDesc d = descs[lo];
-    skinny_block<SRC, MT>(d, table[d.layer * S + stage], t - d.tile_begin + d.tile_first, red);
+    skinny_block<SRC, MT, SK_WAVES_GROUPED>(d, table[d.layer * S + stage],
+                                            t - d.tile_begin + d.tile_first, red);
 }
 
 // Token tiles of 16 rows for M rows (M <= 64).
@@ -332,7 +340,8 @@ struct LaunchSingle {
     static hipError_t run(const LayerDesc &d, hipStream_t stream)
     {
         const unsigned grid = (unsigned)((d.N + 31) / 32);
-        hipLaunchKernelGGL((k_skinny<SRC, MT>), dim3(grid), dim3(SK_WAVES * 64), 0, stream, d);
+        hipLaunchKernelGGL((k_skinny<SRC, MT>), dim3(grid), dim3(SK_WAVES_SINGLE * 64), 0, stream,
+                           d);
         return hipGetLastError();
     }
 };
@@ -343,7 +352,8 @@ struct LaunchGrouped {
                           int S, int stage, hipStream_t stream)
     {
         hipLaunchKernelGGL((k_skinny_grouped<SRC, MT>), dim3((unsigned)total),
-                           dim3(SK_WAVES * 64), 0, stream, d_descs, L, d_table, S, stage);
+                           dim3(SK_WAVES_GROUPED * 64), 0, stream, d_descs, L, d_table, S,
+                           stage);
         return hipGetLastError();
     }
 };
