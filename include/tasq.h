@@ -256,24 +256,29 @@ int tasq_masked_conv3x3(const int8_t *X, const int8_t *W, float sx, const float 
  * Bit-plane relayout of a stored weight (App. G.2: plane p holds bit p of
  * the two's-complement code, p = 0 least significant).
  *   W          int8 [N][K] device (read only).
- *   planes_out uint32 [8][KB][N][4] device, KB = ceil(K / 128): the
- *              words planes[q][kb][n][0..3] hold bit p = 7 - q of
- *              W[n][128*kb + r], r = 0..127.  With s = r / 32, h = (r%32)/16,
- *              i = (r%16)/4, c = r%4, element r sits in word 2h + s/2 at bit
- *              (8c + 4(s%2) + i + p) mod 32: each word holds one 16-element
- *              half of two 32-element sub-steps, and plane p's word is
- *              rotated left by p, so that the planes' bits of four
+ *   planes_out uint32 [NB][8][KB][16][4][2] device, NB = ceil(N / 32),
+ *              KB = ceil(K / 128): word planes[nb][q][kb][r][w][f] is word
+ *              w of channel n = 32 nb + 16 f + r in block kb of plane
+ *              p = 7 - q, i.e. bits p of W[n][128*kb + e], e = 0..127.
+ *              With s = e / 32, h = (e%32)/16, i = (e%16)/4, c = e%4,
+ *              element e sits in word w = 2h + s/2 at bit
+ *              (8c + 4(s%2) + i + p) mod 32: each word holds one
+ *              16-element half of two 32-element sub-steps, and plane p's
+ *              word is rotated left by p, so that the planes' bits of four
  *              consecutive elements merge with one AND-OR per plane and one
- *              rotate.  Plane q = 0 is the sign plane; the top b planes are
- *              the contiguous prefix of b*KB*N*4 words.  Bits past K are
- *              zero.  Size tasq_planes_bytes(N, K).
+ *              rotate.  Plane q = 0 is the sign plane.  The top b planes of
+ *              a 32-channel block are one contiguous run of b*KB*128 words,
+ *              and words f = 0, 1 (channels n and n + 16) are adjacent.
+ *              Words of channels past N and bits past K are zero.  Size
+ *              tasq_planes_bytes(N, K).
  * A one-time conversion of the stored buffer, not a per-step cost.  A
  * caller that keeps only the planes (and passes W = NULL with the BITPLANE
  * variant) stores the weight once, at the same 8 bits per element.
  */
 int tasq_pack_planes(const int8_t *W, int N, int K, uint32_t *planes_out, void *stream);
 
-/* Bytes of the planes array for an N x K weight: 8 * ceil(K/128) * N * 16. */
+/* Bytes of the planes array for an N x K weight:
+ * 8 * ceil(K/128) * 32 * ceil(N/32) * 16; 0 when N or K is not positive. */
 size_t tasq_planes_bytes(int N, int K);
 
 /*

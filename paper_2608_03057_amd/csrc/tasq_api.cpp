@@ -312,11 +312,13 @@ enum WeightSrc { SRC_NONE = 0, SRC_ROWS, SRC_PACKED, SRC_PLANES };
 // With few tokens the layer is a weight stream whose time follows the
 // bytes read, so AUTO reads the top b planes there (App. G.2: only the
 // surviving planes are fetched).  Measured on the 112-layer PixArt-shaped
-// schedule at M = 16 (ms per denoising step, TASQ table of mean 4.94 bits /
-// static b = 8): planes 0.083 / 0.112, packed int8 0.105 / 0.105, int8 rows
-// 0.126 / 0.121.  The plane stream wins at every b below 8; at b = 8 it reads
-// as many bytes as the int8 copy and the packed stream is 6% faster, so
-// there AUTO prefers the packed copy when one is given.  For M in the
+// schedule (ms per denoising step, TASQ table of mean 4.94 bits / static
+// b = 8): at M = 16 planes 0.058 / 0.093, packed int8 0.095 / 0.095, int8
+// rows 0.108 / 0.101; at M = 32 planes 0.088 / 0.117, packed 0.111 / 0.111;
+// at M = 64 planes 0.152 / 0.169, packed 0.181 / 0.181.  The plane stream
+// wins at every b below 8; at b = 8 it reads as many bytes as the int8 copy
+// and the two streams are within 7% of each other either way, so there AUTO
+// keeps the packed copy when one is given.  For M in the
 // thousands the weights are a few percent of the traffic and rebuilding the
 // bytes from planes per output tile costs more than it saves, so AUTO takes
 // the int8 copies, and the bit-plane GEMM only when no other copy is given.
