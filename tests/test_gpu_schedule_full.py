@@ -138,6 +138,52 @@ def test_config4_comparison_tables_and_packed_weights_sampled(cfg4):
                     f"config 4 packed weights layer {l} b={b}")
 
 
+@pytest.mark.parametrize("source", ["rows", "packed", "planes", "auto"])
+def test_config4_weight_streaming_schedule_m16_sampled(cfg4, source):
+    """The benchmark's weight-streaming schedule at full size: config 4's 112
+    layers at 16 tokens (the first 16 activation rows, as bench.py draws
+    them), one grouped weight-streaming launch per step, the weight read as
+    int8 rows, as the packed copy, as the top b planes, or under AUTO with
+    all three copies given (the planes below b = 8).  After steps 18-19 every
+    layer holds the last step's output: all 16 rows of 40 sampled columns
+    (and the last) per layer against the oracle, fp32 within 1e-6 relative
+    and the int32 accumulators bit-exactly."""
+    wl, table, Ws, sws, keep = cfg4
+    L, M = len(wl.layers), 16
+    rng = np.random.default_rng(61)
+    hold, layers, outs = [], [], []
+    for l, spec in enumerate(wl.layers):
+        X = inputs.x_rows(wl, l, np.arange(M), device=DEV)
+        W = keep[l][1]
+        P = T.pack_weights(W) if source in ("packed", "auto") else None
+        Q = T.pack_planes(W) if source in ("planes", "auto") else None
+        y = torch.full((M, spec.N), -7.0, dtype=torch.float32, device=DEV)
+        acc = torch.full((M, spec.N), 12345, dtype=torch.int32, device=DEV)
+        Wuse = W if source in ("rows", "auto") else None
+        layers.append(T.make_layer(X, Wuse, wl.sx, keep[l][2], None, acc, y, packed=P, planes=Q))
+        hold += [X, P, Q]
+        outs.append((acc, y))
+    variant = T.VARIANT_BITPLANE if source == "planes" else T.VARIANT_AUTO
+    ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
+    T.run_schedule(layers, table, wl.S, wl.T, wl.T - 2, wl.T, workspace=ws, variant=variant)
+    torch.cuda.synchronize()
+    stage = oracle.stage_of_step(wl.T - 1, wl.S, wl.T)
+    sx = f32(wl.sx)
+    for l, spec in enumerate(wl.layers):
+        b = int(table[l, stage])
+        cols = np.array(sorted(set(rng.integers(0, spec.N, 40).tolist() + [spec.N - 1])),
+                        np.int64)
+        Xr = inputs.x_rows(wl, l, np.arange(M))
+        tc = torch.as_tensor(cols)
+        rr = np.repeat(np.arange(M), len(cols))
+        cc = np.tile(np.arange(len(cols)), M)
+        ra, ry = oracle.masked_linear_entries(Xr, Ws[l][tc], sx, sws[l][tc], b, rr, cc)
+        acc, y = outs[l]
+        check_outputs(acc[:, tc].cpu(), y[:, tc].cpu(), ra.reshape(M, len(cols)),
+                      ry.reshape(M, len(cols)), sx, sws[l][tc], None,
+                      f"config 4 at 16 tokens, {source}, layer {l} b={b}")
+
+
 @pytest.mark.parametrize("cfg", [1, 2, 3])
 def test_block_schedules_full_size_sampled(cfg):
     """Configs 1-3 as full-size schedules through tasq_run_schedule with a
