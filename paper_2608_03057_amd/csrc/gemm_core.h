@@ -872,7 +872,7 @@ __device__ __forceinline__ void unit_coords(const LayerDesc &d, int t, int &m0, 
 
 template <class C>
 __global__ void __launch_bounds__(C::NT, C::OCC)
-k_masked_gemm_persistent(const LayerDesc *__restrict__ descs, int L, int total,
+k_masked_gemm_persistent(const LayerDesc *__restrict__ descs, int L, int total, XcdRuns runs,
                          const uint8_t *__restrict__ table, int S, int stage, int parties)
 {
     __shared__ v4i smA[C::SMA];
@@ -888,8 +888,7 @@ k_masked_gemm_persistent(const LayerDesc *__restrict__ descs, int L, int total,
     const int wgs = gridDim.x / NX / parties;       // workgroups per part
     const int x = blockIdx.x % NX, j = blockIdx.x / NX;
     const int part = j % parties, jj = j / parties;
-    const int span = (total + NX - 1) / NX;
-    const int xbeg = x * span, xend = min(total, xbeg + span);
+    const int xbeg = runs.begin[x], xend = runs.begin[x + 1];
     const int pspan = (xend - xbeg + parties - 1) / parties;
     const int ubeg = xbeg + part * pspan;
     const int uend = min(xend, ubeg + pspan);
@@ -1082,14 +1081,15 @@ hipError_t launch_grouped_cfg(const LayerDesc *d_descs, int L, int total_tiles,
 // each of the 8 XCDs.
 template <class C>
 hipError_t launch_persistent_cfg(const LayerDesc *d_descs, int L, int total_tiles,
-                                 const uint8_t *d_table, int S, int stage, int wgs_per_xcd,
-                                 int parties, hipStream_t stream)
+                                 const XcdRuns &runs, const uint8_t *d_table, int S, int stage,
+                                 int wgs_per_xcd, int parties, hipStream_t stream)
 {
-    if (wgs_per_xcd < 1 || total_tiles < 1 || parties < 1 || wgs_per_xcd % parties != 0)
+    if (wgs_per_xcd < 1 || total_tiles < 1 || parties < 1 || wgs_per_xcd % parties != 0 ||
+        !xcd_runs_valid(runs, total_tiles))
         return hipErrorInvalidValue;
     dim3 g((unsigned)(8 * wgs_per_xcd)), b(C::NT);
     hipLaunchKernelGGL((k_masked_gemm_persistent<C>), g, b, 0, stream, d_descs, L, total_tiles,
-                       d_table, S, stage, parties);
+                       runs, d_table, S, stage, parties);
     return hipGetLastError();
 }
 

@@ -210,7 +210,7 @@ __device__ __forceinline__ void cols_finish(const LayerDesc &d, int m0, int n0,
 // boundary, so the slots need not rotate across tiles).
 template <class C>
 __global__ void __launch_bounds__(C::NT, C::OCC)
-k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int total,
+k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int total, XcdRuns runs,
                             const uint8_t *__restrict__ table, int S, int stage, int parties)
 {
     using Ops = PersOperands<C>;
@@ -227,8 +227,7 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
     const int wgs = gridDim.x / NX / parties;
     const int x = blockIdx.x % NX, j = blockIdx.x / NX;
     const int part = j % parties, jj = j / parties;
-    const int span = (total + NX - 1) / NX;
-    const int xbeg = x * span, xend = min(total, xbeg + span);
+    const int xbeg = runs.begin[x], xend = runs.begin[x + 1];
     const int pspan = (xend - xbeg + parties - 1) / parties;
     const int ubeg = xbeg + part * pspan;
     const int uend = min(xend, ubeg + pspan);
@@ -427,14 +426,15 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
 
 template <class C>
 hipError_t launch_persistent_ds_cfg(const LayerDesc *d_descs, int L, int total_tiles,
-                                    const uint8_t *d_table, int S, int stage, int wgs_per_xcd,
-                                    int parties, hipStream_t stream)
+                                    const XcdRuns &runs, const uint8_t *d_table, int S, int stage,
+                                    int wgs_per_xcd, int parties, hipStream_t stream)
 {
-    if (wgs_per_xcd < 1 || total_tiles < 1 || parties < 1 || wgs_per_xcd % parties != 0)
+    if (wgs_per_xcd < 1 || total_tiles < 1 || parties < 1 || wgs_per_xcd % parties != 0 ||
+        !xcd_runs_valid(runs, total_tiles))
         return hipErrorInvalidValue;
     dim3 g((unsigned)(8 * wgs_per_xcd)), b(C::NT);
     hipLaunchKernelGGL((k_masked_gemm_persistent_ds<C>), g, b, 0, stream, d_descs, L,
-                       total_tiles, d_table, S, stage, parties);
+                       total_tiles, runs, d_table, S, stage, parties);
     return hipGetLastError();
 }
 

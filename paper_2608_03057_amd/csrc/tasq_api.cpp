@@ -26,6 +26,46 @@ constexpr int kXcds = 8;
 constexpr int kComputeUnits = 256;
 constexpr double kImbalanceLimit = 1.10;
 
+// Cost of a 256x256 tile of the persistent step in bytes of K: its K plus a
+// fixed part for its epilogue and the next tile's prologue.  The 28-block
+// PixArt-shaped step (4.13 ms, 147 tiles per compute unit, 12.2 K tiles of
+// 128 each on average) spends about 0.66 ms in tile ends, 4.5 us per tile,
+// against 1.9 us per K tile: about 300 bytes of K.
+constexpr double kTileFixedK = 384.0;
+
+// The XCD runs of a persistent launch: contiguous in the work-unit order
+// (neighbouring tiles share operands in one L2) and cut at about equal cost,
+// a tile costing its K plus kTileFixedK.  Equal counts of tiles would give
+// the XCD whose run ends a block later in the 28-block PixArt-shaped step
+// (more 4608-deep tiles) 3% more work than the mean.
+tasq::XcdRuns cost_runs(const std::vector<LayerDesc> &segs, long long total)
+{
+    double all = 0;
+    for (const LayerDesc &d : segs)
+        all += (double)d.tiles_m * d.tiles_n * ((double)d.K + kTileFixedK);
+    tasq::XcdRuns r = {};
+    int x = 1;
+    double cum = 0;
+    for (const LayerDesc &d : segs) {
+        const long long n = (long long)d.tiles_m * d.tiles_n;
+        const double c = (double)d.K + kTileFixedK;
+        while (x < kXcds && cum + (double)n * c >= all * x / kXcds) {
+            long long take = (long long)((all * x / kXcds - cum) / c + 0.5);
+            take = take < 0 ? 0 : take > n ? n : take;
+            r.begin[x] = (int)(d.tile_begin + take);
+            ++x;
+        }
+        cum += (double)n * c;
+    }
+    for (; x < kXcds; ++x)
+        r.begin[x] = (int)total;
+    r.begin[kXcds] = (int)total;
+    for (int i = 1; i <= kXcds; ++i)
+        if (r.begin[i] < r.begin[i - 1])
+            r.begin[i] = r.begin[i - 1];
+    return r;
+}
+
 // Heaviest XCD run over the mean, for the per-layer tile order, a tile
 // costing about its K plus a fixed part for loading and writing the tile.
 double xcd_imbalance(const std::vector<LayerDesc> &descs, long long G)
@@ -1084,8 +1124,9 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
         tasq::TileShape ts = {32, 32, 128};
         hipError_t (*launch_step)(const LayerDesc *, int, int, const uint8_t *, int, int, bool,
                                   hipStream_t) = nullptr;
-        hipError_t (*launch_persistent)(const LayerDesc *, int, int, const uint8_t *, int, int,
-                                        int, int, hipStream_t) = nullptr;
+        hipError_t (*launch_persistent)(const LayerDesc *, int, int, const tasq::XcdRuns &,
+                                        const uint8_t *, int, int, int, int,
+                                        hipStream_t) = nullptr;
         bool big_tile = false;      // the 256x256 tile, which AUTO runs persistent
         bool extras = false;
         for (int l = 0; l < LG; ++l)
@@ -1128,12 +1169,16 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
         const int wgs_per_xcd = persistent_wgs_per_xcd(opts);
         const int parties = persistent_parties(opts, wgs_per_xcd);
         // The GEMM kernels give each XCD one contiguous run of the work
-        // units (for L2 locality), equal in count.  When the layers' tiles
-        // differ in cost (K) and the layer order leaves one run much heavier
-        // than the others, every layer is cut into kXcds rounds instead, so
-        // that each run holds about an eighth of every layer.
+        // units (for L2 locality): the persistent launch runs of about equal
+        // cost (cost_runs), the one-workgroup-per-tile launches runs equal in
+        // count.  For the latter, when the layers' tiles differ in cost (K)
+        // and the layer order leaves one run much heavier than the others,
+        // every layer is cut into kXcds rounds instead, so that each run
+        // holds about an eighth of every layer (measured slower than
+        // contiguous runs for the persistent step: 4.27 against 4.15 ms).
         std::vector<LayerDesc> segs;
-        if (!all_skinny && xcd_imbalance(descs, total) > kImbalanceLimit) {
+        if (!all_skinny && !launch_persistent &&
+            xcd_imbalance(descs, total) > kImbalanceLimit) {
             segs.reserve((size_t)LG * kXcds);
             long long begin = 0;
             for (int r = 0; r < kXcds; ++r)
@@ -1152,6 +1197,7 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
             segs = descs;
         }
         const int nseg = (int)segs.size();
+        const tasq::XcdRuns runs = cost_runs(segs, total);
         LayerDesc *d_descs = reinterpret_cast<LayerDesc *>(ws);
         uint8_t *d_table = reinterpret_cast<uint8_t *>(
             ws + round_up((size_t)L * kXcds * sizeof(LayerDesc), kWsAlign));
@@ -1191,8 +1237,8 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
                 all_skinny ? tasq::launch_skinny_grouped(d_descs, nseg, (int)total, max_m, src,
                                                          d_table, S, s, st)
                 : launch_persistent
-                    ? launch_persistent(d_descs, nseg, (int)total, d_table, S, s, wgs_per_xcd,
-                                        parties, st)
+                    ? launch_persistent(d_descs, nseg, (int)total, runs, d_table, S, s,
+                                        wgs_per_xcd, parties, st)
                     : launch_step(d_descs, nseg, (int)total, d_table, S, s, any_conv, st);
             if (e != hipSuccess)
                 return TASQ_ERR_HIP;

@@ -51,6 +51,23 @@ struct TileShape {
     int bm, bn, bk;
 };
 
+// First work unit of each XCD's run in a persistent launch: XCD x walks
+// units begin[x] .. begin[x + 1] - 1 (begin[0] = 0, begin[8] = total).
+struct XcdRuns {
+    int begin[9];
+};
+
+// begin[0] = 0, begin[8] = total and non-decreasing in between.
+inline bool xcd_runs_valid(const XcdRuns &r, int total)
+{
+    if (r.begin[0] != 0 || r.begin[8] != total)
+        return false;
+    for (int x = 0; x < 8; ++x)
+        if (r.begin[x + 1] < r.begin[x])
+            return false;
+    return true;
+}
+
 // Launchers of one tile configuration (one translation unit each).
 struct TileOps {
     TileShape shape;
@@ -65,11 +82,11 @@ struct TileOps {
     hipError_t (*split)(const LayerDesc &d, int32_t *part, int splits, int kchunk,
                         hipStream_t stream);
     // Persistent form of grouped over linear layers only: wgs_per_xcd
-    // workgroups per XCD walk the XCD's run of work units, cut into
+    // workgroups per XCD walk the XCD's run of work units (runs), cut into
     // `parties` parts walked side by side (wgs_per_xcd % parties == 0).
     hipError_t (*persistent)(const LayerDesc *d_descs, int L, int total_tiles,
-                             const uint8_t *d_table, int S, int stage, int wgs_per_xcd,
-                             int parties, hipStream_t stream);
+                             const XcdRuns &runs, const uint8_t *d_table, int S, int stage,
+                             int wgs_per_xcd, int parties, hipStream_t stream);
 };
 
 // Sums split-K partials and applies the dequantisation epilogue (splitk.hip).
@@ -98,8 +115,8 @@ struct PackedTileOps {
     // Persistent grouped step (linear layers, no low-rank or weight-zero-
     // point terms), or null for tiles without one.
     hipError_t (*persistent)(const LayerDesc *d_descs, int L, int total_tiles,
-                             const uint8_t *d_table, int S, int stage, int wgs_per_xcd,
-                             int parties, hipStream_t stream);
+                             const XcdRuns &runs, const uint8_t *d_table, int S, int stage,
+                             int wgs_per_xcd, int parties, hipStream_t stream);
 };
 
 enum PackedTileId : int {
