@@ -148,10 +148,11 @@ enum {
  *   tile            t + 1 forces staged-weight tile TASQ_TILE_* t (single
  *                   calls, split-K and grouped schedule steps).
  *   packed_tile     t + 1 forces packed-weight tile TASQ_PTILE_* t.
- *   persistent      grouped schedule steps over linear layers without
- *                   low-rank or weight-zero-point terms: 1 = one workgroup
- *                   per output tile, 2 = the persistent launch (one
- *                   workgroup per compute unit walking a run of tiles),
+ *   persistent      grouped schedule steps over linear layers (with
+ *                   low-rank or weight-zero-point terms only on row-major
+ *                   weights and the TASQ_TILE_256x256_K128_W8 tile): 1 = one
+ *                   workgroup per output tile, 2 = the persistent launch
+ *                   (one workgroup per compute unit walking a run of tiles),
  *                   whatever the tile and the tile count.
  *   persistent_wgs  workgroups per XCD of the persistent launch (1..1024;
  *                   0 = one per compute unit, 32).

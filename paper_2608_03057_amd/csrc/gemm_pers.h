@@ -46,6 +46,14 @@ __device__ __forceinline__ void wait_vm_lgkm0()
     __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
 }
 
+// s_waitcnt lgkmcnt(0) alone (vmcnt and expcnt fields at their maxima): this
+// wave's LDS reads and writes are done, its global requests may still be in
+// flight.
+__device__ __forceinline__ void wait_lgkm0()
+{
+    __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));
+}
+
 // Workgroup barrier with no implied waits (the caller has issued them); the
 // memory clobber keeps LDS accesses on their side of it.
 __device__ __forceinline__ void barrier()
@@ -150,12 +158,12 @@ struct PersOperands {
 // the point of issue.
 template <class C>
 struct ColLoads {
-    float sw[C::FN], bias[C::FN];
+    float sw[C::FN], bias[C::FN], wz[C::FN];
     int cs[C::FN];
     float alpha, zx;
 };
 
-template <class C>
+template <class C, bool EXTRAS = false>
 __device__ __forceinline__ void cols_request(const LayerDesc &d, int n0, int bits,
                                              ColLoads<C> &cl)
 {
@@ -178,10 +186,17 @@ __device__ __forceinline__ void cols_request(const LayerDesc &d, int n0, int bit
             __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rbias, on, 0, 0));
         cl.cs[j] = (int)__builtin_amdgcn_raw_buffer_load_b32(
             rcs, nok ? ((uint32_t)(bits - 1) * (uint32_t)d.N + (uint32_t)n) * 4u : kOOB, 0, 0);
+        cl.wz[j] = 0.f;
+        if constexpr (EXTRAS) {
+            // weight zero points z_n, read only when the epilogue adds their term
+            const rsrc_t rwz = make_rsrc(d.wz, d.wz && d.y ? nb : 0u);
+            cl.wz[j] =
+                __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rwz, on, 0, 0));
+        }
     }
 }
 
-template <class C>
+template <class C, bool EXTRAS = false>
 __device__ __forceinline__ void cols_finish(const LayerDesc &d, int m0, int n0,
                                             const ColLoads<C> &cl, EpiCols<C> &ec)
 {
@@ -197,7 +212,8 @@ __device__ __forceinline__ void cols_finish(const LayerDesc &d, int m0, int n0,
         ec.scale[j] = (asym ? cl.alpha : d.sx) * cl.sw[j];
         ec.bias[j] = cl.bias[j];
         ec.corr[j] = asym ? (128.0f - cl.zx) * (float)cl.cs[j] : 0.0f;
-        ec.wsc[j] = 0.f;
+        // (128 - z_n) times the column scale: the weight zero point's term
+        ec.wsc[j] = EXTRAS && d.wz && d.y ? (128.0f - cl.wz[j]) * ec.scale[j] : 0.f;
         ec.base[j] = nok ? ((uint32_t)mrow * (uint32_t)d.N + (uint32_t)n) * 4u : kOOB;
     }
 }
@@ -208,7 +224,7 @@ __device__ __forceinline__ void cols_finish(const LayerDesc &d, int m0, int n0,
 // and weight stage (g0+t) % 2; weight K tile t sits in register slot t % 2
 // from its load until its LDS store (both slots are empty at a tile
 // boundary, so the slots need not rotate across tiles).
-template <class C>
+template <class C, bool EXTRAS>
 __global__ void __launch_bounds__(C::NT, C::OCC)
 k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int total, XcdRuns runs,
                             const uint8_t *__restrict__ table, int S, int stage, int parties)
@@ -383,7 +399,7 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
         // before the last barrier; the register slots hold only the requests
         // past K.
         ColLoads<C> cl;
-        cols_request<C>(d, n0, bits, cl);
+        cols_request<C, EXTRAS>(d, n0, bits, cl);
         const LayerDesc &dc = d;
         const int mc = m0, nc = n0;
         const int g1 = g0 + nk;
@@ -414,8 +430,32 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
         }
         __builtin_amdgcn_sched_barrier(0);
         EpiCols<C> ec;
-        cols_finish<C>(dc, mc, nc, cl, ec);
-        epilogue_write<C, true, false>(dc, acc, ec, reinterpret_cast<const char *>(sm));
+        cols_finish<C, EXTRAS>(dc, mc, nc, cl, ec);
+        // The low-rank and weight-zero-point operands of the tile are staged
+        // in the weight stages, idle from the last K tile's final LDS reads
+        // (every wave's, after the first barrier) until the next tile's
+        // prologue stores its weight K tile 0 (after the last barrier).
+        bool staged = false;
+        if constexpr (EXTRAS) {
+            const bool lowrank = dc.lr_T != nullptr && dc.y != nullptr;
+            const bool wzero = dc.wz != nullptr && dc.y != nullptr;
+            staged = lowrank || wzero;
+            if (staged) {
+                pers::wait_lgkm0();
+                pers::barrier();
+                if (lowrank)
+                    stage_lowrank<C>(dc, mc, nc, smB);
+                if (wzero)
+                    stage_rowsums<C>(dc, mc, smB);
+                pers::wait_lgkm0();
+                pers::barrier();
+            }
+        }
+        epilogue_write<C, true, EXTRAS>(dc, acc, ec, smB);
+        if (staged) {
+            pers::wait_lgkm0();
+            pers::barrier();
+        }
         __builtin_amdgcn_sched_barrier(0);
         if (!more)
             break;
@@ -424,7 +464,7 @@ k_masked_gemm_persistent_ds(const LayerDesc *__restrict__ descs, int L, int tota
     }
 }
 
-template <class C>
+template <class C, bool EXTRAS>
 hipError_t launch_persistent_ds_cfg(const LayerDesc *d_descs, int L, int total_tiles,
                                     const XcdRuns &runs, const uint8_t *d_table, int S, int stage,
                                     int wgs_per_xcd, int parties, hipStream_t stream)
@@ -433,7 +473,7 @@ hipError_t launch_persistent_ds_cfg(const LayerDesc *d_descs, int L, int total_t
         !xcd_runs_valid(runs, total_tiles))
         return hipErrorInvalidValue;
     dim3 g((unsigned)(8 * wgs_per_xcd)), b(C::NT);
-    hipLaunchKernelGGL((k_masked_gemm_persistent_ds<C>), g, b, 0, stream, d_descs, L,
+    hipLaunchKernelGGL((k_masked_gemm_persistent_ds<C, EXTRAS>), g, b, 0, stream, d_descs, L,
                        total_tiles, runs, d_table, S, stage, parties);
     return hipGetLastError();
 }
@@ -444,7 +484,8 @@ hipError_t launch_persistent_ds_cfg(const LayerDesc *d_descs, int L, int total_t
         static const TileOps ops = {{CFG::BM, CFG::BN, CFG::BK}, &launch_single_cfg<CFG>,   \
                                     &launch_planes_cfg<CFG>, &launch_grouped_cfg<CFG>,      \
                                     &launch_split_cfg<CFG>,                                 \
-                                    &launch_persistent_ds_cfg<CFG>};                        \
+                                    &launch_persistent_ds_cfg<CFG, false>,                  \
+                                    &launch_persistent_ds_cfg<CFG, true>};                  \
         return ops;                                                                         \
     }
 

@@ -1147,8 +1147,8 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
             const tasq::TileOps &ops = tasq::tile_ops(tile);
             ts = ops.shape;
             launch_step = ops.grouped;
-            if (!any_conv && !extras)
-                launch_persistent = ops.persistent;
+            if (!any_conv)
+                launch_persistent = extras ? ops.persistent_extras : ops.persistent;
             big_tile = tile == tasq::TILE_256x256_K128_W8_PF1;
         }
         long long total = 0;

@@ -87,6 +87,11 @@ struct TileOps {
     hipError_t (*persistent)(const LayerDesc *d_descs, int L, int total_tiles,
                              const XcdRuns &runs, const uint8_t *d_table, int S, int stage,
                              int wgs_per_xcd, int parties, hipStream_t stream);
+    // The same with the low-rank and weight-zero-point epilogue terms, or
+    // null for tiles without one.
+    hipError_t (*persistent_extras)(const LayerDesc *d_descs, int L, int total_tiles,
+                                    const XcdRuns &runs, const uint8_t *d_table, int S,
+                                    int stage, int wgs_per_xcd, int parties, hipStream_t stream);
 };
 
 // Sums split-K partials and applies the dequantisation epilogue (splitk.hip).

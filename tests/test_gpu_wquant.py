@@ -188,7 +188,7 @@ def test_quantized_weights_full_size_sampled(cfg, l):
         del acc, y
 
 
-@pytest.mark.parametrize("mode", ["per_layer", "grouped", "skinny", "packed"])
+@pytest.mark.parametrize("mode", ["per_layer", "grouped", "persistent", "skinny", "packed"])
 def test_quantized_weights_schedule(mode):
     if mode == "skinny":
         shapes = [(16, 1152, 1152), (64, 130, 528), (33, 257, 304)]
@@ -221,7 +221,10 @@ def test_quantized_weights_schedule(mode):
     if mode != "per_layer":
         ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
     for (t0, t1) in [(0, 20), (0, 1), (6, 7), (14, 20)]:
-        T.run_schedule(layers, table, S_, Tn, t0, t1, workspace=ws)
+        # persistent: the one-workgroup-per-CU step with its epilogue operands
+        # staged in the weight stages (forced on, 256x256 tiles)
+        tune = dict(persistent=2, tile=1) if mode == "persistent" else None
+        T.run_schedule(layers, table, S_, Tn, t0, t1, workspace=ws, tune=tune)
         torch.cuda.synchronize()
         stage = oracle.stage_of_step(t1 - 1, S_, Tn)
         for i, h in enumerate(host):
