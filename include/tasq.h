@@ -386,6 +386,33 @@ int tasq_weight_colsums(const int8_t *W, int N, int K, int32_t *colsums_out, voi
 int tasq_quantize_weights(const float *W, int N, int K, int8_t *W_out, float *alpha_out,
                           float *z_out, float *sw_out, void *stream);
 
+/* One weight of tasq_quantize_weights_batch: the arguments of one
+ * tasq_quantize_weights call. */
+typedef struct tasq_weight_job {
+    const float *W;         /* fp32 [N][K] device */
+    int32_t N, K;
+    int8_t *W_out;          /* int8 [N][K] device */
+    float *alpha_out, *z_out, *sw_out;  /* fp32 [N] device */
+} tasq_weight_job;
+
+/*
+ * The quantizer of tasq_quantize_weights (App. A.1.1) over n weights, e.g.
+ * every layer of a model, in one launch per 16 weights instead of one per
+ * weight: the rows of up to 16 weights share a launch.  Every job's codes,
+ * alpha, z and sw equal those of a tasq_quantize_weights call on it.
+ *   jobs    host array of n jobs, read during the call only; each as the
+ *           arguments of tasq_quantize_weights.  Jobs with N == 0 are
+ *           skipped.  No two jobs may share an alpha_out buffer
+ *           (TASQ_ERR_RANGE); other overlaps of outputs with inputs or
+ *           each other are the caller's error.
+ *   n       number of jobs, >= 0 (TASQ_ERR_RANGE otherwise); n == 0
+ *           enqueues nothing.
+ * Every job is validated before anything is enqueued (TASQ_ERR_NULL, _DIM,
+ * _OVERFLOW, _ALIGN as for the single call).  Asynchronous on `stream`;
+ * allocates nothing on the device.
+ */
+int tasq_quantize_weights_batch(const tasq_weight_job *jobs, int n, void *stream);
+
 /*
  * Row sums of int8 activation codes, out[m] = sum_k X[m][k] (int32 [M]),
  * the x_rowsums that a weight zero point needs.  M == 0 enqueues nothing.

@@ -10,7 +10,7 @@ from .api import (  # noqa: F401
     masked_linear, masked_conv3x3, pack_planes, planes_bytes, pack_weights, packed_weight_bytes,
     quantize_activations, quantize_activations_batch, quantize_activations_lowrank,
     lowrank_down, weight_colsums,
-    quantize_weights, row_sums, schedule_cost,
+    quantize_weights, quantize_weights_batch, row_sums, schedule_cost,
     stage_of_step, run_schedule, run_schedule_noalloc, schedule_workspace_bytes,
     workspace_bytes, make_layer, status_string,
 )

@@ -41,7 +41,7 @@ KIND_CONV3X3 = 1
 EXPORTS = (
     "tasq_masked_linear", "tasq_masked_conv3x3", "tasq_pack_planes", "tasq_planes_bytes",
     "tasq_pack_weights", "tasq_packed_weight_bytes", "tasq_quantize_activations",
-    "tasq_quantize_activations_batch",
+    "tasq_quantize_activations_batch", "tasq_quantize_weights_batch",
     "tasq_weight_colsums", "tasq_lowrank_down", "tasq_quantize_activations_lowrank",
     "tasq_quantize_weights", "tasq_row_sums", "tasq_schedule_cost",
     "tasq_stage_of_step", "tasq_run_schedule", "tasq_run_schedule_noalloc",
@@ -91,6 +91,12 @@ class ActJob(ctypes.Structure):
                 ("X_out", ctypes.c_void_p), ("act_params", ctypes.c_void_p)]
 
 
+class WeightJob(ctypes.Structure):
+    _fields_ = [("W", ctypes.c_void_p), ("N", ctypes.c_int32), ("K", ctypes.c_int32),
+                ("W_out", ctypes.c_void_p), ("alpha_out", ctypes.c_void_p),
+                ("z_out", ctypes.c_void_p), ("sw_out", ctypes.c_void_p)]
+
+
 class TasqError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -125,6 +131,8 @@ def lib() -> ctypes.CDLL:
         L.tasq_quantize_activations.restype = i32
         L.tasq_quantize_activations_batch.argtypes = [ctypes.POINTER(ActJob), i32, vp]
         L.tasq_quantize_activations_batch.restype = i32
+        L.tasq_quantize_weights_batch.argtypes = [ctypes.POINTER(WeightJob), i32, vp]
+        L.tasq_quantize_weights_batch.restype = i32
         L.tasq_weight_colsums.argtypes = [vp, i32, i32, vp, vp]
         L.tasq_weight_colsums.restype = i32
         L.tasq_schedule_cost.argtypes = [vp, i32, vp, i32, i32, i32, i32, i32, vp]

@@ -184,6 +184,36 @@ def quantize_weights(W: torch.Tensor):
     return Q, alpha, z, sw
 
 
+def quantize_weights_batch(Ws, outs=None):
+    """quantize_weights over a list of fp32 weights in one launch per 16
+    (App. A.1.1): returns one (codes, alpha, z, sw) tuple per weight, each
+    equal to what quantize_weights gives for it.  ``outs``: such tuples to
+    write into (allocated here when None)."""
+    Ws = list(Ws)
+    n = len(Ws)
+    jobs = (_lib.WeightJob * max(n, 1))()
+    if outs is None:
+        outs = [None] * n
+    outs = list(outs)
+    if len(outs) != n:
+        raise ValueError("Ws and outs differ in length")
+    for j, W in enumerate(Ws):
+        N = W.shape[0]
+        K = W.numel() // N if N else 0
+        _need(W, torch.float32, tuple(W.shape), "W")
+        if outs[j] is None:
+            outs[j] = (torch.empty(W.shape, dtype=torch.int8, device=W.device),
+                       *(torch.empty(N, dtype=torch.float32, device=W.device) for _ in range(3)))
+        Q, alpha, z, sw = outs[j]
+        _need(Q, torch.int8, tuple(W.shape), "codes")
+        for t, name in ((alpha, "alpha"), (z, "z"), (sw, "sw")):
+            _need(t, torch.float32, (N,), name)
+        jobs[j] = _lib.WeightJob(_ptr(W), N, K, _ptr(Q), _ptr(alpha), _ptr(z), _ptr(sw))
+    check(_lib.lib().tasq_quantize_weights_batch(jobs, n, _stream()),
+          "tasq_quantize_weights_batch")
+    return outs
+
+
 def row_sums(X: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """int32 [M]: sum_k X[m, k] of int8 codes X [M, K]."""
     M = X.shape[0]

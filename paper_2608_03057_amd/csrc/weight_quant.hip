@@ -14,25 +14,45 @@
 //
 // Also the row sums of int8 activation codes, which the weight zero point
 // needs: sum_k x_hat w_hat_b = sw (sum_k x_hat W_b + (128 - z) sum_k x_hat).
+#include "tasq.h"
 #include "tasq_internal.h"
+
+#include <algorithm>
+#include <vector>
 
 namespace tasq {
 
 namespace {
 
-// One wave per output channel: range, then codes; lane 0 writes the
-// channel's alpha, z and sw.  vec: W rows 16-byte aligned (K % 4 == 0 and
-// W aligned) and Q rows 4-byte aligned.
-__global__ void __launch_bounds__(256) k_weight_quantize(const float *__restrict__ W, int N, int K,
-                                                         int8_t *__restrict__ Q,
-                                                         float *__restrict__ alpha_out,
-                                                         float *__restrict__ z_out,
-                                                         float *__restrict__ sw_out, bool vec)
+// fp32 code decision of value v (the order written in the header comment).
+__device__ __forceinline__ int8_t weight_code(float v, float alpha, float z)
+{
+    float f = floorf(__fadd_rn(__fdiv_rn(v, alpha), z));
+    f = fminf(fmaxf(f, 0.0f), 255.0f);
+    return (int8_t)((int)f - 128);
+}
+
+__device__ __forceinline__ void range_to_scale(float mn, float mx, float &alpha, float &z)
+{
+    if (mx == mn) {
+        alpha = 1.0f;
+        z = -mn;
+    } else {
+        alpha = __fdiv_rn(mx - mn, 256.0f);
+        z = __fdiv_rn(-mn, alpha);
+    }
+}
+
+// Output channel n of one weight, by one wave: range, then codes (the row
+// read a second time, from L2); lane 0 writes the channel's alpha, z and
+// sw.  vec: W rows 16-byte aligned (K % 4 == 0 and W aligned) and Q rows
+// 4-byte aligned.
+__device__ __forceinline__ void quantize_row(const float *__restrict__ W, int K,
+                                             int8_t *__restrict__ Q, float *__restrict__ alpha_out,
+                                             float *__restrict__ z_out,
+                                             float *__restrict__ sw_out, bool vec, long long n)
 {
     const int lane = threadIdx.x & 63;
-    const long long n = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (n >= N)
-        return;
     const float *w = W + n * (long long)K;
     int8_t *q = Q + n * (long long)K;
     float mn = __builtin_huge_valf(), mx = -__builtin_huge_valf();
@@ -52,18 +72,8 @@ __global__ void __launch_bounds__(256) k_weight_quantize(const float *__restrict
         mx = fmaxf(mx, __shfl_xor(mx, off));
     }
     float alpha, z;
-    if (mx == mn) {
-        alpha = 1.0f;
-        z = -mn;
-    } else {
-        alpha = __fdiv_rn(mx - mn, 256.0f);
-        z = __fdiv_rn(-mn, alpha);
-    }
-    auto code = [&](float v) -> int8_t {
-        float f = floorf(__fadd_rn(__fdiv_rn(v, alpha), z));
-        f = fminf(fmaxf(f, 0.0f), 255.0f);
-        return (int8_t)((int)f - 128);
-    };
+    range_to_scale(mn, mx, alpha, z);
+    auto code = [&](float v) -> int8_t { return weight_code(v, alpha, z); };
     char4 *q4 = reinterpret_cast<char4 *>(q);
     for (int i = lane; i < K4; i += 64) {
         const float4 v = w4[i];
@@ -76,6 +86,49 @@ __global__ void __launch_bounds__(256) k_weight_quantize(const float *__restrict
         z_out[n] = z;
         sw_out[n] = __fdiv_rn(alpha * 256.0f, 255.0f);
     }
+}
+
+// One wave per output channel of one weight.
+__global__ void __launch_bounds__(256) k_weight_quantize(const float *__restrict__ W, int N, int K,
+                                                         int8_t *__restrict__ Q,
+                                                         float *__restrict__ alpha_out,
+                                                         float *__restrict__ z_out,
+                                                         float *__restrict__ sw_out, bool vec)
+{
+    const long long n = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (n >= N)
+        return;
+    quantize_row(W, K, Q, alpha_out, z_out, sw_out, vec, n);
+}
+
+// Up to 16 weights per launch, travelling by value: the launch's rows are
+// the weights' rows end to end, one wave per row (first: the task's first
+// row in the launch).
+struct WeightTask {
+    const float *W;
+    int8_t *Q;
+    float *alpha, *z, *sw;
+    long long first;
+    int N, K;
+    int vec;
+};
+constexpr int kWeightBatchTasks = 16;
+struct WeightLaunch {
+    WeightTask t[kWeightBatchTasks];
+    int ntasks;
+};
+
+__global__ void __launch_bounds__(256) k_weight_quantize_batch(WeightLaunch L)
+{
+    const long long g = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    int j = 0;
+    while (j + 1 < L.ntasks && g >= L.t[j + 1].first)
+        ++j;
+    const WeightTask &t = L.t[j];
+    const long long n = g - t.first;
+    if (n < 0 || n >= t.N)
+        return;
+    quantize_row(t.W, t.K, t.Q, t.alpha, t.z, t.sw, t.vec != 0, n);
 }
 
 // One wave per row: sum_k X[m][k] of int8 codes, exact in int32 for
@@ -115,6 +168,36 @@ hipError_t launch_quantize_weights(const float *W, int N, int K, int8_t *Q, floa
     return hipGetLastError();
 }
 
+// Weights of the batch, up to 16 per launch (validated by the caller).
+hipError_t launch_quantize_weights_batch(const tasq_weight_job *jobs, int n, hipStream_t stream)
+{
+    WeightLaunch L = {};
+    long long rows = 0;
+    auto flush = [&]() -> hipError_t {
+        if (L.ntasks == 0)
+            return hipSuccess;
+        hipLaunchKernelGGL(k_weight_quantize_batch, dim3((unsigned)((rows + 3) / 4)), dim3(256),
+                           0, stream, L);
+        L = {};
+        rows = 0;
+        return hipGetLastError();
+    };
+    for (int j = 0; j < n; ++j) {
+        const tasq_weight_job &a = jobs[j];
+        if (a.N == 0)
+            continue;
+        const bool vec = (a.K % 4) == 0 && (reinterpret_cast<uintptr_t>(a.W) & 15) == 0 &&
+                         (reinterpret_cast<uintptr_t>(a.W_out) & 3) == 0;
+        L.t[L.ntasks++] = {a.W, a.W_out, a.alpha_out, a.z_out, a.sw_out, rows, a.N, a.K,
+                           vec ? 1 : 0};
+        rows += a.N;
+        if (L.ntasks == kWeightBatchTasks)
+            if (hipError_t e = flush(); e != hipSuccess)
+                return e;
+    }
+    return flush();
+}
+
 hipError_t launch_row_sums(const int8_t *X, int M, int K, int32_t *out, hipStream_t stream)
 {
     const bool vec = (K % 4) == 0 && (reinterpret_cast<uintptr_t>(X) & 3) == 0;
@@ -124,3 +207,39 @@ hipError_t launch_row_sums(const int8_t *X, int M, int K, int32_t *out, hipStrea
 }
 
 }  // namespace tasq
+
+// The batched offline weight quantizer: every job validated as
+// tasq_quantize_weights validates its arguments, before any launch.
+extern "C" int tasq_quantize_weights_batch(const tasq_weight_job *jobs, int n, void *stream)
+{
+    if (n < 0)
+        return TASQ_ERR_RANGE;
+    if (n == 0)
+        return TASQ_OK;
+    if (!jobs)
+        return TASQ_ERR_NULL;
+    std::vector<const float *> bufs;
+    bufs.reserve((size_t)n);
+    for (int j = 0; j < n; ++j) {
+        const tasq_weight_job &a = jobs[j];
+        if (a.N < 0 || a.K < 0 || (a.N > 0 && a.K == 0))
+            return TASQ_ERR_DIM;
+        if (a.K > TASQ_MAX_K)
+            return TASQ_ERR_OVERFLOW;
+        if (a.N == 0)
+            continue;
+        if (!a.W || !a.W_out || !a.alpha_out || !a.z_out || !a.sw_out)
+            return TASQ_ERR_NULL;
+        if ((reinterpret_cast<uintptr_t>(a.W) & 3) || (reinterpret_cast<uintptr_t>(a.alpha_out) & 3) ||
+            (reinterpret_cast<uintptr_t>(a.z_out) & 3) || (reinterpret_cast<uintptr_t>(a.sw_out) & 3))
+            return TASQ_ERR_ALIGN;
+        if ((long long)a.N * a.K >= (1LL << 40))
+            return TASQ_ERR_DIM;
+        bufs.push_back(a.alpha_out);
+    }
+    std::sort(bufs.begin(), bufs.end());
+    if (std::adjacent_find(bufs.begin(), bufs.end()) != bufs.end())
+        return TASQ_ERR_RANGE;
+    hipError_t e = tasq::launch_quantize_weights_batch(jobs, n, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TASQ_OK : TASQ_ERR_HIP;
+}

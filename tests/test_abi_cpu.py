@@ -202,6 +202,42 @@ def test_quantize_activations_batch_rejects():
     assert f(jobs((None, 0, 4, None, None), (None, 5, 0, None, None)), 2, None) == _lib.TASQ_OK
 
 
+def test_quantize_weights_batch_rejects():
+    """Every weight job is validated before anything is enqueued, as the
+    single call validates its arguments; a bad job anywhere fails the call."""
+    f = L.tasq_quantize_weights_batch
+
+    def jobs(*js):
+        arr = (_lib.WeightJob * len(js))()
+        for i, j in enumerate(js):
+            arr[i] = _lib.WeightJob(*j)
+        return arr
+    good = (FAKE, 4, 8, FAKE, FAKE, FAKE, FAKE)
+
+    def job(**kw):
+        names = ["W", "N", "K", "W_out", "alpha_out", "z_out", "sw_out"]
+        v = dict(zip(names, (FAKE, 4, 8, FAKE, FAKE + 8192, FAKE, FAKE)))
+        v.update(kw)
+        return tuple(v[n] for n in names)
+    assert f(None, 0, None) == _lib.TASQ_OK                           # nothing to do
+    assert f(None, 2, None) == _lib.TASQ_ERR_NULL
+    assert f(jobs(good), -1, None) == _lib.TASQ_ERR_RANGE
+    for name in ("W", "W_out", "alpha_out", "z_out", "sw_out"):
+        assert f(jobs(good, job(**{name: None})), 2, None) == _lib.TASQ_ERR_NULL, name
+    assert f(jobs(good, job(N=-1)), 2, None) == _lib.TASQ_ERR_DIM
+    assert f(jobs(good, job(K=-3)), 2, None) == _lib.TASQ_ERR_DIM
+    assert f(jobs(good, job(K=0)), 2, None) == _lib.TASQ_ERR_DIM     # N > 0 with K == 0
+    assert f(jobs(good, job(K=_lib.TASQ_MAX_K + 1)), 2, None) == _lib.TASQ_ERR_OVERFLOW
+    for name in ("W", "alpha_out", "z_out", "sw_out"):
+        bad = job(**{name: FAKE + 8192 + 2})
+        assert f(jobs(good, bad), 2, None) == _lib.TASQ_ERR_ALIGN, name
+    # two jobs sharing one alpha_out buffer
+    assert f(jobs(good, job(alpha_out=FAKE)), 2, None) == _lib.TASQ_ERR_RANGE
+    # empty jobs are skipped, whatever their pointers
+    assert f(jobs((None, 0, 4, None, None, None, None), (None, 0, 0, None, None, None, None)),
+             2, None) == _lib.TASQ_OK
+
+
 def test_lowrank_down_rejects():
     f = L.tasq_lowrank_down
     assert f(FAKE, 4, 4, FAKE, 24, FAKE, None) == _lib.TASQ_ERR_DIM
@@ -386,7 +422,8 @@ def test_struct_layouts_match_header(tmp_path):
     """The ctypes structs mirror tasq_opts and tasq_layer field by field: a C
     program compiled against include/tasq.h prints each field's offset and
     the struct sizes."""
-    structs = {"tasq_opts": Opts, "tasq_layer": Layer, "tasq_act_job": _lib.ActJob}
+    structs = {"tasq_opts": Opts, "tasq_layer": Layer, "tasq_act_job": _lib.ActJob,
+               "tasq_weight_job": _lib.WeightJob}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "tasq.h"', "int main(void){"]
     for cname, py in structs.items():
         lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')

@@ -62,6 +62,34 @@ def test_weight_quantizer_special_rows():
     assert np.array_equal((Q.cpu().numpy().astype(np.int16) + 128).astype(np.uint8), rQ)
 
 
+def test_weight_quantizer_batch_matches_single():
+    """The batched quantizer over 35 weights (three launches of up to 16;
+    ragged K, K not a multiple of 4, a 4-byte-aligned view, an empty weight)
+    gives each weight's single-call codes, alpha, z and sw bit for bit, and
+    the oracle's on a sample."""
+    shapes = [(1, 1), (5, 31), (64, 128), (1152, 1152), (70, 9 * 48), (3, 7000), (0, 16),
+              (4608, 1152), (33, 65), (257, 640)] * 3 + [(9, 10), (2, 2), (1152, 4608), (7, 3),
+                                                          (16, 1)]
+    Ws = [inputs.weights_f32((i * 131 + N * 7 + K) % 30011, N, K).to(DEV)
+          for i, (N, K) in enumerate(shapes)]
+    flat = inputs.weights_f32(5, 6, 65).reshape(-1).to(DEV)
+    Ws[8] = flat[1:1 + 6 * 64].reshape(6, 64)          # not 16-byte aligned: element-wise path
+    got = T.quantize_weights_batch(Ws)
+    torch.cuda.synchronize()
+    assert len(got) == len(Ws)
+    for i, (W, g) in enumerate(zip(Ws, got)):
+        ref = T.quantize_weights(W)
+        torch.cuda.synchronize()
+        assert torch.equal(g[0], ref[0]), f"codes of weight {i} {tuple(W.shape)}"
+        for name, a, r in zip(("alpha", "z", "sw"), g[1:], ref[1:]):
+            assert torch.equal(a.view(torch.int32), r.view(torch.int32)), f"{name} of weight {i}"
+    for i in (1, 8, 9, 33):
+        rQ, ra, rz, rsw = oracle.weight_quant(Ws[i].cpu())
+        Q = (got[i][0].cpu().numpy().astype(np.int16) + 128).astype(np.uint8).reshape(rQ.shape)
+        assert np.array_equal(Q, rQ), f"oracle codes of weight {i}"
+        assert np.array_equal(got[i][1].cpu().numpy().view(np.uint32), ra.view(np.uint32))
+
+
 @pytest.mark.parametrize("M,K", [(1, 1), (7, 13), (300, 1152), (5, 4099)])
 def test_row_sums_bit_exact(M, K):
     X = inputs.random_case(M + K, M, 1, K)[0]
