@@ -86,6 +86,32 @@ def test_fuzz_shapes(case):
         check_outputs(acc, y, ra, ry, sx, sw, use_bias, f"fuzz {M}x{N}x{K} b={b}")
 
 
+@pytest.mark.parametrize("M,N,K", [(3, 33, 131071), (3, 40, 131056), (70, 40, 131071),
+                                   (70, 33, 131056)])
+def test_max_k_extreme_values(M, N, K):
+    """K at TASQ_MAX_K (and the largest multiple of 16 below it): rows of
+    -128 against columns of -128 put acc at 128 * 128 * K, 16384 below
+    2^31 at K = 131071, through the weight-streaming kernels (M = 3), the
+    GEMM (M = 70), the packed buffer and the bit planes, at b = 8 and b = 1
+    (where -128 is kept whole); other rows and columns are random."""
+    X, W, sw, _ = inputs.random_case(1000 + M + N + K % 977, M, N, K)
+    X[0, :] = -128
+    W[0, :] = -128
+    W[1, :] = 127
+    sx = f32(1.0 / 65536)
+    Wd = W.to(DEV)
+    for b in (8, 1):
+        ra, ry = oracle.masked_linear(X, W, sx, sw, b)
+        assert ra[0, 0] == 128 * 128 * K
+        acc, y = gpu_linear(X, W, sx, sw, b)
+        check_outputs(acc, y, ra, ry, sx, sw, None, f"max K {M}x{N}x{K} b={b} rows")
+        acc, y = gpu_linear(X, None, sx, sw, b, packed=T.pack_weights(Wd))
+        check_outputs(acc, y, ra, ry, sx, sw, None, f"max K {M}x{N}x{K} b={b} packed")
+        acc, y = gpu_linear(X, None, sx, sw, b, variant=T.VARIANT_BITPLANE,
+                            planes=T.pack_planes(Wd))
+        check_outputs(acc, y, ra, ry, sx, sw, None, f"max K {M}x{N}x{K} b={b} planes")
+
+
 def test_output_modes():
     M, N, K = 70, 90, 300
     X, W, sw, bias = inputs.random_case(7, M, N, K)
