@@ -186,6 +186,10 @@ hipError_t launch_quantize_weights_batch(const tasq_weight_job *jobs, int n, hip
         const tasq_weight_job &a = jobs[j];
         if (a.N == 0)
             continue;
+        // a launch's grid stays below 2^30 workgroups of 4 rows
+        if (rows + a.N > (1LL << 32))
+            if (hipError_t e = flush(); e != hipSuccess)
+                return e;
         const bool vec = (a.K % 4) == 0 && (reinterpret_cast<uintptr_t>(a.W) & 15) == 0 &&
                          (reinterpret_cast<uintptr_t>(a.W_out) & 3) == 0;
         L.t[L.ntasks++] = {a.W, a.W_out, a.alpha_out, a.z_out, a.sw_out, rows, a.N, a.K,
