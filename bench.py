@@ -151,6 +151,41 @@ def time_schedule(layers, table, wl, ws, steps, warmup):
     return start.elapsed_time(end) / steps
 
 
+def shard_shapes(wl, table, keep, full_ms, device, parts=8, steps=3, warmup=1):
+    """The step on one GPU's share of a ``parts``-way split (shard 0), at its
+    real shapes: the first M/parts token rows of every layer (W replicated),
+    or its first N/parts output channels (W, sw and outputs split).  Neither
+    split exchanges anything between GPUs, so a shard's step time is the
+    split step's time.  The shard's operands are views of the full
+    workload's device tensors (row-major weights); its outputs are fresh."""
+    out = {"parts": parts}
+    for axis, key in (("M", "token_split"), ("N", "channel_split")):
+        swl = inputs.shard(wl, axis, parts)
+        layers, ys = [], []
+        for l, spec in enumerate(swl.layers):
+            X, W, sw, _ = keep[l]
+            if axis == "M":
+                X = X[:spec.M]
+            else:
+                W, sw = W[:spec.N], sw[:spec.N]
+            y = torch.empty((spec.M, spec.N), dtype=torch.float32, device=device)
+            ys.append(y)
+            layers.append(T.make_layer(X, W, swl.sx, sw, None, None, y))
+        ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=device)
+        ms = time_schedule(layers, table, swl, ws, steps, warmup)
+        out[key] = {
+            "shapes": sorted({(sp.M, sp.K, sp.N) for sp in swl.layers}),
+            "ms_per_schedule": round(ms, 4),
+            "ms_per_denoising_step": round(ms / swl.T, 4),
+            "TOPS": round(gemm_ops(swl) * swl.T / (ms * 1e-3) / 1e12, 1),
+            # the full step's time over `parts` against the shard's
+            "split_efficiency": round(full_ms / parts / ms, 4),
+        }
+        del layers, ys, ws
+        torch.cuda.empty_cache()
+    return out
+
+
 def measured_peaks(device, blocks=768, iters=40000, copy_reps=5):
     """What the GPU sustains, measured here rather than taken from the
     datasheet: the int8 matrix-instruction rate with no memory traffic
@@ -684,6 +719,9 @@ def main():
                          "its JSON")
     ap.add_argument("--no-skinny", action="store_true",
                     help="skip the extra weight-streaming (M=16) schedule measurement")
+    ap.add_argument("--shard-shapes", action="store_true",
+                    help="only the step at one GPU's share of the 8-way token and channel "
+                         "splits (one JSON line)")
     ap.add_argument("--no-act", action="store_true",
                     help="skip the extra asymmetric-activation (fp32 input) measurement")
     ap.add_argument("--per-layer", action="store_true",
@@ -714,6 +752,19 @@ def main():
             print(json.dumps(row), flush=True)
         for row in config_schedules("cuda"):
             print(json.dumps(row), flush=True)
+        return
+    if args.shard_shapes:
+        wl = inputs.workload(4)
+        table = inputs.b_table(wl)
+        log("building the full step and timing it")
+        layers, keep = build_workload(wl, "cuda", packed=False)
+        ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device="cuda")
+        full_ms = time_schedule(layers, table, wl, ws, 3, 1)
+        log("timing one GPU's share of the 8-way token and channel splits")
+        row = {"workload": wl.name, "full_ms_per_schedule": round(full_ms, 4),
+               "full_ms_per_denoising_step": round(full_ms / wl.T, 4)}
+        row.update(shard_shapes(wl, table, keep, full_ms, "cuda"))
+        print(json.dumps(row), flush=True)
         return
     if args.skinny_sweep:
         for row in skinny_sweep("cuda"):

@@ -194,6 +194,29 @@ def workload(i: int, M_override: Optional[int] = None) -> Workload:
     raise ValueError(f"no workload {i}")
 
 
+def shard(wl: Workload, axis: str, parts: int) -> Workload:
+    """Shard 0 of a ``parts``-way split of every layer of ``wl``.
+
+    ``axis`` "M" keeps the first ceil(M / parts) token rows (X and the
+    outputs split, W replicated); "N" keeps the first ceil(N / parts) output
+    channels (W, sw and the outputs split, X replicated).  Neither split
+    needs an exchange between shards, and b stays per layer.  The seed is
+    kept, and every draw is counter-based, so the shard's tensors are
+    exactly those rows or channels of the full workload's tensors.
+    Convolutions are not split."""
+    if axis not in ("M", "N") or parts < 1:
+        raise ValueError("axis is 'M' or 'N', parts >= 1")
+    layers = []
+    for spec in wl.layers:
+        if spec.kind != "linear":
+            raise ValueError("only linear layers are split")
+        if axis == "M":
+            layers.append(dataclasses.replace(spec, M=-(-spec.M // parts)))
+        else:
+            layers.append(dataclasses.replace(spec, N=-(-spec.N // parts)))
+    return dataclasses.replace(wl, name=f"{wl.name}_{axis}{parts}", layers=layers)
+
+
 # tensor ids within a workload's seed
 def tid_x(l): return 2 * l
 def tid_w(l): return 2 * l + 1

@@ -55,3 +55,27 @@ def test_cpu_baseline_reports_one_and_all_threads():
         assert len(v["TOPS_runs"]) == 3 and v["TOPS_median"] > 0
     assert r["value"] == r["all_threads_TOPS"]
     assert r["nproc"] >= 1
+
+
+def test_shard_workloads_are_rows_and_channels_of_the_full_one():
+    """inputs.shard keeps the seed: shard 0 of the token split draws the first
+    rows of every X, shard 0 of the channel split the first channels of every
+    W and sw, and both keep the b table; other axes and convs are refused."""
+    import torch
+    wl = inputs.workload(4)
+    m8, n8 = inputs.shard(wl, "M", 8), inputs.shard(wl, "N", 8)
+    assert [s.M for s in m8.layers[:4]] == [1024] * 4
+    assert [s.N for s in n8.layers[:4]] == [432, 144, 576, 144]
+    assert all(a.K == b.K == c.K for a, b, c in zip(wl.layers, m8.layers, n8.layers))
+    rows = torch.arange(7)
+    for l in (0, 3, 110):
+        assert torch.equal(inputs.x_rows(m8, l, rows), inputs.x_rows(wl, l, rows))
+        assert torch.equal(inputs.w_rows(n8, l, rows), inputs.w_rows(wl, l, rows))
+        assert torch.equal(inputs.sw_full(n8, l), inputs.sw_full(wl, l)[:n8.layers[l].N])
+    assert torch.equal(inputs.b_table(m8), inputs.b_table(wl))
+    assert torch.equal(inputs.b_table(n8), inputs.b_table(wl))
+    with pytest.raises(ValueError):
+        inputs.shard(wl, "K", 8)
+    with pytest.raises(ValueError):
+        inputs.shard(inputs.workload(3), "N", 8)
+

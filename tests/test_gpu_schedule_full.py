@@ -184,6 +184,41 @@ def test_config4_weight_streaming_schedule_m16_sampled(cfg4, source):
                       f"config 4 at 16 tokens, {source}, layer {l} b={b}")
 
 
+@pytest.mark.parametrize("axis", ["M", "N"])
+def test_config4_shard_schedules_sampled(cfg4, axis):
+    """One GPU's share of an 8-way split of config 4 at its real shapes, as
+    bench.py --shard-shapes times it: shard 0 of the token split (the first
+    1024 rows of every layer) or of the channel split (the first N/8 output
+    channels: 432, 144, 576, 144 per block), operands as views of the full
+    device tensors, all 20 denoising steps through the bench's launch.
+    Sampled outputs of the layers of blocks 0, 9, 18 and 27 against the
+    oracle, fp32 within 1e-6 relative."""
+    wl, table, Ws, sws, keep = cfg4
+    swl = inputs.shard(wl, axis, 8)
+    layers, ys = [], []
+    for l, spec in enumerate(swl.layers):
+        X, Wd, swd = keep[l]
+        if axis == "M":
+            X = X[:spec.M]
+        else:
+            Wd, swd = Wd[:spec.N], swd[:spec.N]
+        y = torch.full((spec.M, spec.N), -7.0, dtype=torch.float32, device=DEV)
+        layers.append(T.make_layer(X, Wd, swl.sx, swd, None, None, y))
+        ys.append(y)
+    ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
+    T.run_schedule(layers, table, swl.S, swl.T, 0, swl.T, workspace=ws)
+    torch.cuda.synchronize()
+    stage = oracle.stage_of_step(swl.T - 1, swl.S, swl.T)
+    rng = np.random.default_rng(45)
+    for blk in (0, 9, 18, 27):
+        for l in range(4 * blk, 4 * blk + 4):
+            spec = swl.layers[l]
+            W = Ws[l] if axis == "M" else Ws[l][:spec.N]
+            sw = sws[l] if axis == "M" else sws[l][:spec.N]
+            check_layer(swl, l, W, sw, ys[l], None, int(table[l, stage]), rng,
+                        f"config 4 shard 0 of 8 along {axis}, layer {l}")
+
+
 @pytest.mark.parametrize("cfg", [1, 2, 3])
 def test_block_schedules_full_size_sampled(cfg):
     """Configs 1-3 as full-size schedules through tasq_run_schedule with a
