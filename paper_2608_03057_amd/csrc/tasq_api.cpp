@@ -1059,22 +1059,34 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
             below8 = below8 || b_table[(size_t)l * S + s] < 8;
         wsrc[l] = weight_source(descs[l], opts, below8, true);
     }
+    // Only layers with a product to compute (M, N and K all positive) take
+    // part in a grouped launch and decide its form; a layer with outputs
+    // but K = 0 writes its bias (or zero) through the single-layer launcher
+    // each step, and a layer without outputs has nothing to do.
+    auto multiplies = [](const LayerDesc &d) { return d.M > 0 && d.N > 0 && d.K > 0; };
     tasq::SkinnyWeights src = tasq::SKINNY_ROWS;
     bool all_skinny = have_ws;
+    bool seen = false;
     int max_m = 0;
     for (int l = 0; all_skinny && l < L; ++l) {
+        if (!multiplies(descs[l]))
+            continue;
         tasq::SkinnyWeights sl;
-        all_skinny = skinny_source(descs[l], wsrc[l], sl) && (l == 0 || sl == src);
+        all_skinny = skinny_source(descs[l], wsrc[l], sl) && (!seen || sl == src);
         src = sl;
+        seen = true;
         max_m = descs[l].M > max_m ? descs[l].M : max_m;
     }
     bool all_packed = true;
     for (int l = 0; l < L; ++l)
-        all_packed = all_packed && wsrc[l] == SRC_PACKED && packed_fits(descs[l]);
+        all_packed = all_packed && (!multiplies(descs[l]) ||
+                                    (wsrc[l] == SRC_PACKED && packed_fits(descs[l])));
     const int v = variant_of_opts(opts);
     bool grouped = have_ws && v != TASQ_VARIANT_BITPLANE;
     for (int l = 0; grouped && l < L; ++l) {
         const LayerDesc &d = descs[l];
+        if (!multiplies(d))
+            continue;
         const bool staged = v != TASQ_VARIANT_PACKED && wsrc[l] != SRC_PLANES && d.W &&
                             aligned16(d.W);
         grouped = x_aligned(d) && (all_packed || staged);
@@ -1091,22 +1103,32 @@ static int run_schedule_impl(const tasq_layer *layers, int L, const uint8_t *b_t
         // every layer (SDXL-Turbo-shaped block: 174.5 us per step grouped,
         // 99.1 + 39.1 us split this way).
         std::vector<LayerDesc> solo;
+        {
+            std::vector<LayerDesc> rest;
+            for (const LayerDesc &d : descs) {
+                if (multiplies(d))
+                    rest.push_back(d);
+                else if (d.M > 0 && d.N > 0)
+                    solo.push_back(d);
+            }
+            descs.swap(rest);
+        }
         if (!all_skinny && !all_packed) {
             double ops = 0;
             for (const LayerDesc &d : descs)
                 ops += 2.0 * d.M * (double)d.N * d.K;
-            std::vector<LayerDesc> rest;
+            std::vector<LayerDesc> rest, split;
             for (const LayerDesc &d : descs) {
                 const bool long_tile = 2.0 * 256 * 256 * (double)d.K > ops / kComputeUnits;
                 if (long_tile && auto_splits(d.M, d.N, d.K) > 1)
-                    solo.push_back(d);
+                    split.push_back(d);
                 else
                     rest.push_back(d);
             }
-            if (rest.empty())
-                solo.clear();
-            else if (!solo.empty())
+            if (!rest.empty() && !split.empty()) {
                 descs.swap(rest);
+                solo.insert(solo.end(), split.begin(), split.end());
+            }
         }
         // Weight streaming: the workgroups of the deepest layers first.  A
         // workgroup streams all of its layer's K, so the 4608-deep layers'

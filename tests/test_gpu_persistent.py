@@ -78,6 +78,41 @@ def test_persistent_schedule(tile, wgs, parties):
                               f"b={b}")
 
 
+@pytest.mark.parametrize("tune", [dict(persistent=2, persistent_wgs=3, tile=1),
+                                  dict(persistent=1), None])
+def test_schedule_with_empty_and_k0_layers(tune):
+    """Layers without a product inside a grouped schedule: one with outputs
+    but K = 0 (with a non-null weight pointer, as a C-ABI caller may pass
+    one) writes its bias and zero accumulators, layers with M = 0 or N = 0
+    write nothing, and the layers around them match the oracle, through the
+    persistent launch, the one-workgroup-per-tile grouped launch and AUTO."""
+    dummy = torch.zeros(4096, dtype=torch.int8, device=DEV)          # never read
+    shapes = [(300, 200, 304), (40, 70, 0), (0, 64, 128), (33, 0, 32), (300, 70, 0),
+              (520, 260, 1152)]
+    host, layers, keep = [], [], []
+    for i, (M, N, K) in enumerate(shapes):
+        X, W, sw, bias = inputs.random_case(300 + i, M, N, K)
+        Xd, Wd, swd, bd = X.to(DEV), W.to(DEV), sw.to(DEV), bias.to(DEV)
+        acc = torch.full((M, N), 12345, dtype=torch.int32, device=DEV)
+        y = torch.full((M, N), -7.0, dtype=torch.float32, device=DEV)
+        ly = T.make_layer(Xd, Wd, SX, swd, bd, acc, y)
+        if K == 0:
+            ly.W = dummy.data_ptr()
+        layers.append(ly)
+        keep.append((Xd, Wd, swd, bd))
+        host.append((X, W, sw, bias, acc, y))
+    table = torch.tensor([[3, 8], [5, 1], [8, 8], [2, 4], [6, 2], [7, 6]], dtype=torch.uint8)
+    ws = torch.empty(T.schedule_workspace_bytes(layers), dtype=torch.uint8, device=DEV)
+    T.run_schedule(layers, table, 2, 4, 0, 4, workspace=ws, tune=tune)
+    torch.cuda.synchronize()
+    stage = oracle.stage_of_step(3, 2, 4)
+    for i, (X, W, sw, bias, acc, y) in enumerate(host):
+        b = int(table[i, stage])
+        ra, ry = oracle.masked_linear(X, W, SX, sw, b, bias)
+        check_outputs(acc, y, ra, ry, SX, sw, bias, f"layer {i} {tuple(X.shape)}x{W.shape[0]} "
+                                                     f"b={b} tune={tune}")
+
+
 def test_persistent_matches_grouped():
     """The persistent step (forced on) and the non-persistent grouped launch
     (forced off) write identical outputs at the 256x256 tile."""
