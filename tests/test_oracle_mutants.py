@@ -7,7 +7,10 @@ squares a scale or pairs a row with the wrong channel, a stage map off by
 one, an activation quantiser that rounds ties away from zero or flips the
 zero point, a weight quantiser without the 2^n / (2^n - 1) factor, an
 asymmetric layer that ignores its zero point, a convolution with flipped
-taps, a bf16 conversion that truncates.  It then runs the pins written for
+taps, a bf16 conversion that truncates, a low-rank branch on unrounded
+inputs or with its rank components out of order, bit planes stored least
+significant first, packed weights with their bytes reversed, channel sums
+of the unmasked weights.  It then runs the pins written for
 that function and asserts that at least one of them fails.  A pin set that
 let such a mistake through would not pin the oracle."""
 import numpy as np
@@ -18,7 +21,8 @@ import test_oracle_pins as pins
 
 REAL = {name: getattr(oracle, name) for name in
         ("mask", "masked_linear", "stage_of_step", "act_quant", "weight_quant",
-         "masked_linear_asym", "conv3x3", "bf16_round")}
+         "masked_linear_asym", "conv3x3", "bf16_round", "lowrank", "pack_planes",
+         "pack_weights", "weight_colsums")}
 
 
 def failures(checks):
@@ -134,6 +138,33 @@ def _bf16_truncate(x):
     return (np.asarray(x, np.float32).view(np.uint32) >> 16).astype(np.uint16)
 
 
+def _lowrank_unrounded_input(x, down, up):
+    """The fp32 input used as it is instead of rounded to bfloat16."""
+    D, U = oracle.bf16_value(down), oracle.bf16_value(up)
+    T = np.asarray(x, np.float32).astype(np.float64) @ D.T
+    return T, T @ U.T
+
+
+def _lowrank_rank_order_reversed(x, down, up):
+    T, lr = REAL["lowrank"](x, down, up)
+    U = oracle.bf16_value(up)
+    return T, T @ U[:, ::-1].T
+
+
+def _planes_lsb_first(W):
+    return np.ascontiguousarray(REAL["pack_planes"](W)[:, ::-1])
+
+
+def _packed_chunk_bytes_reversed(W):
+    P = np.asarray(REAL["pack_weights"](W))
+    return np.ascontiguousarray(P.reshape(-1, 16)[:, ::-1]).reshape(P.shape)
+
+
+def _colsums_unmasked(W):
+    cs = REAL["weight_colsums"](W)
+    return np.repeat(cs[7:8], cs.shape[0], axis=0)
+
+
 # --------------------------------------------------------------- pin groups
 
 MASK_PINS = ([(pins.test_mask_exhaustive_vs_unsigned_codes, (b,)) for b in range(1, 9)] +
@@ -168,6 +199,20 @@ CONV_PINS = ([(pins.test_conv_direct_vs_im2col, s)
 BF16_PINS = ([(pins.test_bf16_round_worked_values, xb) for xb in pins.BF16_WORKED] +
              [(pins.test_bf16_round_matches_torch_rne, ())])
 
+LOWRANK_PINS = [(pins.test_lowrank_exact_rational_tiny, ()), (pins.test_lowrank_merged_weight, ()),
+                (pins.test_lowrank_one_hot, ()), (pins.test_lowrank_entries_match_full, ())]
+
+PLANES_PINS = ([(pins.test_planes_bit_position_worked_example, ())] +
+               [(pins.test_planes_round_trip, s)
+                for s in [(1, 1), (5, 31), (7, 32), (3, 100), (4, 300), (40, 200)]] +
+               [(pins.test_bit_plane_identity, (b,)) for b in range(1, 9)])
+
+PACKED_PINS = ([(pins.test_packed_weights_worked_positions, ())] +
+               [(pins.test_packed_weights_round_trip, s)
+                for s in [(1, 1), (5, 31), (32, 128), (33, 129), (70, 300)]])
+
+COLSUM_PINS = [(pins.test_weight_colsums, ())]
+
 CASES = [
     ("mask", _mask_extra_bit, MASK_PINS),
     ("mask", _mask_magnitude, MASK_PINS),
@@ -188,13 +233,18 @@ CASES = [
     ("masked_linear_asym", _asym_unsigned_acc, ASYM_PINS),
     ("conv3x3", _conv_flipped_taps, CONV_PINS),
     ("bf16_round", _bf16_truncate, BF16_PINS),
+    ("lowrank", _lowrank_unrounded_input, LOWRANK_PINS),
+    ("lowrank", _lowrank_rank_order_reversed, LOWRANK_PINS),
+    ("pack_planes", _planes_lsb_first, PLANES_PINS),
+    ("pack_weights", _packed_chunk_bytes_reversed, PACKED_PINS),
+    ("weight_colsums", _colsums_unmasked, COLSUM_PINS),
 ]
 
 
 def test_pins_pass_on_the_real_oracle():
     """Every pin group passes unmodified (so a failure below is the mutant's)."""
     for group in (MASK_PINS, LINEAR_PINS, STAGE_PINS, ACT_PINS, WQ_PINS, ASYM_PINS, CONV_PINS,
-                  BF16_PINS):
+                  BF16_PINS, LOWRANK_PINS, PLANES_PINS, PACKED_PINS, COLSUM_PINS):
         assert failures(group) == 0
 
 
