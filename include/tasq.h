@@ -500,7 +500,10 @@ typedef struct tasq_layer {
  * the step and which split-K would cut (a long K on few tiles, e.g. a 3x3
  * conv over 32x32 pixels) is launched on its own each step, split-K over the
  * partials room of the workspace, ahead of the grouped launch over the
- * other layers.  The whole table and every layer are validated before
+ * other layers.  A layer with M == 0 or N == 0 does nothing, and a layer
+ * with K == 0 (acc = 0, y = bias or 0, as tasq_masked_linear) is launched
+ * on its own each step; neither takes part in, or decides the form of, the
+ * grouped launch.  The whole table and every layer are validated before
  * anything is enqueued.
  */
 int tasq_run_schedule(const tasq_layer *layers, int L, const uint8_t *b_table, int S, int T,
