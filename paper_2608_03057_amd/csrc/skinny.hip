@@ -107,7 +107,8 @@ __device__ __forceinline__ void skinny_stream(const LayerDesc &d, int b, int nb,
 
     // One K block's operands: every load of the block is issued before any
     // is used.  Latency is covered by the other waves of the CU (8 per SIMD
-    // with one token tile) rather than by a second buffer.
+    // with one token tile) rather than by a second buffer, except in the
+    // grouped packed stream (below).
     struct Block {
         v2i pw[8];
         v4i w[2][2];
