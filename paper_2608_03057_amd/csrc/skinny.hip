@@ -53,6 +53,14 @@ enum SkinnySource : int { SRC_ROWS = 0, SRC_PACKED = 1, SRC_PLANES = 2 };
 // plane and block, and a workgroup's top b planes are one contiguous run.
 // Register v of accumulator (f, mt) of lane l is channel n0 + 16 f +
 // 4 (l / 16) + v, token 16 mt + l % 16.
+// Packed weights are read once per step in whole 16-byte MFMA fragments:
+// non-temporal loads (about 3.5% shorter step at 16 tokens; the row and
+// plane streams measured slower with them).
+__device__ __forceinline__ v4i ld16_nt(rsrc_t r, uint32_t off)
+{
+    return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
+}
+
 template <int SRC, int MT, int BP, int W>
 __device__ __forceinline__ void skinny_stream(const LayerDesc &d, int b, int nb, int *red)
 {
@@ -130,7 +138,7 @@ __device__ __forceinline__ void skinny_stream(const LayerDesc &d, int b, int nb,
 #pragma unroll
                 for (int t = 0; t < 2; ++t) {
                     if constexpr (SRC == SRC_PACKED)
-                        bl.w[f][t] = ld16(rW, offW[f] + (uint32_t)(4 * kb + t) * 1024u);
+                        bl.w[f][t] = ld16_nt(rW, offW[f] + (uint32_t)(4 * kb + t) * 1024u);
                     else
                         bl.w[f][t] = ld16(rW, offW[f] + k0 + 32u * t);
                 }
